@@ -1,0 +1,35 @@
+"""CPU oracle for the AdaptiveSpec verification path. TEST INFRASTRUCTURE ONLY.
+
+Plain, slow, float64 implementation of what the verification path computes, written from the
+paper ("Margins, Not Windows: Training-Free Per-Step Lossy Speculative Decoding"): the target
+LM-head logits of every draft-tree row, the per-row max / argmax / log-sum-exp, the margin rule
+of Sec. 3.2 Eq. (1), the tree walk that promotes mismatches, the draft top-1 confidence of
+Sec. 3.3 Eq. (2) and the rolling acceptance history of Sec. 3.3.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of ``bench.py`` may
+import it. It shares no code with the HIP path (``paper_2609_02897_amd``); both read inputs from
+``workloads`` only.
+
+Parity pins live in ``tests/test_oracle_pins.py``. Functions whose result the paper does not fix
+are marked "parity unpinned" in their docstrings (the walk's sibling choice, the promotion
+count, the acceptance observation, the history reset on a breaker trip).
+"""
+
+from .asv_oracle import (  # noqa: F401
+    LN_BAND,
+    Params,
+    ReqState,
+    accept_flags,
+    draft_confidence,
+    drafted_logits,
+    logits,
+    row_stats,
+    row_top8,
+    state_init,
+    state_update,
+    verify,
+    walk,
+    walk_bands,
+    widen_bf16,
+    widen_weights,
+)
