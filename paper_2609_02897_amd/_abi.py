@@ -1,0 +1,79 @@
+"""ctypes mirror of include/asv.h and the loader of libasv.so (argument marshalling only)."""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libasv.so")
+
+ASV_OK, ASV_EINVAL, ASV_EWORKSPACE, ASV_EHIP = 0, -1, -2, -3
+RS_BAD_ROOT, RS_BAD_PARENT, RS_BAD_TOKEN, RS_BAD_OFFSETS, RS_BAD_TAU = 1, 2, 4, 16, 32
+HIST_WINDOW = 16
+
+# Every entry point include/asv.h declares.
+EXPORTS = ("asv_version", "asv_status_string", "asv_workspace_bytes", "asv_state_init",
+           "asv_verify")
+
+
+class AsvReqState(ctypes.Structure):
+    _fields_ = [("rar", ctypes.c_float), ("hist", ctypes.c_float * HIST_WINDOW),
+                ("hist_head", ctypes.c_int32), ("hist_count", ctypes.c_int32),
+                ("zero_streak", ctypes.c_int32), ("breaker", ctypes.c_int32),
+                ("steps", ctypes.c_int32), ("hist_mean", ctypes.c_float),
+                ("draft_conf", ctypes.c_float)]
+
+
+class AsvParams(ctypes.Structure):
+    _fields_ = [("alpha", ctypes.c_float), ("rar0", ctypes.c_float),
+                ("breaker_n", ctypes.c_int32), ("max_promotions", ctypes.c_int32)]
+
+
+_P = ctypes.c_void_p
+
+
+class AsvVerifyArgs(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("N", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("V", ctypes.c_int32),
+                ("hidden", _P), ("w_lm", _P), ("draft_tok", _P), ("parent", _P),
+                ("req_offsets", _P), ("tau", _P), ("draft_logits", _P),
+                ("row_max", _P), ("row_lse", _P), ("row_argmax", _P),
+                ("drafted_logit", _P), ("accept", _P),
+                ("accepted_len", _P), ("bonus_token", _P), ("accepted_path", _P),
+                ("draft_conf", _P), ("state", _P), ("req_status", _P),
+                ("params", AsvParams),
+                ("k1_begin_event", _P), ("k1_end_event", _P)]
+
+
+assert ctypes.sizeof(AsvReqState) == 96
+
+
+class LibraryMissing(RuntimeError):
+    pass
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libasv.so (built in-tree by ``__graft_entry__.build()``); raise if it is absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise LibraryMissing(
+            f"{path} is not built; run `python -c 'import __graft_entry__ as g; g.build()'`")
+    lib = ctypes.CDLL(path)
+    lib.asv_version.restype = ctypes.c_int
+    lib.asv_version.argtypes = []
+    lib.asv_status_string.restype = ctypes.c_char_p
+    lib.asv_status_string.argtypes = [ctypes.c_int]
+    lib.asv_workspace_bytes.restype = ctypes.c_int
+    lib.asv_workspace_bytes.argtypes = [ctypes.c_int32] * 4 + [ctypes.POINTER(ctypes.c_uint64)]
+    lib.asv_state_init.restype = ctypes.c_int
+    lib.asv_state_init.argtypes = [_P, ctypes.c_int32, ctypes.POINTER(AsvParams), _P]
+    lib.asv_verify.restype = ctypes.c_int
+    lib.asv_verify.argtypes = [ctypes.POINTER(AsvVerifyArgs), _P, ctypes.c_uint64, _P]
+    _lib = lib
+    return lib

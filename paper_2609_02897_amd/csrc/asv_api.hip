@@ -1,0 +1,163 @@
+// Host side of libasv: argument checks, workspace layout, tile selection and the launch
+// sequence of one verification step. Every entry point is declared in include/asv.h.
+#include <hip/hip_runtime.h>
+
+#include "asv.h"
+#include "k_accept.h"
+#include "k_lmhead.h"
+#include "k_reduce.h"
+
+namespace asv {
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Tile families of K1, chosen from the number of tree rows. Few rows (the weight-streaming
+// regime of small batches) use a 64- or 128-row tile so that all rows share one pass over W;
+// many rows (large batch x nodes, MFMA-bound) use 256x256 tiles.
+enum class Tile { kRows64, kRows128, kRows256 };
+
+Tile pick_tile(int N) {
+  if (N <= 64) return Tile::kRows64;
+  if (N <= 128) return Tile::kRows128;
+  return Tile::kRows256;
+}
+
+int tile_rows(Tile t) { return t == Tile::kRows64 ? 64 : t == Tile::kRows128 ? 128 : 256; }
+
+struct Layout {
+  int S = 0;       // vocabulary slabs
+  int n_conf = 0;  // draft-confidence chunks per request
+  size_t off_rec_m = 0, off_rec_s = 0, off_rec_a = 0, off_conf_m = 0, off_conf_s = 0;
+  size_t bytes = 0;
+};
+
+Layout layout(int B, int N, int V) {
+  Layout L;
+  L.S = (V + kSlab - 1) / kSlab;
+  L.n_conf = (V + kConfChunk - 1) / kConfChunk;
+  const size_t rec = (size_t)N * L.S * 4;
+  const size_t conf = (size_t)B * L.n_conf * 4;
+  size_t at = 0;
+  L.off_rec_m = at;  at += align_up(rec);
+  L.off_rec_s = at;  at += align_up(rec);
+  L.off_rec_a = at;  at += align_up(rec);
+  L.off_conf_m = at; at += align_up(conf);
+  L.off_conf_s = at; at += align_up(conf);
+  L.bytes = at;
+  return L;
+}
+
+bool sizes_ok(int B, int N, int H, int V) {
+  if (B < 0 || N < 0 || H <= 0 || V <= 0) return false;
+  if ((B == 0) != (N == 0) || N < B) return false;
+  if (H % kBK != 0) return false;
+  return true;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+template <int TV, int TR, int WV, int WR>
+void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStream_t s) {
+  const int RT = (a->N + TR - 1) / TR;
+  const int grid = L.S * RT;
+  k_lmhead_partial<TV, TR, WV, WR><<<grid, WV * WR * kWave, 0, s>>>(
+      a->hidden, a->w_lm, a->parent, a->draft_tok, a->req_offsets, a->B, a->N, a->H, a->V,
+      L.S, RT, reinterpret_cast<float*>(ws + L.off_rec_m),
+      reinterpret_cast<float*>(ws + L.off_rec_s), reinterpret_cast<int32_t*>(ws + L.off_rec_a),
+      a->drafted_logit);
+}
+
+}  // namespace
+}  // namespace asv
+
+using namespace asv;
+
+extern "C" int asv_version(void) { return ASV_VERSION; }
+
+extern "C" const char* asv_status_string(int code) {
+  switch (code) {
+    case ASV_OK: return "ok";
+    case ASV_EINVAL: return "invalid argument (size, null or misaligned pointer, parameter)";
+    case ASV_EWORKSPACE: return "workspace too small or not 256-byte aligned";
+    case ASV_EHIP: return "HIP runtime error or kernel launch failure";
+    default: return "unknown asv status code";
+  }
+}
+
+extern "C" int asv_workspace_bytes(int32_t B, int32_t N, int32_t H, int32_t V,
+                                   uint64_t* bytes) {
+  if (!bytes || !sizes_ok(B, N, H, V)) return ASV_EINVAL;
+  *bytes = layout(B, N, V).bytes;
+  return ASV_OK;
+}
+
+extern "C" int asv_state_init(asv_req_state* state, int32_t B, const asv_params* p,
+                              void* stream) {
+  if (B < 0 || !p || (B > 0 && !state)) return ASV_EINVAL;
+  if (B == 0) return ASV_OK;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  k_state_init<<<(B + 255) / 256, 256, 0, s>>>(state, B, *p);
+  return hipGetLastError() == hipSuccess ? ASV_OK : ASV_EHIP;
+}
+
+extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t workspace_bytes,
+                          void* stream) {
+  if (!a || !sizes_ok(a->B, a->N, a->H, a->V)) return ASV_EINVAL;
+  if (a->B == 0) return ASV_OK;
+  if (!a->hidden || !a->w_lm || !a->draft_tok || !a->parent || !a->req_offsets || !a->tau ||
+      !a->row_max || !a->row_lse || !a->row_argmax || !a->drafted_logit || !a->accept ||
+      !a->accepted_len || !a->bonus_token || !a->accepted_path || !a->req_status)
+    return ASV_EINVAL;
+  if (!aligned16(a->hidden) || !aligned16(a->w_lm)) return ASV_EINVAL;
+  const asv_params& p = a->params;
+  if (!(p.alpha > 0.f && p.alpha <= 1.f) || p.breaker_n < 1 || p.max_promotions < -1)
+    return ASV_EINVAL;
+  const Layout L = layout(a->B, a->N, a->V);
+  if (!workspace || workspace_bytes < L.bytes ||
+      (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return ASV_EWORKSPACE;
+
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  const bool conf = a->draft_logits != nullptr;
+  (void)hipGetLastError();
+
+  // K4 first: it only needs the inputs and overlaps nothing it depends on.
+  if (conf) {
+    k_draft_conf_partial<<<dim3(L.n_conf, a->B), kConfThreads, 0, s>>>(
+        a->N, a->V, a->req_offsets, a->draft_logits, reinterpret_cast<float*>(ws + L.off_conf_m),
+        reinterpret_cast<float*>(ws + L.off_conf_s));
+  }
+
+  if (a->k1_begin_event) {
+    if (hipEventRecord(reinterpret_cast<hipEvent_t>(a->k1_begin_event), s) != hipSuccess)
+      return ASV_EHIP;
+  }
+  switch (pick_tile(a->N)) {
+    case Tile::kRows64: launch_lmhead<256, 64, 4, 1>(a, L, ws, s); break;
+    case Tile::kRows128: launch_lmhead<256, 128, 2, 2>(a, L, ws, s); break;
+    case Tile::kRows256: launch_lmhead<256, 256, 2, 2>(a, L, ws, s); break;
+  }
+  if (a->k1_end_event) {
+    if (hipEventRecord(reinterpret_cast<hipEvent_t>(a->k1_end_event), s) != hipSuccess)
+      return ASV_EHIP;
+  }
+
+  k_slab_merge<<<(a->N + kMergeRowsPerBlock - 1) / kMergeRowsPerBlock,
+                 kMergeRowsPerBlock * kWave, 0, s>>>(
+      a->N, L.S, reinterpret_cast<const float*>(ws + L.off_rec_m),
+      reinterpret_cast<const float*>(ws + L.off_rec_s),
+      reinterpret_cast<const int32_t*>(ws + L.off_rec_a), a->row_max, a->row_lse, a->row_argmax);
+
+  k_tree_accept<<<a->B, kWave, 0, s>>>(
+      a->B, a->N, a->V, a->req_offsets, a->parent, a->draft_tok, a->tau, a->row_max,
+      a->row_argmax, a->drafted_logit, a->accept, a->accepted_len, a->bonus_token,
+      a->accepted_path, reinterpret_cast<const float*>(ws + L.off_conf_m),
+      reinterpret_cast<const float*>(ws + L.off_conf_s), conf ? L.n_conf : 0, a->draft_conf,
+      a->state, a->req_status, a->params);
+
+  return hipGetLastError() == hipSuccess ? ASV_OK : ASV_EHIP;
+}

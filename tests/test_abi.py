@@ -1,0 +1,102 @@
+"""The C-ABI library: it loads, exports every entry point of include/asv.h, and rejects bad
+arguments on the host before touching the GPU (these calls run without a GPU)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_02897_amd as asv
+from paper_2609_02897_amd import _abi, _build
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not _build.is_built():
+        _build.build_library()
+    return asv.load()
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "asv.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(asv_[a-z_]+)\s*\(", src)))
+
+
+def test_header_matches_binding():
+    assert _declared_functions() == sorted(_abi.EXPORTS)
+
+
+def test_exports(lib):
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+
+
+def test_version_and_status(lib):
+    assert lib.asv_version() == 100
+    for code in (0, -1, -2, -3, 7):
+        assert lib.asv_status_string(code)
+
+
+def test_struct_layouts():
+    assert ctypes.sizeof(_abi.AsvReqState) == 96
+    assert ctypes.sizeof(_abi.AsvParams) == 16
+    # 4 ints, 18 pointers, params (16 B), 2 event pointers
+    assert ctypes.sizeof(_abi.AsvVerifyArgs) == 16 + 18 * 8 + 16 + 2 * 8
+
+
+def test_workspace_bytes(lib):
+    out = ctypes.c_uint64(0)
+    assert lib.asv_workspace_bytes(1, 60, 4096, 128256, ctypes.byref(out)) == 0
+    S = (128256 + 255) // 256
+    assert out.value >= 3 * 60 * S * 4
+    assert out.value % 256 == 0
+    assert lib.asv_workspace_bytes(0, 0, 64, 10, ctypes.byref(out)) == 0
+    for bad in [(1, 0, 64, 10), (2, 1, 64, 10), (1, 4, 100, 10), (1, 4, 64, 0),
+                (-1, 4, 64, 10)]:
+        assert lib.asv_workspace_bytes(*bad, ctypes.byref(out)) == asv.ASV_EINVAL, bad
+    assert lib.asv_workspace_bytes(1, 4, 64, 10, None) == asv.ASV_EINVAL
+
+
+def test_verify_rejects_on_host(lib):
+    """Every rejection below happens before any HIP call, so it runs without a GPU."""
+    a = _abi.AsvVerifyArgs()
+    assert lib.asv_verify(None, None, 0, None) == asv.ASV_EINVAL
+    a.B, a.N, a.H, a.V = 1, 4, 100, 10          # H not a multiple of 64
+    assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
+    a.H = 64                                    # null pointers
+    assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
+    fake = 0x100000
+    for f, _ in _abi.AsvVerifyArgs._fields_[4:]:
+        if f not in ("params", "draft_logits", "draft_conf", "state", "k1_begin_event",
+                     "k1_end_event"):
+            setattr(a, f, fake)
+    a.params = asv.make_params()
+    assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EWORKSPACE
+    a.params = asv.make_params(alpha=0.0)
+    assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
+    a.params = asv.make_params(breaker_n=0)
+    assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
+    a.params = asv.make_params(max_promotions=-2)
+    assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
+    a.params = asv.make_params()
+    a.hidden = fake + 2                         # misaligned bf16 rows
+    assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
+    a.hidden = fake
+    need = ctypes.c_uint64(0)
+    lib.asv_workspace_bytes(1, 4, 64, 10, ctypes.byref(need))
+    assert lib.asv_verify(ctypes.byref(a), ctypes.c_void_p(fake + 64), need.value,
+                          None) == asv.ASV_EWORKSPACE          # misaligned workspace
+    assert lib.asv_verify(ctypes.byref(a), ctypes.c_void_p(fake), need.value - 1,
+                          None) == asv.ASV_EWORKSPACE          # too small
+    a.B, a.N = 0, 0                              # empty batch: nothing to do
+    assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_OK
+
+
+def test_state_init_rejects(lib):
+    p = asv.make_params()
+    assert lib.asv_state_init(None, 3, ctypes.byref(p), None) == asv.ASV_EINVAL
+    assert lib.asv_state_init(None, 0, ctypes.byref(p), None) == asv.ASV_OK

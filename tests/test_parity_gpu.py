@@ -1,0 +1,260 @@
+"""GPU parity of the HIP path (through the C ABI) with the float64 CPU oracle.
+
+Small and ragged shapes (several vocabulary slabs with a ragged last slab, one to three tree-row
+tiles with a ragged last tile, every K1 tile family) and the degenerate cases the method has.
+The oracle runs live on these sizes. Full-size configurations are in test_parity_full_gpu.py.
+"""
+
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+from harness import compare, compare_state, device_inputs, reference, resolve_with_oracle, \
+    to_host
+from workloads import build_tree, custom_workload, make_workload
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module")
+def asv():
+    import paper_2609_02897_amd as m
+    m.load()
+    return m
+
+
+def _run(asv, w, W, dev, tau=None, state=None, params=None, out=None):
+    import torch
+    d = device_inputs(w, W, dev, tau)
+    o = asv.verify(d["hidden"], d["w_lm"], d["draft_tok"], d["parent"], d["req_offsets"],
+                   d["tau"], d["draft_logits"], state=state, params=params, out=out)
+    torch.cuda.synchronize()
+    return to_host(o)
+
+
+def _trees(kind, n_req, seed):
+    rng = np.random.default_rng(seed)
+    return [build_tree(kind, rng, b) for b in range(n_req)]
+
+
+def _rand_tree(rng, n, depth_max, branch_max):
+    parent, depth, kids = [-1], [0], [0]
+    while len(parent) < n:
+        open_nodes = [i for i in range(len(parent)) if depth[i] < depth_max and
+                      kids[i] < branch_max]
+        p = int(open_nodes[rng.integers(len(open_nodes))])
+        parent.append(p)
+        depth.append(depth[p] + 1)
+        kids.append(0)
+        kids[p] += 1
+    return parent
+
+
+def _case(name):
+    rng = np.random.default_rng(zlib.crc32(name.encode()))
+    if name == "tiny_config":
+        return make_workload(0)
+    if name == "rows64_eagle60_ragged_vocab":
+        # one 60-node EAGLE-style tree, 17 slabs with a ragged last slab of 77 entries
+        return custom_workload(name, 256, 16 * 256 + 77, _trees("eagle60", 1, 1), 0.3,
+                               seed=1, w_std=0.08)
+    if name == "rows128_mixed":
+        trees = [_rand_tree(rng, int(rng.integers(1, 40)), 6, 4) for _ in range(5)]
+        return custom_workload(name, 128, 3000, trees, 0.2, seed=2, w_std=0.11,
+                               draft_logits=True)
+    if name == "rows256_three_tiles":
+        trees = _trees("adaptive", 9, 3)
+        return custom_workload(name, 192, 2500, trees, 0.2, seed=3, w_std=0.09,
+                               draft_logits=True)
+    if name == "deep_chain_and_wide":
+        trees = [[-1] + list(range(40)), [-1] + [0] * 100, [-1]]
+        return custom_workload(name, 64, 1024, trees, 0.05, seed=4, w_std=0.16)
+    if name == "root_only_requests":
+        trees = [[-1], [-1, 0, 1, 1], [-1], [-1, 0]]
+        return custom_workload(name, 64, 700, trees, 0.3, seed=5, w_std=0.16)
+    raise KeyError(name)
+
+
+CASES = ["tiny_config", "rows64_eagle60_ragged_vocab", "rows128_mixed", "rows256_three_tiles",
+         "deep_chain_and_wide", "root_only_requests"]
+
+
+@pytest.mark.parametrize("tau", [None, 0.0, 0.05, 0.3, 1.0])
+@pytest.mark.parametrize("name", CASES)
+def test_parity_small(asv, dev, name, tau):
+    print(f"[parity] case={name} tau={tau}", flush=True)
+    w = _case(name)
+    W = w.weights()
+    w64 = oracle.widen_weights(W)
+    resolve_with_oracle(w, w64)
+    taus = None if tau is None else np.full(w.B, tau, dtype=np.float32)
+    ref = reference(w, w64, tau=taus)
+    got = _run(asv, w, W, dev, tau=taus)
+    rep = compare(w, ref, got)
+    print(f"  {rep}", flush=True)
+    if tau == 0.0:
+        assert np.all(got["accept"] == 1)
+    if tau == 1.0:
+        # strict verification: every accepted node is the argmax of its parent row
+        for c in got["accepted_path"][got["accepted_path"] >= 0]:
+            p = w.parent[c]
+            assert w.draft_tok[c] == got["row_argmax"][p] or ref["row_gap"][p] < 1e-3
+
+
+def test_determinism(asv, dev):
+    w = _case("rows256_three_tiles")
+    W = w.weights()
+    resolve_with_oracle(w, oracle.widen_weights(W))
+    a = _run(asv, w, W, dev)
+    b = _run(asv, w, W, dev)
+    for k in a:
+        if a[k] is not None:
+            assert np.array_equal(a[k], b[k], equal_nan=True), k
+
+
+@pytest.mark.parametrize("max_promotions", [0, 1, 2])
+def test_promotion_cap(asv, dev, max_promotions):
+    w = _case("deep_chain_and_wide")
+    W = w.weights()
+    w64 = oracle.widen_weights(W)
+    resolve_with_oracle(w, w64)
+    p = oracle.Params(max_promotions=max_promotions)
+    ref = reference(w, w64, params=p)
+    got = _run(asv, w, W, dev, params=asv.make_params(max_promotions=max_promotions))
+    compare(w, ref, got)
+
+
+def test_exact_ties_lowest_index(asv, dev):
+    """Bit-identical W rows give bit-identical logits in both implementations; the argmax, the
+    bonus and the sibling choice must take the lowest index, across lanes, waves and slabs."""
+    w = custom_workload("ties", 128, 2000, [[-1, 0, 0, 1, 1, 2]], 1.0, seed=9, w_std=0.11)
+    W = np.array(w.weights())
+    w64 = oracle.widen_weights(W)
+    z = oracle.logits(oracle.widen_bf16(w.hidden), w64)
+    a0 = int(np.argmax(z[0]))
+    a1 = int(np.argmax(z[1]))
+    # row 0's winner duplicated into a later slab and an earlier slab (the earlier one wins)
+    W[min(a0 + 700, 1999)] = W[a0]
+    lo_id = 3 if a0 != 3 else 5
+    W[lo_id] = W[a0]
+    # row 1's winner duplicated at the next index (same slab, neighbouring lanes)
+    nxt = a1 + 1 if a1 + 1 < 2000 and a1 + 1 not in (a0, lo_id) else a1 - 1
+    W[nxt] = W[a1]
+    w64 = oracle.widen_weights(W)
+    z = oracle.logits(oracle.widen_bf16(w.hidden), w64)
+    top8 = oracle.row_top8(z)
+    w.with_drafts(top8)
+    # siblings 1 and 2 draft the two tied tokens of row 0: equal logits, lowest node id wins
+    w.draft_tok[1] = lo_id
+    w.draft_tok[2] = a0
+    ref = reference(w, w64)
+    got = _run(asv, w, W, dev)
+    for r in (0, 1):
+        ties = np.flatnonzero(z[r] == z[r].max())
+        assert len(ties) >= 2
+        assert got["row_argmax"][r] == ref["row_argmax"][r] == ties.min()
+    assert got["drafted_logit"][1] == got["drafted_logit"][2]
+    assert list(got["accepted_path"]) == list(ref["accepted_path"])
+    assert got["bonus_token"][0] == ref["bonus_token"][0]
+
+
+def test_history_state_over_steps(asv, dev):
+    """20 steps through the policy state: EMA, ring wrap at 16, breaker (forced with kappa=1
+    and non-argmax drafts on every other stretch of steps)."""
+    import torch
+    H, V = 64, 900
+    p = oracle.Params()
+    st_ref = [oracle.state_init(p) for _ in range(3)]
+    st_gpu = asv.state_init(3, asv.make_params(), device=dev)
+    for step in range(20):
+        rng = np.random.default_rng(100 + step)
+        trees = [_rand_tree(rng, int(rng.integers(2, 12)), 4, 3) for _ in range(3)]
+        w = custom_workload(f"hist{step}", H, V, trees, 0.3, seed=200 + step, w_std=0.2,
+                            draft_logits=True)
+        W = w.weights()
+        w64 = oracle.widen_weights(W)
+        resolve_with_oracle(w, w64)
+        if 6 <= step < 13:
+            # zero-accept steps: strict rule and drafts that are never the argmax
+            z = oracle.logits(oracle.widen_bf16(w.hidden), w64)
+            for c in range(w.N):
+                if w.parent[c] >= 0:
+                    w.draft_tok[c] = int(np.argsort(-z[w.parent[c]])[3])
+            w.tau[:] = 1.0
+        ref = reference(w, w64, state=st_ref, params=p)
+        got = _run(asv, w, W, dev, state=st_gpu)
+        rep = compare(w, ref, got)
+        assert rep.banded_requests == 0
+        st_ref = ref["state"]
+        compare_state(asv.state_fields(st_gpu), st_ref)
+        if step == 10:   # fifth consecutive zero-accept step
+            assert all(s.breaker == 1 for s in st_ref)
+        if 6 <= step < 10:
+            assert all(s.breaker == 0 and s.zero_streak == step - 5 for s in st_ref)
+
+
+def test_malformed_inputs_are_reported(asv, dev):
+    """Bad trees, tokens, thresholds and offsets set req_status bits; other requests are
+    unaffected and nothing faults."""
+    trees = [[-1, 0, 1], [-1, 0, 0], [-1, 0], [-1, 0, 1], [-1, 0]]
+    w = custom_workload("bad", 64, 500, trees, 0.3, seed=11, w_std=0.16)
+    W = w.weights()
+    w64 = oracle.widen_weights(W)
+    resolve_with_oracle(w, w64)
+    good_ref = reference(w, w64)
+    off = w.req_offsets
+    w.parent[off[0] + 2] = off[0] + 2          # request 0: parent not before the child
+    w.draft_tok[off[1] + 1] = 500              # request 1: token out of range
+    w.parent[off[2]] = 0                       # request 2: root with a parent
+    tau = w.tau.copy()
+    tau[3] = 1.5                               # request 3: threshold outside [0, 1]
+    got = _run(asv, w, W, dev, tau=tau)
+    assert got["req_status"][0] == asv.RS_BAD_PARENT
+    assert got["req_status"][1] == asv.RS_BAD_TOKEN
+    assert got["req_status"][2] == asv.RS_BAD_ROOT
+    assert got["req_status"][3] == asv.RS_BAD_TAU
+    assert got["req_status"][4] == 0
+    for b in range(4):
+        assert got["accepted_len"][b] == 0 and got["bonus_token"][b] == -1
+        assert np.all(got["accepted_path"][off[b]:off[b + 1]] == -1)
+    b = 4
+    assert got["accepted_len"][b] == good_ref["accepted_len"][b]
+    assert got["bonus_token"][b] == good_ref["bonus_token"][b]
+
+
+def test_bad_offsets_reported(asv, dev):
+    import torch
+    trees = [[-1, 0], [-1, 0, 0]]
+    w = custom_workload("badoff", 64, 300, trees, 0.3, seed=12, w_std=0.16)
+    W = w.weights()
+    resolve_with_oracle(w, oracle.widen_weights(W))
+    d = device_inputs(w, W, dev)
+    d["req_offsets"][2] = w.N - 1              # last offset != N
+    o = asv.verify(d["hidden"], d["w_lm"], d["draft_tok"], d["parent"], d["req_offsets"],
+                   d["tau"])
+    torch.cuda.synchronize()
+    st = o.req_status.cpu().numpy()
+    assert st[1] == asv.RS_BAD_OFFSETS and st[0] == 0
+
+
+def test_empty_batch(asv, dev):
+    import torch
+    e = dict(hidden=torch.empty((0, 64), dtype=torch.bfloat16, device=dev),
+             w_lm=torch.zeros((10, 64), dtype=torch.bfloat16, device=dev),
+             draft_tok=torch.empty(0, dtype=torch.int32, device=dev),
+             parent=torch.empty(0, dtype=torch.int32, device=dev),
+             req_offsets=torch.zeros(1, dtype=torch.int32, device=dev),
+             tau=torch.empty(0, dtype=torch.float32, device=dev))
+    o = asv.verify(**e)
+    torch.cuda.synchronize()
+    assert o.accepted_len.numel() == 0
