@@ -1,0 +1,243 @@
+"""Throughput of the AdaptiveSpec verification hot path on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1|3] [--no-cpu] \
+                    [--secondary 3|none]
+
+A step is one asv_verify call (LM-head kernel over every tree row with the per-slab
+reductions and drafted-logit gather, slab merge, margin rule + tree walk) on one batch of
+seeded synthetic inputs already resident in HBM. The headline workload is the Llama-3.1-8B
+shaped batch-1 verify (H=4096, V=128256, one 60-node EAGLE-style tree, kappa=0.3); the
+32x64-node batch (2048 rows) is measured after it as the MFMA-bound point. Prints one JSON
+line: verified tree nodes per second, the LM-head kernel's roofline fraction (its duration
+from HIP events recorded around it in every timed step) and the CPU oracle's throughput on a
+bounded sample of the same workload.
+"""
+
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+BF16_PEAK_TFLOPS = 2516.6      # MI355X dense bf16 MFMA (256 CU x 2.4 GHz x 4096 flop/clk)
+TABLES = os.path.join(ROOT, "tests", "golden")
+TRAFFIC = os.path.join(ROOT, "profiles", "k1_traffic.json")
+K1_SOURCES = [os.path.join(ROOT, "paper_2609_02897_amd", "csrc", f)
+              for f in ("k_lmhead.h", "k_common.h")]
+
+
+def k1_source_sha() -> str:
+    h = hashlib.sha256()
+    for p in K1_SOURCES:
+        h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
+
+
+class HipEvents:
+    """Raw hipEvent_t handles from the HIP runtime torch loaded (same soname)."""
+
+    def __init__(self):
+        self.hip = ctypes.CDLL("libamdhip64.so.7")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float),
+                                                 ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def create(self) -> int:
+        ev = ctypes.c_void_p()
+        assert self.hip.hipEventCreate(ctypes.byref(ev)) == 0
+        return ev.value
+
+    def elapsed_ms(self, a: int, b: int) -> float:
+        ms = ctypes.c_float()
+        assert self.hip.hipEventElapsedTime(ctypes.byref(ms), a, b) == 0
+        return ms.value
+
+    def destroy(self, ev: int):
+        self.hip.hipEventDestroy(ev)
+
+
+def load_workload(cfg: int, step: int = 0):
+    from workloads import CONFIGS, make_workload
+    w = make_workload(cfg, step)
+    path = os.path.join(TABLES, f"oracle_cfg{cfg}.npz")
+    with np.load(path, allow_pickle=False) as t:
+        w.draft_tok = t[f"draft_tok_s{step}"].astype(np.int32)
+        assert t[f"sha_hidden_s{step}"] == hashlib.sha256(w.hidden.tobytes()).hexdigest(), \
+            "seeded hidden states differ from the ones the oracle tables were made for"
+    return w, CONFIGS[cfg]
+
+
+def to_device(w, W, dev):
+    import torch
+
+    def t(x):
+        return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+
+    return dict(hidden=t(w.hidden.view(np.int16)).view(torch.bfloat16),
+                w_lm=t(W.view(np.int16)).view(torch.bfloat16),
+                draft_tok=t(w.draft_tok), parent=t(w.parent), req_offsets=t(w.req_offsets),
+                tau=t(w.tau),
+                draft_logits=None if w.draft_logits is None else t(w.draft_logits))
+
+
+def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents):
+    import torch
+    import paper_2609_02897_amd as asv
+    w, c = load_workload(cfg)
+    W = w.weights()
+    d = to_device(w, W, dev)
+    out = asv.alloc_outputs(w.B, w.N, dev, d["draft_logits"] is not None)
+    ws = asv.alloc_workspace(w.B, w.N, w.H, w.V, dev)
+    state = asv.state_init(w.B, device=dev)
+    evs = [(hip.create(), hip.create()) for _ in range(steps)]
+
+    def step(k1=None):
+        asv.verify(d["hidden"], d["w_lm"], d["draft_tok"], d["parent"], d["req_offsets"],
+                   d["tau"], d["draft_logits"], state=state, out=out, workspace=ws,
+                   k1_events=k1)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    k1_ms = [hip.elapsed_ms(a, b) for a, b in evs]
+    for a, b in evs:
+        hip.destroy(a)
+        hip.destroy(b)
+    status = out.req_status.cpu().numpy()
+    assert np.all(status == 0), status
+    k1_avg = float(np.mean(k1_ms))
+    nodes = w.N * steps
+    bytes_alg = 2 * w.V * w.H + 2 * w.N * w.H
+    flops_alg = 2 * w.N * w.V * w.H
+    res = dict(cfg=cfg, name=c["name"], N=w.N, B=w.B, H=w.H, V=w.V,
+               tau=float(w.tau[0]), value=nodes / dt, ms_per_step=1e3 * dt / steps,
+               k1_avg_ms=k1_avg, k1_min_ms=float(np.min(k1_ms)),
+               k1_share=k1_avg * steps / (1e3 * dt),
+               hbm_gbs=bytes_alg / (k1_avg * 1e-3) / 1e9,
+               mfma_tflops=flops_alg / (k1_avg * 1e-3) / 1e12,
+               bytes_alg=bytes_alg, flops_alg=flops_alg,
+               accepted_len=out.accepted_len.cpu().numpy().tolist()[:4])
+    del d, out, ws
+    torch.cuda.empty_cache()
+    return res, w, W
+
+
+def roofline(r: dict) -> dict:
+    bound_hbm = r["bytes_alg"] / (HBM_PEAK_GBS * 1e9) >= r["flops_alg"] / (BF16_PEAK_TFLOPS * 1e12)
+    if bound_hbm:
+        ro = dict(bound="hbm", achieved=round(r["hbm_gbs"], 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                  frac=round(r["hbm_gbs"] / HBM_PEAK_GBS, 4))
+    else:
+        ro = dict(bound="mfma", achieved=round(r["mfma_tflops"], 1), peak=BF16_PEAK_TFLOPS,
+                  unit="TFLOP/s", frac=round(r["mfma_tflops"] / BF16_PEAK_TFLOPS, 4))
+    ro["kernel"] = "k_lmhead_partial"
+    ro["k1_avg_us"] = round(1e3 * r["k1_avg_ms"], 2)
+    ro["traffic"] = measured_traffic(r["cfg"])
+    return ro
+
+
+def measured_traffic(cfg: int):
+    """HBM bytes per K1 launch from the committed rocprofv3 counter summary, if it was taken
+    on the current K1 source; otherwise None."""
+    if not os.path.exists(TRAFFIC):
+        return None
+    with open(TRAFFIC) as f:
+        t = json.load(f)
+    e = t.get(f"cfg{cfg}")
+    if not e or t.get("k1_source_sha") != k1_source_sha():
+        return None
+    return e.get("bytes_per_launch")
+
+
+def cpu_baseline(w, W, budget_s: float = 12.0) -> dict:
+    """The float64 oracle on the same step, repeated until about ``budget_s`` of CPU work."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    except Exception:  # pragma: no cover
+        threads = os.cpu_count() or 1
+    w64 = oracle.widen_weights(W)
+    n, t0 = 0, time.perf_counter()
+    while True:
+        oracle.verify(w64, w.hidden, w.draft_tok, w.parent, w.req_offsets, w.tau,
+                      w.draft_logits)
+        n += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return dict(value=round(w.N * n / dt, 2), unit="nodes/s", cores=int(threads), kind="oracle",
+                sample=f"{n} full verify steps of the headline workload ({w.N} rows each; "
+                       f"float64 logits via BLAS, weights pre-widened outside the timing), "
+                       f"{dt:.1f} s")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=1)
+    ap.add_argument("--secondary", default="3")
+    ap.add_argument("--no-cpu", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build measures one GPU only: the verification path "
+                          "runs on a single MI355X (multi-GPU sharding is design-only)"}))
+        sys.exit(2)
+    import torch
+    import paper_2609_02897_amd as asv
+    if not torch.cuda.is_available():
+        sys.exit("bench.py needs a GPU")
+    asv.load()
+    dev = torch.device("cuda:0")
+    hip = HipEvents()
+    r, w, W = measure(args.config, args.steps, args.warmup, dev, hip)
+    print(f"# cfg{r['cfg']} {r['name']}: {r['ms_per_step']*1e3:.1f} us/step, "
+          f"K1 {r['k1_avg_ms']*1e3:.1f} us, {r['hbm_gbs']:.0f} GB/s, "
+          f"{r['mfma_tflops']:.0f} TFLOP/s", file=sys.stderr, flush=True)
+    line = {
+        "metric": "verified tree nodes/sec (fused LM-head+margin accept); % HBM/MFMA roofline",
+        "value": round(r["value"], 1), "unit": "nodes/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(r["ms_per_step"], 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded bf16 W~N(0,0.02), hidden~N(0,1), EAGLE-style trees)",
+        "config": {"workload": r["name"], "H": r["H"], "V": r["V"], "rows": r["N"],
+                   "requests": r["B"], "tau": r["tau"], "parallelism": "single GPU"},
+        "roofline": roofline(r),
+    }
+    if args.secondary != "none" and int(args.secondary) != args.config:
+        del w, W
+        r2, _, _ = measure(int(args.secondary), args.steps, args.warmup, dev, hip)
+        print(f"# cfg{r2['cfg']} {r2['name']}: {r2['ms_per_step']*1e3:.1f} us/step, "
+              f"K1 {r2['k1_avg_ms']*1e3:.1f} us, {r2['mfma_tflops']:.0f} TFLOP/s",
+              file=sys.stderr, flush=True)
+        line["secondary"] = {"workload": r2["name"], "rows": r2["N"], "requests": r2["B"],
+                             "value": round(r2["value"], 1), "unit": "nodes/s",
+                             "ms_per_step": round(r2["ms_per_step"], 4),
+                             "roofline": roofline(r2)}
+        w, _ = load_workload(args.config)
+        W = w.weights()
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline(w, W)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

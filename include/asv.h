@@ -117,6 +117,11 @@ int asv_version(void);
 /* Static, human-readable text for an ASV_* return code. */
 const char *asv_status_string(int code);
 
+/* Details of the most recent ASV_EHIP failure on the calling host thread (the failing launch
+ * or runtime call and the HIP error text); "" if none. Valid until the next failing call on
+ * this thread. */
+const char *asv_last_error(void);
+
 /* Device workspace that asv_verify needs for these sizes (partial per-vocab-slab records of
  * the LM-head kernel and draft-confidence partials). Writes the byte count to *bytes. The
  * workspace must be 256-byte aligned; its contents need no initialisation and are

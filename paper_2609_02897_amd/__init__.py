@@ -34,8 +34,10 @@ class VerifyOut(NamedTuple):
 
 class AsvError(RuntimeError):
     def __init__(self, code: int):
-        msg = load().asv_status_string(code).decode()
-        super().__init__(f"libasv returned {code}: {msg}")
+        lib = load()
+        msg = lib.asv_status_string(code).decode()
+        detail = lib.asv_last_error().decode() if code == ASV_EHIP else ""
+        super().__init__(f"libasv returned {code}: {msg}" + (f" [{detail}]" if detail else ""))
         self.code = code
 
 

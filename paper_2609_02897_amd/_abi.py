@@ -13,8 +13,8 @@ RS_BAD_ROOT, RS_BAD_PARENT, RS_BAD_TOKEN, RS_BAD_OFFSETS, RS_BAD_TAU = 1, 2, 4, 
 HIST_WINDOW = 16
 
 # Every entry point include/asv.h declares.
-EXPORTS = ("asv_version", "asv_status_string", "asv_workspace_bytes", "asv_state_init",
-           "asv_verify")
+EXPORTS = ("asv_version", "asv_status_string", "asv_last_error", "asv_workspace_bytes",
+           "asv_state_init", "asv_verify")
 
 
 class AsvReqState(ctypes.Structure):
@@ -64,11 +64,21 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     if not os.path.exists(path):
         raise LibraryMissing(
             f"{path} is not built; run `python -c 'import __graft_entry__ as g; g.build()'`")
+    # torch wheels bundle their own HIP runtime (same soname, libamdhip64.so.7). Importing torch
+    # first makes the dynamic loader bind libasv to that already-loaded runtime, so torch's
+    # allocations, streams and events and libasv's launches share one HIP context; a second
+    # runtime in the same process would not see the GPU.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     lib = ctypes.CDLL(path)
     lib.asv_version.restype = ctypes.c_int
     lib.asv_version.argtypes = []
     lib.asv_status_string.restype = ctypes.c_char_p
     lib.asv_status_string.argtypes = [ctypes.c_int]
+    lib.asv_last_error.restype = ctypes.c_char_p
+    lib.asv_last_error.argtypes = []
     lib.asv_workspace_bytes.restype = ctypes.c_int
     lib.asv_workspace_bytes.argtypes = [ctypes.c_int32] * 4 + [ctypes.POINTER(ctypes.c_uint64)]
     lib.asv_state_init.restype = ctypes.c_int

@@ -15,6 +15,8 @@ OUT = os.path.join(_HERE, "libasv.so")
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    # code objects every ROCm 7.x runtime loads (torch may bring an older runtime than hipcc)
+    "-mcode-object-version=5",
     # keep the compiler from forming packed fp32 (v_pk_*_f32) instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]

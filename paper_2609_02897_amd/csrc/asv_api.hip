@@ -2,6 +2,8 @@
 // sequence of one verification step. Every entry point is declared in include/asv.h.
 #include <hip/hip_runtime.h>
 
+#include <cstdio>
+
 #include "asv.h"
 #include "k_accept.h"
 #include "k_lmhead.h"
@@ -11,6 +13,22 @@ namespace asv {
 namespace {
 
 constexpr size_t kAlign = 256;
+
+// Text of the most recent failure on this host thread (see asv_last_error).
+thread_local char g_last_error[256] = "";
+
+void set_error(const char* what, hipError_t e) {
+  snprintf(g_last_error, sizeof(g_last_error), "%s: %s (%d)", what, hipGetErrorString(e),
+           (int)e);
+}
+
+// ASV_OK when the launches enqueued so far succeeded, else ASV_EHIP with the error recorded.
+int launch_status(const char* what) {
+  const hipError_t e = hipGetLastError();
+  if (e == hipSuccess) return ASV_OK;
+  set_error(what, e);
+  return ASV_EHIP;
+}
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -77,6 +95,8 @@ using namespace asv;
 
 extern "C" int asv_version(void) { return ASV_VERSION; }
 
+extern "C" const char* asv_last_error(void) { return g_last_error; }
+
 extern "C" const char* asv_status_string(int code) {
   switch (code) {
     case ASV_OK: return "ok";
@@ -99,8 +119,9 @@ extern "C" int asv_state_init(asv_req_state* state, int32_t B, const asv_params*
   if (B < 0 || !p || (B > 0 && !state)) return ASV_EINVAL;
   if (B == 0) return ASV_OK;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
   k_state_init<<<(B + 255) / 256, 256, 0, s>>>(state, B, *p);
-  return hipGetLastError() == hipSuccess ? ASV_OK : ASV_EHIP;
+  return launch_status("k_state_init");
 }
 
 extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t workspace_bytes,
@@ -130,20 +151,28 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
     k_draft_conf_partial<<<dim3(L.n_conf, a->B), kConfThreads, 0, s>>>(
         a->N, a->V, a->req_offsets, a->draft_logits, reinterpret_cast<float*>(ws + L.off_conf_m),
         reinterpret_cast<float*>(ws + L.off_conf_s));
+    if (int rc = launch_status("k_draft_conf_partial")) return rc;
   }
 
   if (a->k1_begin_event) {
-    if (hipEventRecord(reinterpret_cast<hipEvent_t>(a->k1_begin_event), s) != hipSuccess)
+    const hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(a->k1_begin_event), s);
+    if (e != hipSuccess) {
+      set_error("hipEventRecord(k1_begin_event)", e);
       return ASV_EHIP;
+    }
   }
   switch (pick_tile(a->N)) {
     case Tile::kRows64: launch_lmhead<256, 64, 4, 1>(a, L, ws, s); break;
     case Tile::kRows128: launch_lmhead<256, 128, 2, 2>(a, L, ws, s); break;
     case Tile::kRows256: launch_lmhead<256, 256, 2, 2>(a, L, ws, s); break;
   }
+  if (int rc = launch_status("k_lmhead_partial")) return rc;
   if (a->k1_end_event) {
-    if (hipEventRecord(reinterpret_cast<hipEvent_t>(a->k1_end_event), s) != hipSuccess)
+    const hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(a->k1_end_event), s);
+    if (e != hipSuccess) {
+      set_error("hipEventRecord(k1_end_event)", e);
       return ASV_EHIP;
+    }
   }
 
   k_slab_merge<<<(a->N + kMergeRowsPerBlock - 1) / kMergeRowsPerBlock,
@@ -151,6 +180,7 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
       a->N, L.S, reinterpret_cast<const float*>(ws + L.off_rec_m),
       reinterpret_cast<const float*>(ws + L.off_rec_s),
       reinterpret_cast<const int32_t*>(ws + L.off_rec_a), a->row_max, a->row_lse, a->row_argmax);
+  if (int rc = launch_status("k_slab_merge")) return rc;
 
   k_tree_accept<<<a->B, kWave, 0, s>>>(
       a->B, a->N, a->V, a->req_offsets, a->parent, a->draft_tok, a->tau, a->row_max,
@@ -158,6 +188,5 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
       a->accepted_path, reinterpret_cast<const float*>(ws + L.off_conf_m),
       reinterpret_cast<const float*>(ws + L.off_conf_s), conf ? L.n_conf : 0, a->draft_conf,
       a->state, a->req_status, a->params);
-
-  return hipGetLastError() == hipSuccess ? ASV_OK : ASV_EHIP;
+  return launch_status("k_tree_accept");
 }

@@ -184,6 +184,8 @@ def test_history_state_over_steps(asv, dev):
         W = w.weights()
         w64 = oracle.widen_weights(W)
         resolve_with_oracle(w, w64)
+        if step < 6:
+            w.tau[:] = 0.0      # accept everything: every streak is 0 before the stretch
         if 6 <= step < 13:
             # zero-accept steps: strict rule and drafts that are never the argmax
             z = oracle.logits(oracle.widen_bf16(w.hidden), w64)
