@@ -108,6 +108,26 @@ def bf16_weights(V: int, H: int, std: float = 0.02, tag: int = 0) -> np.ndarray:
     return out
 
 
+def _dl_chunk(args):
+    key, V, r0, rows = args
+    x = np.random.default_rng([BASE_SEED, _S_DLOGIT, *key, r0]).standard_normal(
+        (rows, V), dtype=np.float32)
+    x *= np.float32(2.0)
+    return x
+
+
+def draft_logit_matrix(key, N: int, V: int, rows_per_chunk: int = 32) -> np.ndarray:
+    """Draft-model logits [N, V] float32 ~N(0, 2), in fixed row chunks with their own keys
+    (drawn on a thread pool; independent of the thread count)."""
+    out = np.empty((N, V), dtype=np.float32)
+    jobs = [(tuple(key), V, r0, min(rows_per_chunk, N - r0)) for r0 in range(0, N, rows_per_chunk)]
+    workers = max(1, min(16, os.cpu_count() or 1))
+    with ThreadPoolExecutor(workers) as ex:
+        for (_, _, r0, rows), blk in zip(jobs, ex.map(_dl_chunk, jobs)):
+            out[r0:r0 + rows] = blk
+    return out
+
+
 # ----------------------------------------------------------------------------- trees
 
 def tree_depths(parent: np.ndarray) -> np.ndarray:
@@ -294,10 +314,7 @@ def custom_workload(name: str, H: int, V: int, trees, tau, *, seed: int,
     kind, rank, uid = draft_choices(np.random.default_rng([BASE_SEED, _S_DRAFT, 1000 + seed]),
                                     depth, V, mix)
     tau = np.broadcast_to(np.asarray(tau, dtype=np.float32), (B,)).copy()
-    dl = None
-    if draft_logits:
-        dl = np.random.default_rng([BASE_SEED, _S_DLOGIT, 1000 + seed]).standard_normal(
-            (N, V), dtype=np.float32) * np.float32(2.0)
+    dl = draft_logit_matrix((1000 + seed,), N, V) if draft_logits else None
     return Workload(name, H, V, B, N, off, parent, depth, tau, hidden, kind, rank, uid, dl,
                     w_std, w_tag)
 
@@ -315,10 +332,6 @@ def make_workload(cfg: int, step: int = 0, tau: Optional[float] = None) -> Workl
                                     depth, V, c["mix"])
     t = c["taus"][-1] if tau is None else tau
     taus = np.full(B, t, dtype=np.float32)
-    dl = None
-    if c["draft_logits"]:
-        dl = np.random.default_rng([BASE_SEED, cfg, step, _S_DLOGIT]).standard_normal(
-            (N, V), dtype=np.float32)
-        dl *= np.float32(2.0)
+    dl = draft_logit_matrix((cfg, step), N, V) if c["draft_logits"] else None
     return Workload(c["name"], H, V, B, N, off, parent, depth, taus, hidden, kind, rank, uid,
                     dl)
