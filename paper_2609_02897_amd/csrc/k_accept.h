@@ -35,6 +35,10 @@ __device__ __forceinline__ void best_child_reduce(float& g, int& c) {
   }
 }
 
+// Requests with at most this many nodes are staged in LDS with one round of loads and walked
+// there; larger ones are walked from global memory (same arithmetic).
+constexpr int kStageNodes = 1024;
+
 __global__ __launch_bounds__(kWave)
 void k_tree_accept(int B, int N, int V, const int32_t* __restrict__ off,
                    const int32_t* __restrict__ parent, const int32_t* __restrict__ tok,
@@ -45,6 +49,8 @@ void k_tree_accept(int B, int N, int V, const int32_t* __restrict__ off,
                    const float* __restrict__ conf_m, const float* __restrict__ conf_s,
                    int n_conf, float* __restrict__ draft_conf, asv_req_state* __restrict__ state,
                    int32_t* __restrict__ status, asv_params prm) {
+  __shared__ int32_t s_par[kStageNodes], s_tok[kStageNodes], s_arg[kStageNodes];
+  __shared__ float s_g[kStageNodes], s_max[kStageNodes];
   const int b = blockIdx.x, lane = threadIdx.x;
   const int lo = off[b], hi = off[b + 1];
   if (lo < 0 || lo >= hi || hi > N || (b == 0 && lo != 0) || (b == B - 1 && hi != N)) {
@@ -56,14 +62,45 @@ void k_tree_accept(int B, int N, int V, const int32_t* __restrict__ off,
     }
     return;
   }
+  const int n = hi - lo;
+  const float kappa = tau[b];
+
+  // draft-confidence partials: issued now, merged after the walk
+  Rec conf_r = rec_empty();
+  for (int i = lane; i < n_conf; i += kWave)
+    conf_r = rec_merge(conf_r, Rec{conf_m[(size_t)b * n_conf + i],
+                                   conf_s[(size_t)b * n_conf + i], 0});
+
+  // ---- stage the request: parent, token, drafted logit and the row max / argmax of every node
+  const bool staged = n <= kStageNodes;
+  if (staged) {
+    for (int i0 = 0; i0 < n; i0 += 4 * kWave) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int i = i0 + u * kWave + lane;
+        if (i < n) {
+          s_par[i] = parent[lo + i];
+          s_tok[i] = tok[lo + i];
+          s_g[i] = g[lo + i];
+          s_max[i] = row_max[lo + i];
+          s_arg[i] = row_arg[lo + i];
+        }
+      }
+    }
+    __syncthreads();
+  }
+  auto P = [&](int c) { return staged ? s_par[c - lo] : parent[c]; };
+  auto D = [&](int c) { return staged ? s_tok[c - lo] : tok[c]; };
+  auto Gc = [&](int c) { return staged ? s_g[c - lo] : g[c]; };
+  auto Mr = [&](int r) { return staged ? s_max[r - lo] : row_max[r]; };
+  auto Ar = [&](int r) { return staged ? s_arg[r - lo] : row_arg[r]; };
 
   // ---- validate the tree
-  const float kappa = tau[b];
   int st = 0;
   if (!(kappa >= 0.f && kappa <= 1.f)) st |= ASV_RS_BAD_TAU;
-  if (lane == 0 && parent[lo] != -1) st |= ASV_RS_BAD_ROOT;
+  if (lane == 0 && P(lo) != -1) st |= ASV_RS_BAD_ROOT;
   for (int c = lo + 1 + lane; c < hi; c += kWave) {
-    const int p = parent[c], d = tok[c];
+    const int p = P(c), d = D(c);
     if (p < lo || p >= c) st |= ASV_RS_BAD_PARENT;
     if (d < 0 || d >= V) st |= ASV_RS_BAD_TOKEN;
   }
@@ -87,8 +124,8 @@ void k_tree_accept(int B, int N, int V, const int32_t* __restrict__ off,
   for (int c = lo + lane; c < hi; c += kWave) {
     uint8_t ok = 1;
     if (c != lo) {
-      const int p = parent[c];
-      ok = (tok[c] == row_arg[p]) || kappa == 0.f || (g[c] - row_max[p] >= ln_kappa);
+      const int p = P(c);
+      ok = (D(c) == Ar(p)) || kappa == 0.f || (Gc(c) - Mr(p) >= ln_kappa);
     }
     accept[c] = ok;
   }
@@ -99,8 +136,8 @@ void k_tree_accept(int B, int N, int V, const int32_t* __restrict__ off,
     float bg = kNegInf;
     int bc = kNoIndex;
     for (int c = lo + 1 + lane; c < hi; c += kWave) {
-      if (parent[c] == cur) {
-        const float gc = g[c];
+      if (P(c) == cur) {
+        const float gc = Gc(c);
         if (bc == kNoIndex || gc > bg || (gc == bg && c < bc)) {
           bg = gc;
           bc = c;
@@ -109,9 +146,9 @@ void k_tree_accept(int B, int N, int V, const int32_t* __restrict__ off,
     }
     best_child_reduce(bg, bc);
     if (bc == kNoIndex) break;
-    const int arg = row_arg[cur];
-    const int d = tok[bc];
-    const bool ok = (d == arg) || kappa == 0.f || (bg - row_max[cur] >= ln_kappa);
+    const int arg = Ar(cur);
+    const int d = D(bc);
+    const bool ok = (d == arg) || kappa == 0.f || (bg - Mr(cur) >= ln_kappa);
     if (!ok) break;
     if (d != arg) {
       if (prm.max_promotions >= 0 && promos >= prm.max_promotions) break;
@@ -126,53 +163,61 @@ void k_tree_accept(int B, int N, int V, const int32_t* __restrict__ off,
   // ---- draft top-1 confidence of the root row: 1 / sum_v exp(q_v - max q)
   float conf = 0.f;
   if (n_conf > 0) {
-    Rec r = rec_empty();
-    for (int i = lane; i < n_conf; i += kWave)
-      r = rec_merge(r, Rec{conf_m[(size_t)b * n_conf + i], conf_s[(size_t)b * n_conf + i], 0});
-    r = rec_wave_reduce(r);
-    conf = 1.f / r.s;
+    conf_r = rec_wave_reduce(conf_r);
+    conf = 1.f / conf_r.s;
   }
 
-  if (lane != 0) return;
-  acc_len[b] = len;
-  bonus[b] = row_arg[cur];
-  status[b] = 0;
-  if (n_conf > 0 && draft_conf) draft_conf[b] = conf;
+  if (lane == 0) {
+    acc_len[b] = len;
+    bonus[b] = Ar(cur);
+    status[b] = 0;
+    if (n_conf > 0 && draft_conf) draft_conf[b] = conf;
+  }
   if (!state) return;
 
-  // ---- policy state (one lane)
-  asv_req_state* s = state + b;
-  const int n = hi - lo;
-  if (n > 1) {
-    const float x = (float)len / (float)(n - 1);
-    s->rar = s->rar + prm.alpha * (x - s->rar);
-    const int head = ((s->hist_head % ASV_HIST_WINDOW) + ASV_HIST_WINDOW) % ASV_HIST_WINDOW;
-    s->hist[head] = x;
-    const int new_head = (head + 1) % ASV_HIST_WINDOW;
-    const int count = min(max(s->hist_count, 0) + 1, ASV_HIST_WINDOW);
-    float sum = 0.f;
-    for (int i = 0; i < count; ++i)
-      sum += s->hist[(new_head - 1 - i + 2 * ASV_HIST_WINDOW) % ASV_HIST_WINDOW];
-    s->hist_head = new_head;
-    s->hist_count = count;
-    s->hist_mean = sum / (float)count;
-    const int streak = (len == 0) ? s->zero_streak + 1 : 0;
-    const int trip = streak >= prm.breaker_n ? 1 : 0;
-    s->breaker = trip;
-    s->zero_streak = streak;
-    if (trip) {
-      s->rar = prm.rar0;
-      for (int i = 0; i < ASV_HIST_WINDOW; ++i) s->hist[i] = 0.f;
-      s->hist_head = 0;
-      s->hist_count = 0;
-      s->hist_mean = prm.rar0;
-      s->zero_streak = 0;
+  // ---- policy state: the 24 words are read in one round (one per lane), updated by lane 0 in
+  // registers-to-LDS, and written back one word per lane.
+  static_assert(sizeof(asv_req_state) == 24 * 4, "state layout");
+  __shared__ asv_req_state s_st;
+  uint32_t* const st_words = reinterpret_cast<uint32_t*>(state + b);
+  uint32_t* const sh_words = reinterpret_cast<uint32_t*>(&s_st);
+  if (lane < 24) sh_words[lane] = st_words[lane];
+  __syncthreads();
+  if (lane == 0) {
+    asv_req_state& q = s_st;
+    if (n > 1) {
+      const float x = (float)len / (float)(n - 1);
+      q.rar = q.rar + prm.alpha * (x - q.rar);
+      const int head = ((q.hist_head % ASV_HIST_WINDOW) + ASV_HIST_WINDOW) % ASV_HIST_WINDOW;
+      q.hist[head] = x;
+      const int new_head = (head + 1) % ASV_HIST_WINDOW;
+      const int count = min(max(q.hist_count, 0) + 1, ASV_HIST_WINDOW);
+      float sum = 0.f;
+      for (int i = 0; i < count; ++i)
+        sum += q.hist[(new_head - 1 - i + 2 * ASV_HIST_WINDOW) % ASV_HIST_WINDOW];
+      q.hist_head = new_head;
+      q.hist_count = count;
+      q.hist_mean = sum / (float)count;
+      const int streak = (len == 0) ? q.zero_streak + 1 : 0;
+      const int trip = streak >= prm.breaker_n ? 1 : 0;
+      q.breaker = trip;
+      q.zero_streak = streak;
+      if (trip) {
+        q.rar = prm.rar0;
+        for (int i = 0; i < ASV_HIST_WINDOW; ++i) q.hist[i] = 0.f;
+        q.hist_head = 0;
+        q.hist_count = 0;
+        q.hist_mean = prm.rar0;
+        q.zero_streak = 0;
+      }
+    } else {
+      q.breaker = 0;
     }
-  } else {
-    s->breaker = 0;
+    q.steps = q.steps + 1;
+    if (n_conf > 0) q.draft_conf = conf;
   }
-  s->steps = s->steps + 1;
-  if (n_conf > 0) s->draft_conf = conf;
+  __syncthreads();
+  if (lane < 24) st_words[lane] = sh_words[lane];
 }
 
 __global__ void k_state_init(asv_req_state* state, int B, asv_params prm) {

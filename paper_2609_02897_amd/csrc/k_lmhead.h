@@ -8,12 +8,15 @@
 // tile, read from the very accumulator the max saw. These are the target probabilities the
 // margin rule of Sec. 3.2, Eq. (1) needs; the [N][V] logits never reach memory.
 //
-// Data flow: W and X tiles are staged HBM -> registers -> LDS (double buffered, 64 K-elements
-// per stage, XOR-swizzled 16-byte chunks), read back in the MFMA operand layout and fed to
-// v_mfma_f32_32x32x16_bf16. Both operands are K-contiguous (W is [V][H], X is [N][H]), so every
-// lane moves 16 contiguous bytes per load. The MFMA's A operand is W (32 vocab rows) and B is X
-// (32 tree rows): each lane then owns one tree row and 16 vocabulary entries of every 32x32
-// output block, so the per-row reduction is mostly lane-local.
+// Data flow: a ring of NST LDS stages, each holding BK K-elements of every W and X row of the
+// tile. Stages are filled by direct global->LDS buffer loads (no staging registers), issued
+// NST-1 stages ahead of their use; their completion is awaited by hand (s_waitcnt vmcnt) just
+// before the one workgroup barrier per stage. 16-byte chunks are XOR-swizzled so that
+// ds_read_b128 in the MFMA operand layout is free of bank conflicts. The MFMA is
+// v_mfma_f32_32x32x16_bf16 with A = W (32 vocabulary rows) and B = X (32 tree rows): each lane
+// then owns one tree row and 16 vocabulary entries of every 32x32 output block, so the
+// per-row reduction is mostly lane-local. Fragments of the next K16 step are read while the
+// current MFMAs run.
 #pragma once
 
 #include "k_common.h"
@@ -23,36 +26,84 @@ namespace asv {
 typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
 
-constexpr int kBK = 64;     // K elements per stage (one 128-byte segment of a row)
-constexpr int kSlab = 256;  // vocabulary rows per workgroup = width of one record slab
-
-// Staged tiles hold 8 chunks of 16 bytes per row; logical chunk c of row r sits at
-// c ^ (r & 7), so 8 consecutive rows reading the same chunk use 8 distinct bank groups.
-__device__ __forceinline__ int swz(int row, int chunk) { return row * 8 + (chunk ^ (row & 7)); }
+constexpr int kSlab = 256;    // vocabulary rows per workgroup = width of one record slab
+constexpr int kKAlign = 64;   // H must be a multiple of this (host check)
 
 // Word 3 of a raw buffer resource on gfx9-family GPUs (32-bit data format, no swizzle).
 constexpr int kRsrcWord3 = 0x00020000;
 
-__device__ __forceinline__ uint4 ld16(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-  const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
-  return make_uint4(v.x, v.y, v.z, v.w);
+// A staged row of BK bf16 is CPR = BK / 8 chunks of 16 bytes. Logical chunk c of row r is
+// stored at position c ^ f(r) (16-byte units from the region start), with f(r) = r & 7 for
+// 128-byte rows and (r >> 1) & 3 for 64-byte rows: any 8 consecutive rows reading the same
+// logical chunk then hit 8 distinct 16-byte LDS bank groups.
+template <int CPR>
+__device__ __forceinline__ int swz_phase(int row) {
+  static_assert(CPR == 4 || CPR == 8, "64- or 128-byte staged rows");
+  return CPR == 8 ? (row & 7) : ((row >> 1) & 3);
+}
+template <int CPR>
+__device__ __forceinline__ int swz(int row, int chunk) {
+  return row * CPR + (chunk ^ swz_phase<CPR>(row));
 }
 
-template <int TV, int TR, int WV, int WR>
+// Direct global->LDS copy of 16 bytes per lane: lane t's 16 bytes land at LDS byte address
+// lds + 16 t. Out-of-range offsets of the buffer resource write zeros.
+// M0 is reserved: the compiler sets it right before each instruction that reads it and never
+// keeps a value in it across other code on gfx9-family GPUs, so overwriting it here is safe;
+// the clobber is declared anyway.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16(int lds, int voff, __amdgpu_buffer_rsrc_t r) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(r)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Wait until at most N vector-memory operations of this wave are outstanding and its LDS
+// reads are done, then join the workgroup barrier. Loads complete in order, so this retires
+// every older stage copy.
+template <int N>
+__device__ __forceinline__ void wait_vm_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" : : "n"(N) : "memory");
+}
+
+// wait_vm_barrier<newer * L>() for a run-time newer in [0, 3].
+template <int L>
+__device__ __forceinline__ void wait_stage_barrier(int newer) {
+  if (newer >= 3) wait_vm_barrier<3 * L>();
+  else if (newer == 2) wait_vm_barrier<2 * L>();
+  else if (newer == 1) wait_vm_barrier<L>();
+  else wait_vm_barrier<0>();
+}
+
+template <int TV, int TR, int WV, int WR, int BK, int NST>
 struct LmheadCfg {
-  static constexpr int kThreads = WV * WR * kWave;
+  static constexpr int kWaves = WV * WR;
+  static constexpr int kThreads = kWaves * kWave;
   static constexpr int kWaveV = TV / WV;        // vocabulary rows per wave
   static constexpr int kWaveR = TR / WR;        // tree rows per wave
   static constexpr int MV = kWaveV / 32;        // 32x32 blocks per wave, vocab direction
   static constexpr int MR = kWaveR / 32;        // 32x32 blocks per wave, tree-row direction
-  static constexpr int CW = TV * 8 / kThreads;  // 16-byte W chunks each thread stages
-  static constexpr int CX = TR * 8 / kThreads;  // 16-byte X chunks each thread stages
+  static constexpr int CPR = BK / 8;            // 16-byte chunks per staged row
+  static constexpr int kRowsPerCopy = 64 / CPR; // rows one 1 KB wave copy fills
+  static constexpr int kStageW = TV * BK * 2;   // bytes of W per stage
+  static constexpr int kStageX = TR * BK * 2;   // bytes of X per stage
+  static constexpr int kStage = kStageW + kStageX;
+  static constexpr int DW = kStageW / 1024 / kWaves;  // 1 KB copies per wave per stage, W
+  static constexpr int DX = kStageX / 1024 / kWaves;  // 1 KB copies per wave per stage, X
+  static constexpr int kLoads = DW + DX;        // vector-memory ops per lane per stage
+  static constexpr int kLds = NST * kStage;
   static constexpr int kCand = 2;               // gather candidates prefetched per thread
   static_assert(TV == kSlab, "one record slab per workgroup");
-  static_assert(MV >= 1 && MR >= 1 && CW >= 1 && CX >= 1, "tile too small for the wave grid");
-  static_assert((TV * 8) % kThreads == 0 && (TR * 8) % kThreads == 0, "uneven staging");
-  static_assert((kThreads / 8) % 8 == 0, "staged row groups must keep the swizzle phase");
+  static_assert(MV >= 1 && MR >= 1, "tile too small for the wave grid");
+  static_assert(BK == 32 || BK == 64, "stage depth");
+  static_assert(NST >= 2 && NST <= 5, "ring depth");
+  static_assert(DW >= 1 && DX >= 1 && DW * kWaves * 1024 == kStageW &&
+                DX * kWaves * 1024 == kStageX, "each wave copies whole 1 KB groups");
+  static_assert((NST - 2) * kLoads <= 63, "vmcnt range");
+  static_assert(kLds <= 160 * 1024, "LDS per workgroup");
 };
 
 // Map a launch-order block id to a tile so that each XCD (blocks are dealt to the 8 XCDs
@@ -63,60 +114,56 @@ __device__ __forceinline__ int xcd_tile(int bid, int G) {
   return xcd * q + min(xcd, rem) + loc;
 }
 
-template <int TV, int TR, int WV, int WR>
+template <int TV, int TR, int WV, int WR, int BK, int NST>
 __global__ __launch_bounds__(WV * WR * kWave)
 void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                       const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
                       const int32_t* __restrict__ req_offsets, int B, int N, int H, int V,
                       int S, int RT, float* __restrict__ rec_m, float* __restrict__ rec_s,
                       int32_t* __restrict__ rec_a, float* __restrict__ drafted_logit) {
-  using C = LmheadCfg<TV, TR, WV, WR>;
+  using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
+  constexpr int CPR = C::CPR;
   constexpr int T = C::kThreads;
-  // One LDS block: two W stages, two X stages. The epilogue reuses it (gather list in the W
-  // stages, reduction scratch at the start of X stage 0, two counters at X stage 1).
-  __shared__ uint4 smem[2 * TV * 8 + 2 * TR * 8];
-  auto sW = [&](int stage) { return smem + stage * (TV * 8); };
-  auto sX = [&](int stage) { return smem + 2 * TV * 8 + stage * (TR * 8); };
-  int* const s_seg_end = reinterpret_cast<int*>(sX(1));
-  int* const s_cnt = s_seg_end + 1;
+  __shared__ uint4 smem[C::kLds / 16];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wv = wave % WV, wr = wave / WV;
   const int tile = xcd_tile(blockIdx.x, gridDim.x);
   const int slab = tile / RT, rt = tile % RT;
   const int v0 = slab * TV, r0 = rt * TR;
   const int v_end = min(v0 + TV, V);
   const int r_last = min(r0 + TR, N) - 1;
+  const int lds0 = __builtin_amdgcn_readfirstlane((int)(size_t)smem);
 
-  // ---- staging through buffer loads: one resource per operand covering only this tile's
-  // valid rows, so rows past V (last slab) or past N (last row tile) read as zeros and never
-  // touch memory outside the arrays; their results are discarded below.
+  // ---- one buffer resource per operand covering only this tile's valid rows: rows past V
+  // (last slab) or past N (last row tile) read as zeros and never touch memory outside the
+  // arrays; their results are discarded below.
   const __amdgpu_buffer_rsrc_t w_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(W + (size_t)v0 * H), (short)0, (v_end - v0) * H * 2, kRsrcWord3);
   const __amdgpu_buffer_rsrc_t x_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(X + (size_t)r0 * H), (short)0, (r_last + 1 - r0) * H * 2,
       kRsrcWord3);
-  // Thread t stages 16-byte chunk (t & 7) of rows (t >> 3) + i * T/8; consecutive threads read
-  // consecutive 16 bytes of a row (8 threads cover one 128-byte segment).
-  const int st_row = tid >> 3, st_ch = tid & 7;
-  const int st_voff = st_row * H * 2 + st_ch * 16;
-  const int st_dst = swz(st_row, st_ch);   // + i * T for chunk i (T/8 is a multiple of 8)
-  uint4 rw[C::CW], rx[C::CX];
-  auto load_stage = [&](int k0) {
+  // Copy j of a stage region fills rows R j .. R j + R - 1 (R = kRowsPerCopy, a multiple of
+  // 8); lane t supplies 16 bytes of row R j + t / CPR at swizzled position t % CPR, i.e. the
+  // logical chunk (t % CPR) ^ f(t / CPR).
+  const int cp_row = lane / CPR;
+  const int cp_chunk = (lane % CPR) ^ swz_phase<CPR>(cp_row);
+  const int cp_voff = cp_row * H * 2 + cp_chunk * 16;
+  auto issue_stage = [&](int ks) {
+    const int k2 = ks * BK * 2;
+    const int base = lds0 + (ks % NST) * C::kStage;
 #pragma unroll
-    for (int i = 0; i < C::CW; ++i)
-      rw[i] = ld16(w_rsrc, st_voff + i * (T / 8) * H * 2, k0 * 2);
+    for (int i = 0; i < C::DW; ++i) {
+      const int j = i * C::kWaves + wave;
+      dma16(base + j * 1024, cp_voff + j * C::kRowsPerCopy * H * 2 + k2, w_rsrc);
+    }
 #pragma unroll
-    for (int i = 0; i < C::CX; ++i)
-      rx[i] = ld16(x_rsrc, st_voff + i * (T / 8) * H * 2, k0 * 2);
+    for (int i = 0; i < C::DX; ++i) {
+      const int j = i * C::kWaves + wave;
+      dma16(base + C::kStageW + j * 1024, cp_voff + j * C::kRowsPerCopy * H * 2 + k2, x_rsrc);
+    }
   };
-  auto store_stage = [&](int stage) {
-#pragma unroll
-    for (int i = 0; i < C::CW; ++i) sW(stage)[st_dst + i * T] = rw[i];
-#pragma unroll
-    for (int i = 0; i < C::CX; ++i) sX(stage)[st_dst + i * T] = rx[i];
-  };
-  load_stage(0);
 
   // ---- prefetch what the drafted-logit gather needs: the request offsets (to find the end
   // of the segment holding the tile's last row; children of the tile's rows lie before it)
@@ -138,10 +185,7 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
     }
   }
 
-  store_stage(0);
-  __syncthreads();
-
-  // ---- main loop over K: prefetch stage kt+1 into registers while stage kt feeds the MFMAs
+  // ---- main loop over K
   f32x16 acc[C::MV][C::MR];
 #pragma unroll
   for (int i = 0; i < C::MV; ++i)
@@ -150,42 +194,87 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  const int KT = H / kBK;
+  const int KT = H / BK;
   const int frag_row = lane & 31, frag_half = lane >> 5;
-  for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    const bool more = kt + 1 < KT;
-    if (more) load_stage((kt + 1) * kBK);
+  const uint4* const lds_u4 = smem;
+  bf16x8 a0[C::MV], b0[C::MR], a1[C::MV], b1[C::MR];
+  // Fragments of K16 step `half` (0 or 1) of the stage in ring slot `slot`.
+  auto load_frags = [&](int slot, int half, bf16x8* a, bf16x8* b) {   // half: K16 step
+    const uint4* w = lds_u4 + slot * (C::kStage / 16);
+    const uint4* x = w + C::kStageW / 16;
 #pragma unroll
-    for (int s = 0; s < kBK / 16; ++s) {
-      bf16x8 a[C::MV], b[C::MR];
+    for (int i = 0; i < C::MV; ++i)
+      a[i] = __builtin_bit_cast(
+          bf16x8, w[swz<CPR>(wv * C::kWaveV + 32 * i + frag_row, 2 * half + frag_half)]);
 #pragma unroll
-      for (int i = 0; i < C::MV; ++i) {
-        const int row = wv * C::kWaveV + 32 * i + frag_row;
-        a[i] = __builtin_bit_cast(bf16x8, sW(cur)[swz(row, 2 * s + frag_half)]);
+    for (int j = 0; j < C::MR; ++j)
+      b[j] = __builtin_bit_cast(
+          bf16x8, x[swz<CPR>(wr * C::kWaveR + 32 * j + frag_row, 2 * half + frag_half)]);
+  };
+  auto mfmas = [&](const bf16x8* a, const bf16x8* b) {
+#pragma unroll
+    for (int i = 0; i < C::MV; ++i)
+#pragma unroll
+      for (int j = 0; j < C::MR; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+  };
+
+  // Prologue: fill the whole ring, then wait for stage 0.
+  const int pro = min(NST, KT);
+  for (int ks = 0; ks < pro; ++ks) issue_stage(ks);
+  wait_stage_barrier<C::kLoads>(pro - 1);
+  load_frags(0, 0, a0, b0);
+
+  // Per stage k with K16 steps s = 0 .. BK/16 - 1: read the fragments of step s + 1 while the
+  // MFMAs of step s run. Before the last step's MFMAs (all reads of slot k done), wait for
+  // stage k+1 and pass the barrier while the previous MFMAs drain, refill slot k with stage
+  // k + NST, and read the first fragments of k+1 under the last step's MFMAs.
+  constexpr int NS16 = BK / 16;
+  for (int k = 0; k < KT; ++k) {
+    const int slot = k % NST;
+#pragma unroll
+    for (int s = 0; s < NS16; ++s) {
+      bf16x8* ca = (s & 1) ? a1 : a0;
+      bf16x8* cb = (s & 1) ? b1 : b0;
+      bf16x8* na = (s & 1) ? a0 : a1;
+      bf16x8* nb = (s & 1) ? b0 : b1;
+      if (s + 1 < NS16) {
+        load_frags(slot, s + 1, na, nb);
+      } else if (k + 1 < KT) {
+        // stage k+1 must have landed; the copies of the newer stages may stay in flight
+        wait_stage_barrier<C::kLoads>(min(NST - 2, KT - 2 - k));
+        if (k + NST < KT) issue_stage(k + NST);
+        load_frags((k + 1) % NST, 0, na, nb);
       }
-#pragma unroll
-      for (int j = 0; j < C::MR; ++j) {
-        const int row = wr * C::kWaveR + 32 * j + frag_row;
-        b[j] = __builtin_bit_cast(bf16x8, sX(cur)[swz(row, 2 * s + frag_half)]);
-      }
-#pragma unroll
-      for (int i = 0; i < C::MV; ++i)
-#pragma unroll
-        for (int j = 0; j < C::MR; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      mfmas(ca, cb);
     }
-    if (more) store_stage(cur ^ 1);
-    __syncthreads();
   }
+  static_assert(NS16 % 2 == 0, "fragment double buffer alternates within a stage");
+  __syncthreads();
 
   // Output block (i, j), register e of a lane holds vocab row
   //   32*i + 8*(e/4) + 4*(lane/32) + e%4   (of the wave's vocab range) and
   // tree row 32*j + lane%32 (of the wave's row range).
 
+  // Epilogue scratch reuses the ring: the gather list (kCap entries of 16 bytes), one
+  // 64 x 16-float extraction area per wave, the row-reduction exchange and two counters.
+  constexpr int kCap = 1024;
+  constexpr int kScrOff = kCap * 16;
+  constexpr int kRedOff = kScrOff + C::kWaves * kWave * 16 * 4;
+  constexpr int kCntOff = kRedOff + 3 * WV * TR * 4;
+  static_assert(kCntOff + 8 <= C::kLds, "epilogue scratch exceeds the LDS ring");
+  char* const lds_bytes = reinterpret_cast<char*>(smem);
+  int4* const s_list = reinterpret_cast<int4*>(lds_bytes);
+  float* const wscr = reinterpret_cast<float*>(lds_bytes + kScrOff) + wave * (kWave * 16);
+  float* const red_m = reinterpret_cast<float*>(lds_bytes + kRedOff);
+  float* const red_s = red_m + WV * TR;
+  int* const red_a = reinterpret_cast<int*>(red_s + WV * TR);
+  int* const s_seg_end = reinterpret_cast<int*>(lds_bytes + kCntOff);
+  int* const s_cnt = s_seg_end + 1;
+
   // ---- drafted logits: nodes whose parent row and drafted token fall inside this tile.
-  // Matches are collected in LDS (the stage buffers are free now) and extracted by the lane
-  // that owns the accumulator. Candidates beyond the prefetched ones are read in rounds.
+  // Matches are collected in LDS and extracted by the lane that owns the accumulator.
+  // Candidates beyond the prefetched ones are read in rounds of kCap.
   if (tid == 0) *s_seg_end = N;
   __syncthreads();
   if (tid < B && off_lo <= r_last && r_last < off_hi) atomicMin(s_seg_end, off_hi);
@@ -196,11 +285,6 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
   __syncthreads();
   // Malformed offsets only widen or empty the candidate range; every access stays < N.
   const int cand_hi = max(r0 + 1, min(*s_seg_end, N));
-  // Gather list in W stage 0, per-wave extraction scratch (64 lanes x 16 floats) in stage 1.
-  int4* const s_list = reinterpret_cast<int4*>(sW(0));
-  constexpr int kCap = TV * 8;
-  float* const wscr = reinterpret_cast<float*>(sW(1)) + wave * (kWave * 16);
-  static_assert(WV * WR * kWave * 16 * 4 <= TV * 8 * 16, "extraction scratch exceeds a stage");
   for (int base = r0 + 1; base < cand_hi; base += kCap) {
     if (tid == 0) *s_cnt = 0;
     __syncthreads();
@@ -251,9 +335,6 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
 
   // ---- per-row slab record: lane-local pass, then the two lane halves, then the waves
   // that share the same tree rows (through LDS).
-  float* const red_m = reinterpret_cast<float*>(sX(0));
-  float* const red_s = red_m + WV * TR;
-  int* const red_a = reinterpret_cast<int*>(red_s + WV * TR);
 #pragma unroll
   for (int j = 0; j < C::MR; ++j) {
     Rec r = rec_empty();

@@ -13,6 +13,9 @@ constexpr int kConfThreads = 256;
 
 // One wave per tree row: lanes stride over the S slab records, then a butterfly merge.
 // row_lse = M + log(sum_s l_s * exp(m_s - M)); the argmax keeps the lowest index on ties.
+// Each lane issues the loads of kMergeBatch records before merging any, so a row of up to
+// 64 * kMergeBatch slabs costs one memory round trip.
+constexpr int kMergeBatch = 8;
 __global__ __launch_bounds__(kMergeRowsPerBlock * kWave)
 void k_slab_merge(int N, int S, const float* __restrict__ rec_m, const float* __restrict__ rec_s,
                   const int32_t* __restrict__ rec_a, float* __restrict__ row_max,
@@ -22,8 +25,16 @@ void k_slab_merge(int N, int S, const float* __restrict__ rec_m, const float* __
   if (n >= N) return;
   const size_t base = (size_t)n * S;
   Rec r = rec_empty();
-  for (int s = lane; s < S; s += kWave) r = rec_merge(r, Rec{rec_m[base + s], rec_s[base + s],
-                                                               rec_a[base + s]});
+  for (int s0 = 0; s0 < S; s0 += kWave * kMergeBatch) {
+    Rec batch[kMergeBatch];
+#pragma unroll
+    for (int u = 0; u < kMergeBatch; ++u) {
+      const int s = s0 + u * kWave + lane;
+      batch[u] = s < S ? Rec{rec_m[base + s], rec_s[base + s], rec_a[base + s]} : rec_empty();
+    }
+#pragma unroll
+    for (int u = 0; u < kMergeBatch; ++u) r = rec_merge(r, batch[u]);
+  }
   r = rec_wave_reduce(r);
   if (lane == 0) {
     row_max[n] = r.m;
