@@ -14,6 +14,10 @@ namespace {
 
 constexpr size_t kAlign = 256;
 
+// Vocabulary rows per K1 workgroup tile = width of one record slab; every tile family below
+// uses this width, so the record layout depends only on V.
+constexpr int kSlab = 256;
+
 // Text of the most recent failure on this host thread (see asv_last_error).
 thread_local char g_last_error[256] = "";
 
@@ -79,6 +83,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 template <int TV, int TR, int WV, int WR, int BK, int NST>
 void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStream_t s) {
+  static_assert(TV == kSlab, "tiles span exactly one record slab");
   const int RT = (a->N + TR - 1) / TR;
   const int grid = L.S * RT;
   k_lmhead_partial<TV, TR, WV, WR, BK, NST><<<grid, WV * WR * kWave, 0, s>>>(

@@ -1,6 +1,6 @@
 // K1: fused target LM-head over every draft-tree row, reduced per vocabulary slab.
 //
-// For a tile of TV vocabulary rows x TR tree rows, the workgroup computes the logits
+// For a tile of TV vocabulary rows (one record slab) x TR tree rows, the workgroup computes the logits
 // z[n][v] = sum_h W[v][h] * X[n][h] (bf16 inputs, fp32 accumulation on the MFMA units) and,
 // instead of storing them, writes one online-softmax record per (tree row, slab): the slab's
 // max logit, the sum of exp(z - max) and the lowest argmax. It also writes the drafted logit
@@ -26,20 +26,21 @@ namespace asv {
 typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
 
-constexpr int kSlab = 256;    // vocabulary rows per workgroup = width of one record slab
 constexpr int kKAlign = 64;   // H must be a multiple of this (host check)
 
 // Word 3 of a raw buffer resource on gfx9-family GPUs (32-bit data format, no swizzle).
 constexpr int kRsrcWord3 = 0x00020000;
 
 // A staged row of BK bf16 is CPR = BK / 8 chunks of 16 bytes. Logical chunk c of row r is
-// stored at position c ^ f(r) (16-byte units from the region start), with f(r) = r & 7 for
-// 128-byte rows and (r >> 1) & 3 for 64-byte rows: any 8 consecutive rows reading the same
-// logical chunk then hit 8 distinct 16-byte LDS bank groups.
+// stored at position c ^ f(r) (16-byte units from the region start). ds_read_b128 serves 16
+// lanes per pass from 64 four-byte banks; in the MFMA operand layout 16 consecutive lanes read
+// the same logical chunk of 16 consecutive rows, so f is chosen to put every aligned group of
+// 16 rows (and of 8 rows, for 8-lane passes) on distinct 16-byte bank groups:
+//   128-byte rows: f(r) = (r & 7) ^ ((r >> 3) & 1);  64-byte rows: f(r) = ((r >> 2) ^ (r >> 1)) & 3.
 template <int CPR>
 __device__ __forceinline__ int swz_phase(int row) {
   static_assert(CPR == 4 || CPR == 8, "64- or 128-byte staged rows");
-  return CPR == 8 ? (row & 7) : ((row >> 1) & 3);
+  return CPR == 8 ? ((row & 7) ^ ((row >> 3) & 1)) : (((row >> 2) ^ (row >> 1)) & 3);
 }
 template <int CPR>
 __device__ __forceinline__ int swz(int row, int chunk) {
@@ -96,7 +97,7 @@ struct LmheadCfg {
   static constexpr int kLoads = DW + DX;        // vector-memory ops per lane per stage
   static constexpr int kLds = NST * kStage;
   static constexpr int kCand = 2;               // gather candidates prefetched per thread
-  static_assert(TV == kSlab, "one record slab per workgroup");
+  static_assert(TV % 32 == 0 && TR % 32 == 0, "whole 32x32 MFMA blocks");
   static_assert(MV >= 1 && MR >= 1, "tile too small for the wave grid");
   static_assert(BK == 32 || BK == 64, "stage depth");
   static_assert(NST >= 2 && NST <= 5, "ring depth");
@@ -114,8 +115,8 @@ __device__ __forceinline__ int xcd_tile(int bid, int G) {
   return xcd * q + min(xcd, rem) + loc;
 }
 
-template <int TV, int TR, int WV, int WR, int BK, int NST>
-__global__ __launch_bounds__(WV * WR * kWave)
+template <int TV, int TR, int WV, int WR, int BK, int NST, int OCC = 1>
+__global__ __launch_bounds__(WV * WR * kWave, OCC)
 void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                       const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
                       const int32_t* __restrict__ req_offsets, int B, int N, int H, int V,
@@ -144,25 +145,27 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
   const __amdgpu_buffer_rsrc_t x_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(X + (size_t)r0 * H), (short)0, (r_last + 1 - r0) * H * 2,
       kRsrcWord3);
-  // Copy j of a stage region fills rows R j .. R j + R - 1 (R = kRowsPerCopy, a multiple of
-  // 8); lane t supplies 16 bytes of row R j + t / CPR at swizzled position t % CPR, i.e. the
-  // logical chunk (t % CPR) ^ f(t / CPR).
-  const int cp_row = lane / CPR;
-  const int cp_chunk = (lane % CPR) ^ swz_phase<CPR>(cp_row);
-  const int cp_voff = cp_row * H * 2 + cp_chunk * 16;
+  // Copy j of a stage region fills rows R j .. R j + R - 1 (R = kRowsPerCopy); lane t
+  // supplies 16 bytes of row R j + t / CPR at swizzled position t % CPR, i.e. the logical
+  // chunk (t % CPR) ^ f(R j + t / CPR).
+  auto copy_voff = [&](int j) {
+    const int row = j * C::kRowsPerCopy + lane / CPR;
+    return row * H * 2 + ((lane % CPR) ^ swz_phase<CPR>(row)) * 16;
+  };
+  int w_voff[C::DW], x_voff[C::DX];
+#pragma unroll
+  for (int i = 0; i < C::DW; ++i) w_voff[i] = copy_voff(i * C::kWaves + wave);
+#pragma unroll
+  for (int i = 0; i < C::DX; ++i) x_voff[i] = copy_voff(i * C::kWaves + wave);
   auto issue_stage = [&](int ks) {
     const int k2 = ks * BK * 2;
     const int base = lds0 + (ks % NST) * C::kStage;
 #pragma unroll
-    for (int i = 0; i < C::DW; ++i) {
-      const int j = i * C::kWaves + wave;
-      dma16(base + j * 1024, cp_voff + j * C::kRowsPerCopy * H * 2 + k2, w_rsrc);
-    }
+    for (int i = 0; i < C::DW; ++i)
+      dma16(base + (i * C::kWaves + wave) * 1024, w_voff[i] + k2, w_rsrc);
 #pragma unroll
-    for (int i = 0; i < C::DX; ++i) {
-      const int j = i * C::kWaves + wave;
-      dma16(base + C::kStageW + j * 1024, cp_voff + j * C::kRowsPerCopy * H * 2 + k2, x_rsrc);
-    }
+    for (int i = 0; i < C::DX; ++i)
+      dma16(base + C::kStageW + (i * C::kWaves + wave) * 1024, x_voff[i] + k2, x_rsrc);
   };
 
   // ---- prefetch what the drafted-logit gather needs: the request offsets (to find the end
