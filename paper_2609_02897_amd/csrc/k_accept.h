@@ -71,7 +71,13 @@ void k_tree_accept(int B, int N, int V, const int32_t* __restrict__ off,
     conf_r = rec_merge(conf_r, Rec{conf_m[(size_t)b * n_conf + i],
                                    conf_s[(size_t)b * n_conf + i], 0});
 
-  // ---- stage the request: parent, token, drafted logit and the row max / argmax of every node
+  // ---- stage the request: parent, token, drafted logit and the row max / argmax of every node,
+  // plus the 24-word policy state (one word per lane), all in one round of loads
+  static_assert(sizeof(asv_req_state) == 24 * 4, "state layout");
+  __shared__ asv_req_state s_st;
+  uint32_t* const sh_words = reinterpret_cast<uint32_t*>(&s_st);
+  uint32_t* const st_words = state ? reinterpret_cast<uint32_t*>(state + b) : nullptr;
+  if (state && lane < 24) sh_words[lane] = st_words[lane];
   const bool staged = n <= kStageNodes;
   if (staged) {
     for (int i0 = 0; i0 < n; i0 += 4 * kWave) {
@@ -87,8 +93,8 @@ void k_tree_accept(int B, int N, int V, const int32_t* __restrict__ off,
         }
       }
     }
-    __syncthreads();
   }
+  __syncthreads();
   auto P = [&](int c) { return staged ? s_par[c - lo] : parent[c]; };
   auto D = [&](int c) { return staged ? s_tok[c - lo] : tok[c]; };
   auto Gc = [&](int c) { return staged ? s_g[c - lo] : g[c]; };
@@ -175,14 +181,7 @@ void k_tree_accept(int B, int N, int V, const int32_t* __restrict__ off,
   }
   if (!state) return;
 
-  // ---- policy state: the 24 words are read in one round (one per lane), updated by lane 0 in
-  // registers-to-LDS, and written back one word per lane.
-  static_assert(sizeof(asv_req_state) == 24 * 4, "state layout");
-  __shared__ asv_req_state s_st;
-  uint32_t* const st_words = reinterpret_cast<uint32_t*>(state + b);
-  uint32_t* const sh_words = reinterpret_cast<uint32_t*>(&s_st);
-  if (lane < 24) sh_words[lane] = st_words[lane];
-  __syncthreads();
+  // ---- policy state (staged above): updated by lane 0 in LDS, written back one word per lane
   if (lane == 0) {
     asv_req_state& q = s_st;
     if (n > 1) {

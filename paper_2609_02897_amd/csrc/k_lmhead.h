@@ -19,6 +19,8 @@
 // current MFMAs run.
 #pragma once
 
+#include <type_traits>
+
 #include "k_common.h"
 
 namespace asv {
@@ -115,7 +117,7 @@ __device__ __forceinline__ int xcd_tile(int bid, int G) {
   return xcd * q + min(xcd, rem) + loc;
 }
 
-template <int TV, int TR, int WV, int WR, int BK, int NST, int OCC = 1>
+template <int TV, int TR, int WV, int WR, int BK, int NST, int OCC = 1, int ORDER = 0>
 __global__ __launch_bounds__(WV * WR * kWave, OCC)
 void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                       const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
@@ -131,7 +133,10 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wv = wave % WV, wr = wave / WV;
   const int tile = xcd_tile(blockIdx.x, gridDim.x);
-  const int slab = tile / RT, rt = tile % RT;
+  // ORDER 0: consecutive tiles are the row tiles of one slab (W slab shared in L2);
+  // ORDER 1: consecutive tiles are the slabs of one row tile (X tile resident in L2).
+  const int slab = ORDER == 0 ? tile / RT : tile % S;
+  const int rt = ORDER == 0 ? tile % RT : tile / S;
   const int v0 = slab * TV, r0 = rt * TR;
   const int v_end = min(v0 + TV, V);
   const int r_last = min(r0 + TR, N) - 1;
@@ -337,31 +342,44 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
   }
 
   // ---- per-row slab record: lane-local pass, then the two lane halves, then the waves
-  // that share the same tree rows (through LDS).
+  // that share the same tree rows (through LDS). Within a lane the entries of a tree row are
+  // visited in increasing vocabulary order, so "strictly greater" keeps the lowest argmax;
+  // the argmax is tracked as the entry ordinal k = 16 i + e and turned into a vocabulary id
+  // afterwards. Only the last slab needs the v < V mask. One row block at a time keeps the
+  // accumulator reads short-lived (sched_barrier stops the scheduler from hoisting them).
+  const bool full_slab = v0 + TV <= V;
+  const int vlane = v0 + wv * C::kWaveV + 4 * frag_half;
+  auto entry_v = [&](int k) { return vlane + 32 * (k >> 4) + 8 * ((k & 15) >> 2) + (k & 3); };
+  // Branch-free lane-local record of row block j; MASK drops entries past V (last slab).
+  auto row_record = [&](int j, auto mask_tag) -> Rec {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    float m = kNegInf;
+    int kbest = 0;
+#pragma unroll
+    for (int i = 0; i < C::MV; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int k = 16 * i + e;
+        float z = acc[i][j][e];
+        if constexpr (MASK) z = entry_v(k) < V ? z : kNegInf;
+        kbest = z > m ? k : kbest;
+        m = fmaxf(m, z);
+      }
+    const float mb = m * kLog2e;
+    float sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < C::MV; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float t = exp2f(fmaf(acc[i][j][e], kLog2e, -mb));
+        if constexpr (MASK) sum += entry_v(16 * i + e) < V ? t : 0.f;
+        else sum += t;
+      }
+    return Rec{m, m == kNegInf ? 0.f : sum, m == kNegInf ? kNoIndex : entry_v(kbest)};
+  };
 #pragma unroll
   for (int j = 0; j < C::MR; ++j) {
-    Rec r = rec_empty();
-#pragma unroll
-    for (int i = 0; i < C::MV; ++i)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int v = v0 + wv * C::kWaveV + 32 * i + 8 * (e >> 2) + 4 * frag_half + (e & 3);
-        const float z = acc[i][j][e];
-        if (v < V && z > r.m) {
-          r.m = z;
-          r.a = v;
-        }
-      }
-    float s = 0.f;
-    const float mb = r.m * kLog2e;
-#pragma unroll
-    for (int i = 0; i < C::MV; ++i)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int v = v0 + wv * C::kWaveV + 32 * i + 8 * (e >> 2) + 4 * frag_half + (e & 3);
-        if (v < V) s += exp2f(fmaf(acc[i][j][e], kLog2e, -mb));
-      }
-    r.s = s;
+    Rec r = full_slab ? row_record(j, std::false_type{}) : row_record(j, std::true_type{});
     r = rec_merge(r, rec_shfl_xor(r, 32));
     if (lane < 32) {
       const int row = wr * C::kWaveR + 32 * j + lane;
@@ -369,6 +387,7 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
       red_s[wv * TR + row] = r.s;
       red_a[wv * TR + row] = r.a;
     }
+    __builtin_amdgcn_sched_barrier(0);
   }
   __syncthreads();
   for (int row = tid; row < TR; row += T) {
