@@ -204,7 +204,20 @@ def main():
     ap.add_argument("--config", type=int, default=1)
     ap.add_argument("--secondary", default="3")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB five times (the "
+                         "reference dispatch for scaling HBM traffic counters) and exit")
     args = ap.parse_args()
+    if args.copy_calibration:
+        import torch
+        n = args.copy_calibration << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n, "dispatches": 5}))
+        return
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU only: the verification path "
                           "runs on a single MI355X (multi-GPU sharding is design-only)"}))
