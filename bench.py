@@ -4,7 +4,8 @@
                     [--secondary 3|none]
 
 A step is one asv_verify call (LM-head kernel over every tree row with the per-slab
-reductions and drafted-logit gather, slab merge, margin rule + tree walk) on one batch of
+reductions and drafted-logit gather, then the fused slab merge + margin rule + tree walk +
+policy-state update) on one batch of
 seeded synthetic inputs already resident in HBM. The headline workload is the Llama-3.1-8B
 shaped batch-1 verify (H=4096, V=128256, one 60-node EAGLE-style tree, kappa=0.3); the
 32x64-node batch (2048 rows) is measured after it as the MFMA-bound point. Prints one JSON
@@ -199,8 +200,8 @@ def cpu_baseline(w, W, budget_s: float = 12.0) -> dict:
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--config", type=int, default=1)
     ap.add_argument("--secondary", default="3")
     ap.add_argument("--no-cpu", action="store_true")

@@ -40,13 +40,16 @@ extern "C" {
 #define ASV_EHIP       -3        /* a HIP runtime call or kernel launch failed */
 
 /* req_status bits, set on the device for request b. A request with any bit set gets
- * accepted_len = 0, bonus_token = -1, its path entries and accept flags cleared, and its
- * state left unchanged. */
+ * accepted_len = 0, bonus_token = -1, draft_conf = NaN and its state left unchanged; its path
+ * entries and accept flags are cleared, except under ASV_RS_BAD_OFFSETS, where the request's
+ * rows are unknown and neither is written. Row statistics (row_max, row_lse, row_argmax,
+ * drafted_logit) are produced for all N rows in every case. */
 #define ASV_RS_BAD_ROOT    1     /* parent[req_offsets[b]] != -1 */
 #define ASV_RS_BAD_PARENT  2     /* a non-root c has parent outside [req_offsets[b], c) */
 #define ASV_RS_BAD_TOKEN   4     /* a non-root draft_tok outside [0, V) */
-#define ASV_RS_BAD_OFFSETS 16    /* offsets not increasing, req_offsets[0] != 0 or
-                                    req_offsets[B] != N */
+#define ASV_RS_BAD_OFFSETS 16    /* the offsets array is malformed: not strictly
+                                    increasing, req_offsets[0] != 0 or req_offsets[B] != N.
+                                    Set on every request of the batch. */
 #define ASV_RS_BAD_TAU     32    /* tau[b] outside [0, 1] or NaN */
 
 #define ASV_HIST_WINDOW 16

@@ -53,6 +53,7 @@ struct Layout {
   int S = 0;       // vocabulary slabs
   int n_conf = 0;  // draft-confidence chunks per request
   size_t off_rec_m = 0, off_rec_s = 0, off_rec_a = 0, off_conf_m = 0, off_conf_s = 0;
+  size_t off_cnt = 0;  // B + 1 ints: per-request completion counters, then the bad-offsets flag
   size_t bytes = 0;
 };
 
@@ -68,6 +69,7 @@ Layout layout(int B, int N, int V) {
   L.off_rec_a = at;  at += align_up(rec);
   L.off_conf_m = at; at += align_up(conf);
   L.off_conf_s = at; at += align_up(conf);
+  L.off_cnt = at;    at += align_up((size_t)(B + 1) * 4);
   L.bytes = at;
   return L;
 }
@@ -90,7 +92,33 @@ void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStrea
       a->hidden, a->w_lm, a->parent, a->draft_tok, a->req_offsets, a->B, a->N, a->H, a->V,
       L.S, RT, reinterpret_cast<float*>(ws + L.off_rec_m),
       reinterpret_cast<float*>(ws + L.off_rec_s), reinterpret_cast<int32_t*>(ws + L.off_rec_a),
-      a->drafted_logit);
+      a->drafted_logit, reinterpret_cast<int32_t*>(ws + L.off_cnt), a->B + 1);
+}
+
+AcceptArgs accept_args(const asv_verify_args* a, const Layout& L, char* ws, bool conf) {
+  AcceptArgs r;
+  r.B = a->B;
+  r.N = a->N;
+  r.V = a->V;
+  r.off = a->req_offsets;
+  r.parent = a->parent;
+  r.tok = a->draft_tok;
+  r.tau = a->tau;
+  r.row_max = a->row_max;
+  r.row_arg = a->row_argmax;
+  r.g = a->drafted_logit;
+  r.accept = a->accept;
+  r.acc_len = a->accepted_len;
+  r.bonus = a->bonus_token;
+  r.path = a->accepted_path;
+  r.conf_m = reinterpret_cast<const float*>(ws + L.off_conf_m);
+  r.conf_s = reinterpret_cast<const float*>(ws + L.off_conf_s);
+  r.n_conf = conf ? L.n_conf : 0;
+  r.draft_conf = a->draft_conf;
+  r.state = a->state;
+  r.status = a->req_status;
+  r.prm = a->params;
+  return r;
 }
 
 }  // namespace
@@ -182,18 +210,21 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
     }
   }
 
+  const AcceptArgs acc = accept_args(a, L, ws, conf);
+  const float* rec_m = reinterpret_cast<const float*>(ws + L.off_rec_m);
+  const float* rec_s = reinterpret_cast<const float*>(ws + L.off_rec_s);
+  const int32_t* rec_a = reinterpret_cast<const int32_t*>(ws + L.off_rec_a);
+  int32_t* cnt = reinterpret_cast<int32_t*>(ws + L.off_cnt);
+  if (a->B <= kFusedMaxB) {
+    k_merge_accept<<<(a->N + kFinishWaves - 1) / kFinishWaves, kFinishWaves * kWave, 0, s>>>(
+        L.S, rec_m, rec_s, rec_a, a->row_max, a->row_lse, a->row_argmax, cnt, acc);
+    return launch_status("k_merge_accept");
+  }
   k_slab_merge<<<(a->N + kMergeRowsPerBlock - 1) / kMergeRowsPerBlock,
                  kMergeRowsPerBlock * kWave, 0, s>>>(
-      a->N, L.S, reinterpret_cast<const float*>(ws + L.off_rec_m),
-      reinterpret_cast<const float*>(ws + L.off_rec_s),
-      reinterpret_cast<const int32_t*>(ws + L.off_rec_a), a->row_max, a->row_lse, a->row_argmax);
+      a->N, L.S, rec_m, rec_s, rec_a, a->row_max, a->row_lse, a->row_argmax, a->B,
+      a->req_offsets, cnt + a->B);
   if (int rc = launch_status("k_slab_merge")) return rc;
-
-  k_tree_accept<<<a->B, kWave, 0, s>>>(
-      a->B, a->N, a->V, a->req_offsets, a->parent, a->draft_tok, a->tau, a->row_max,
-      a->row_argmax, a->drafted_logit, a->accept, a->accepted_len, a->bonus_token,
-      a->accepted_path, reinterpret_cast<const float*>(ws + L.off_conf_m),
-      reinterpret_cast<const float*>(ws + L.off_conf_s), conf ? L.n_conf : 0, a->draft_conf,
-      a->state, a->req_status, a->params);
+  k_tree_accept<<<a->B, kWave, 0, s>>>(cnt + a->B, acc);
   return launch_status("k_tree_accept");
 }

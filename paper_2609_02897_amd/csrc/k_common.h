@@ -46,4 +46,72 @@ __device__ __forceinline__ Rec rec_wave_reduce(Rec x) {
   return x;
 }
 
+// ---- wave-wide reductions without LDS round trips: rotations within each 16-lane row (DPP
+// row_ror), then the four row results read as scalars. Every lane returns the same value; the
+// combination order is fixed, so results are deterministic.
+template <int N>
+__device__ __forceinline__ int row_ror(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, 0x120 + N, 0xf, 0xf, false);
+}
+template <int N>
+__device__ __forceinline__ float row_ror(float x) {
+  return __int_as_float(row_ror<N>(__float_as_int(x)));
+}
+__device__ __forceinline__ float lane_value(float x, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), l));
+}
+__device__ __forceinline__ int lane_value(int x, int l) { return __builtin_amdgcn_readlane(x, l); }
+
+__device__ __forceinline__ float wave_max(float x) {
+  x = fmaxf(x, row_ror<8>(x));
+  x = fmaxf(x, row_ror<4>(x));
+  x = fmaxf(x, row_ror<2>(x));
+  x = fmaxf(x, row_ror<1>(x));
+  return fmaxf(fmaxf(lane_value(x, 0), lane_value(x, 16)),
+               fmaxf(lane_value(x, 32), lane_value(x, 48)));
+}
+__device__ __forceinline__ float wave_sum(float x) {
+  x += row_ror<8>(x);
+  x += row_ror<4>(x);
+  x += row_ror<2>(x);
+  x += row_ror<1>(x);
+  return (lane_value(x, 0) + lane_value(x, 16)) + (lane_value(x, 32) + lane_value(x, 48));
+}
+__device__ __forceinline__ int wave_min(int x) {
+  x = min(x, row_ror<8>(x));
+  x = min(x, row_ror<4>(x));
+  x = min(x, row_ror<2>(x));
+  x = min(x, row_ror<1>(x));
+  return min(min(lane_value(x, 0), lane_value(x, 16)), min(lane_value(x, 32), lane_value(x, 48)));
+}
+
+// Wave-wide merge of lane records: M = max m, s = sum s_l exp(m_l - M), a = lowest a_l with
+// m_l = M. Lanes with an empty record (m = -inf, s = 0) contribute nothing; at least one lane
+// must hold a finite m.
+__device__ __forceinline__ Rec rec_wave_reduce_dpp(Rec x) {
+  const float M = wave_max(x.m);
+  const float part = x.m == kNegInf ? 0.f : x.s * __builtin_amdgcn_exp2f((x.m - M) * kLog2e);
+  return Rec{M, wave_sum(part), wave_min(x.m == M ? x.a : kNoIndex)};
+}
+
+// Device-coherent access without cache maintenance, for data one workgroup writes and another
+// workgroup of the same launch reads: device-scope relaxed atomic stores write through the
+// XCD's L2 and device-scope relaxed atomic loads miss it, so neither needs the whole-L2
+// write-back / invalidate that a device-scope fence costs.
+__device__ __forceinline__ void st_device(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_device(int32_t* p, int32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_device(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ int32_t ld_device(const int32_t* p) {
+  return __hip_atomic_load(const_cast<int32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Wait until every global store this wave issued has completed (vmcnt(0)).
+__device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0f70); }
+
 }  // namespace asv

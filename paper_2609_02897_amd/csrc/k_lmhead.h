@@ -123,7 +123,8 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
                       const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
                       const int32_t* __restrict__ req_offsets, int B, int N, int H, int V,
                       int S, int RT, float* __restrict__ rec_m, float* __restrict__ rec_s,
-                      int32_t* __restrict__ rec_a, float* __restrict__ drafted_logit) {
+                      int32_t* __restrict__ rec_a, float* __restrict__ drafted_logit,
+                      int32_t* __restrict__ done_cnt, int n_cnt) {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
   constexpr int CPR = C::CPR;
   constexpr int T = C::kThreads;
@@ -132,6 +133,8 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wv = wave % WV, wr = wave / WV;
+  // clear the per-request completion counters of the finishing kernel that follows
+  for (int i = blockIdx.x * T + tid; i < n_cnt; i += gridDim.x * T) done_cnt[i] = 0;
   const int tile = xcd_tile(blockIdx.x, gridDim.x);
   // ORDER 0: consecutive tiles are the row tiles of one slab (W slab shared in L2);
   // ORDER 1: consecutive tiles are the slabs of one row tile (X tile resident in L2).
@@ -320,6 +323,12 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
       const int4 m = s_list[e];
       const int pr = m.y - wr * C::kWaveR, dv = m.z - wv * C::kWaveV;
       if (pr < 0 || pr >= C::kWaveR || dv < 0 || dv >= C::kWaveV) continue;
+      // Keep the accumulator reads below inside this (rarely taken) loop body: without this
+      // the compiler hoists all of them out of the loop into VGPRs and spills.
+#pragma unroll
+      for (int i = 0; i < C::MV; ++i)
+#pragma unroll
+        for (int j = 0; j < C::MR; ++j) asm volatile("" : "+a"(acc[i][j]));
       const int jj = pr >> 5, ii = dv >> 5, mm = dv & 31;
       const int ee = ((mm >> 3) << 2) | (mm & 3);
       const int owner = (pr & 31) + 32 * ((mm >> 2) & 1);

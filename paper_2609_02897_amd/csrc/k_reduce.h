@@ -1,4 +1,3 @@
-// K2: merge of the per-slab LM-head records into each row's max, log-sum-exp and argmax.
 // K4: partial (max, sum-exp) records over the draft logits of each request's root row, the
 //     input of the draft top-1 confidence p_draft(top1) of Sec. 3.3, Eq. (2).
 #pragma once
@@ -7,41 +6,8 @@
 
 namespace asv {
 
-constexpr int kMergeRowsPerBlock = 4;   // one wave per row
 constexpr int kConfChunk = 8192;        // draft logits per K4 workgroup
 constexpr int kConfThreads = 256;
-
-// One wave per tree row: lanes stride over the S slab records, then a butterfly merge.
-// row_lse = M + log(sum_s l_s * exp(m_s - M)); the argmax keeps the lowest index on ties.
-// Each lane issues the loads of kMergeBatch records before merging any, so a row of up to
-// 64 * kMergeBatch slabs costs one memory round trip.
-constexpr int kMergeBatch = 8;
-__global__ __launch_bounds__(kMergeRowsPerBlock * kWave)
-void k_slab_merge(int N, int S, const float* __restrict__ rec_m, const float* __restrict__ rec_s,
-                  const int32_t* __restrict__ rec_a, float* __restrict__ row_max,
-                  float* __restrict__ row_lse, int32_t* __restrict__ row_argmax) {
-  const int lane = threadIdx.x & 63;
-  const int n = blockIdx.x * kMergeRowsPerBlock + (threadIdx.x >> 6);
-  if (n >= N) return;
-  const size_t base = (size_t)n * S;
-  Rec r = rec_empty();
-  for (int s0 = 0; s0 < S; s0 += kWave * kMergeBatch) {
-    Rec batch[kMergeBatch];
-#pragma unroll
-    for (int u = 0; u < kMergeBatch; ++u) {
-      const int s = s0 + u * kWave + lane;
-      batch[u] = s < S ? Rec{rec_m[base + s], rec_s[base + s], rec_a[base + s]} : rec_empty();
-    }
-#pragma unroll
-    for (int u = 0; u < kMergeBatch; ++u) r = rec_merge(r, batch[u]);
-  }
-  r = rec_wave_reduce(r);
-  if (lane == 0) {
-    row_max[n] = r.m;
-    row_lse[n] = r.m + logf(r.s);
-    row_argmax[n] = r.a;
-  }
-}
 
 // Grid (chunks, B). Workgroup (ch, b) reduces draft_logits[root_b][ch*kConfChunk ...] to one
 // (max, sum of exp(q - max)) record. An out-of-range root (malformed offsets, reported by K3)

@@ -82,11 +82,22 @@ def _case(name):
     if name == "root_only_requests":
         trees = [[-1], [-1, 0, 1, 1], [-1], [-1, 0]]
         return custom_workload(name, 64, 700, trees, 0.3, seed=5, w_std=0.16)
+    if name == "many_tiny_requests":
+        # 300 requests of 1 to 5 nodes: one merge workgroup completes several requests and
+        # requests straddle workgroups (fused finishing kernel)
+        trees = [_rand_tree(rng, int(rng.integers(1, 6)), 3, 3) for _ in range(300)]
+        return custom_workload(name, 64, 900, trees, 0.3, seed=6, w_std=0.16)
+    if name == "unfused_large_batch":
+        # more requests than the fused finishing kernel takes: separate merge and walk kernels
+        trees = [_rand_tree(rng, int(rng.integers(1, 4)), 2, 2) for _ in range(1100)]
+        return custom_workload(name, 64, 600, trees, 0.3, seed=7, w_std=0.16,
+                               draft_logits=True)
     raise KeyError(name)
 
 
 CASES = ["tiny_config", "rows64_eagle60_ragged_vocab", "rows128_mixed", "rows256_three_tiles",
-         "deep_chain_and_wide", "root_only_requests"]
+         "deep_chain_and_wide", "root_only_requests", "many_tiny_requests",
+         "unfused_large_batch"]
 
 
 @pytest.mark.parametrize("tau", [None, 0.0, 0.05, 0.3, 1.0])
@@ -234,19 +245,38 @@ def test_malformed_inputs_are_reported(asv, dev):
     assert got["bonus_token"][b] == good_ref["bonus_token"][b]
 
 
-def test_bad_offsets_reported(asv, dev):
+@pytest.mark.parametrize("n_req", [2, 1030])
+@pytest.mark.parametrize("fault", ["last_not_n", "first_not_zero", "decrease", "empty"])
+def test_bad_offsets_reported(asv, dev, n_req, fault):
+    """A malformed offsets array flags every request; the row statistics of all N rows are
+    still produced (on both the fused and the unfused finishing path)."""
     import torch
-    trees = [[-1, 0], [-1, 0, 0]]
+    print(f"[bad offsets] n_req={n_req} fault={fault}", flush=True)
+    rng = np.random.default_rng(12)
+    trees = [[-1, 0], [-1, 0, 0]] + [_rand_tree(rng, 2, 1, 1) for _ in range(n_req - 2)]
     w = custom_workload("badoff", 64, 300, trees, 0.3, seed=12, w_std=0.16)
     W = w.weights()
-    resolve_with_oracle(w, oracle.widen_weights(W))
+    w64 = oracle.widen_weights(W)
+    resolve_with_oracle(w, w64)
+    ref = reference(w, w64)
     d = device_inputs(w, W, dev)
-    d["req_offsets"][2] = w.N - 1              # last offset != N
-    o = asv.verify(d["hidden"], d["w_lm"], d["draft_tok"], d["parent"], d["req_offsets"],
-                   d["tau"])
+    off = d["req_offsets"]
+    if fault == "last_not_n":
+        off[n_req] = w.N - 1
+    elif fault == "first_not_zero":
+        off[0] = 1
+    elif fault == "decrease":
+        off[1] = off[2] + 1  # request 1 runs backwards, request 0 overlaps request 2
+    else:
+        off[1] = off[2]     # request 1 empty
+    o = asv.verify(d["hidden"], d["w_lm"], d["draft_tok"], d["parent"], off, d["tau"])
     torch.cuda.synchronize()
-    st = o.req_status.cpu().numpy()
-    assert st[1] == asv.RS_BAD_OFFSETS and st[0] == 0
+    got = to_host(o)
+    assert np.all(got["req_status"] == asv.RS_BAD_OFFSETS)
+    assert np.all(got["accepted_len"] == 0) and np.all(got["bonus_token"] == -1)
+    assert np.array_equal(got["row_argmax"], ref["row_argmax"]) or \
+        np.all(ref["row_gap"][got["row_argmax"] != ref["row_argmax"]] < 1e-3)
+    assert np.max(np.abs(got["row_max"] - ref["row_max"])) < 2e-3
 
 
 def test_empty_batch(asv, dev):
