@@ -92,12 +92,22 @@ def _case(name):
         trees = [_rand_tree(rng, int(rng.integers(1, 4)), 2, 2) for _ in range(1100)]
         return custom_workload(name, 64, 600, trees, 0.3, seed=7, w_std=0.16,
                                draft_logits=True)
+    if name == "request_over_lds_stage":
+        # a 300-node request (walked from global memory) beside small ones, fused path
+        trees = [_rand_tree(rng, 300, 12, 4), [-1, 0, 0], _rand_tree(rng, 40, 6, 3)]
+        return custom_workload(name, 64, 800, trees, 0.3, seed=8, w_std=0.16,
+                               draft_logits=True)
+    if name == "unfused_with_large_request":
+        # unfused path with one request above the LDS staging limit
+        trees = [_rand_tree(rng, int(rng.integers(1, 4)), 2, 2) for _ in range(1030)]
+        trees[517] = _rand_tree(rng, 290, 10, 4)
+        return custom_workload(name, 64, 600, trees, 0.3, seed=9, w_std=0.16)
     raise KeyError(name)
 
 
 CASES = ["tiny_config", "rows64_eagle60_ragged_vocab", "rows128_mixed", "rows256_three_tiles",
          "deep_chain_and_wide", "root_only_requests", "many_tiny_requests",
-         "unfused_large_batch"]
+         "unfused_large_batch", "request_over_lds_stage", "unfused_with_large_request"]
 
 
 @pytest.mark.parametrize("tau", [None, 0.0, 0.05, 0.3, 1.0])
@@ -133,9 +143,10 @@ def test_determinism(asv, dev):
             assert np.array_equal(a[k], b[k], equal_nan=True), k
 
 
+@pytest.mark.parametrize("name", ["deep_chain_and_wide", "request_over_lds_stage"])
 @pytest.mark.parametrize("max_promotions", [0, 1, 2])
-def test_promotion_cap(asv, dev, max_promotions):
-    w = _case("deep_chain_and_wide")
+def test_promotion_cap(asv, dev, max_promotions, name):
+    w = _case(name)
     W = w.weights()
     w64 = oracle.widen_weights(W)
     resolve_with_oracle(w, w64)
@@ -179,17 +190,19 @@ def test_exact_ties_lowest_index(asv, dev):
     assert got["bonus_token"][0] == ref["bonus_token"][0]
 
 
-def test_history_state_over_steps(asv, dev):
+@pytest.mark.parametrize("n_req", [3, 1030])
+def test_history_state_over_steps(asv, dev, n_req):
     """20 steps through the policy state: EMA, ring wrap at 16, breaker (forced with kappa=1
-    and non-argmax drafts on every other stretch of steps)."""
-    import torch
+    and non-argmax drafts on a stretch of steps). 1030 requests take the unfused path."""
+    print(f"[history] n_req={n_req}", flush=True)
     H, V = 64, 900
     p = oracle.Params()
-    st_ref = [oracle.state_init(p) for _ in range(3)]
-    st_gpu = asv.state_init(3, asv.make_params(), device=dev)
+    st_ref = [oracle.state_init(p) for _ in range(n_req)]
+    st_gpu = asv.state_init(n_req, asv.make_params(), device=dev)
+    hi_size = 12 if n_req < 100 else 4
     for step in range(20):
         rng = np.random.default_rng(100 + step)
-        trees = [_rand_tree(rng, int(rng.integers(2, 12)), 4, 3) for _ in range(3)]
+        trees = [_rand_tree(rng, int(rng.integers(2, hi_size)), 4, 3) for _ in range(n_req)]
         w = custom_workload(f"hist{step}", H, V, trees, 0.3, seed=200 + step, w_std=0.2,
                             draft_logits=True)
         W = w.weights()
@@ -206,9 +219,16 @@ def test_history_state_over_steps(asv, dev):
             w.tau[:] = 1.0
         ref = reference(w, w64, state=st_ref, params=p)
         got = _run(asv, w, W, dev, state=st_gpu)
-        rep = compare(w, ref, got)
-        assert rep.banded_requests == 0
-        st_ref = ref["state"]
+        compare(w, ref, got)
+        # A request whose walk passed a decision inside the float64 tolerance bands may
+        # legitimately accept a different length; its expected state is the oracle's update
+        # applied to the length the GPU accepted.
+        new_ref = list(ref["state"])
+        for b in np.flatnonzero(ref["band_at"] >= 0):
+            n_b = int(w.req_offsets[b + 1] - w.req_offsets[b])
+            new_ref[b] = oracle.state_update(st_ref[b], int(got["accepted_len"][b]), n_b,
+                                             float(ref["draft_conf"][b]), p)
+        st_ref = new_ref
         compare_state(asv.state_fields(st_gpu), st_ref)
         if step == 10:   # fifth consecutive zero-accept step
             assert all(s.breaker == 1 for s in st_ref)
