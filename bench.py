@@ -1,7 +1,7 @@
 """Throughput of the AdaptiveSpec verification hot path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1|3] [--no-cpu] \
-                    [--secondary 3|none]
+                    [--secondary 3|none] | --reference | --copy-calibration MIB
 
 A step is one asv_verify call (LM-head kernel over every tree row with the per-slab
 reductions and drafted-logit gather, then the fused slab merge + margin rule + tree walk +
@@ -197,6 +197,39 @@ def cpu_baseline(w, W, budget_s: float = 12.0) -> dict:
                        f"{dt:.1f} s")
 
 
+def vendor_reference() -> dict:
+    """Context for the roofline fractions: the vendor bf16 GEMM computing only the [N, V]
+    logits of the two bench shapes (no reductions, gather or walk), and the copy bandwidth."""
+    import torch
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev)
+    g.manual_seed(0)
+    H, V = 4096, 128256
+    W = (torch.randn(V, H, device=dev, generator=g) * 0.02).to(torch.bfloat16)
+    out = {}
+
+    def timed(fn, reps):
+        for _ in range(5):
+            fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / reps
+
+    for N in (60, 2048):
+        X = torch.randn(N, H, device=dev, generator=g).to(torch.bfloat16)
+        sec = timed(lambda: torch.matmul(X, W.t()), 50 if N == 60 else 20)
+        out[f"hipblaslt_logits_n{N}_us"] = round(sec * 1e6, 1)
+        out[f"hipblaslt_logits_n{N}_tflops"] = round(2 * N * V * H / sec / 1e12, 1)
+    src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    sec = timed(lambda: dst.copy_(src), 20)
+    out["d2d_copy_1gib_read_plus_write_gbps"] = round(2 * (1 << 30) / sec / 1e9, 1)
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -205,6 +238,10 @@ def main():
     ap.add_argument("--config", type=int, default=1)
     ap.add_argument("--secondary", default="3")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--reference", action="store_true",
+                    help="only time the vendor references on the bench shapes and exit: "
+                         "torch.matmul (hipBLASLt) of the logits alone, and a 1 GiB "
+                         "device-to-device copy")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB five times (the "
                          "reference dispatch for scaling HBM traffic counters) and exit")
@@ -218,6 +255,9 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"copy_calibration_bytes": n, "dispatches": 5}))
+        return
+    if args.reference:
+        print(json.dumps(vendor_reference()))
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU only: the verification path "
