@@ -199,7 +199,7 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
     // each the fastest of a sweep on MI355X for its row range
     case Tile::kRows64: launch_lmhead<256, 64, 4, 1, 64, 2>(a, L, ws, s); break;
     case Tile::kRows128: launch_lmhead<256, 128, 2, 2, 64, 3>(a, L, ws, s); break;
-    case Tile::kRows256: launch_lmhead<256, 256, 2, 2, 32, 4>(a, L, ws, s); break;
+    case Tile::kRows256: launch_lmhead<256, 256, 2, 2, 64, 2>(a, L, ws, s); break;
   }
   if (int rc = launch_status("k_lmhead_partial")) return rc;
   if (a->k1_end_event) {

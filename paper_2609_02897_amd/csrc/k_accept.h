@@ -74,7 +74,7 @@ __device__ __forceinline__ Rec batch_record(const RecBatch& bt) {
   int a = kNoIndex;
 #pragma unroll
   for (int u = 0; u < kMergeBatch; ++u) {
-    sum += bt.s[u] * __builtin_amdgcn_exp2f((bt.m[u] - m) * kLog2e);
+    sum += bt.s[u] * exp2_rel((bt.m[u] - m) * kLog2e);
     a = min(a, bt.m[u] == m ? bt.a[u] : kNoIndex);
   }
   return m == kNegInf ? rec_empty() : Rec{m, sum, a};

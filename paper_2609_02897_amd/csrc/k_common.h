@@ -20,12 +20,17 @@ struct Rec {
 
 __device__ __forceinline__ Rec rec_empty() { return Rec{kNegInf, 0.f, kNoIndex}; }
 
+// Base-2 exponential of the hardware (v_exp_f32). Every use here exponentiates a value taken
+// relative to a maximum (argument <= 0); results below 2^-126 flush to zero, which changes a
+// sum of such terms (at least one of which is 1) by less than 2^-126 relative.
+__device__ __forceinline__ float exp2_rel(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // Merge two records; the argmax keeps the lowest index among equal maxima.
 __device__ __forceinline__ Rec rec_merge(Rec x, Rec y) {
   Rec r;
   r.m = fmaxf(x.m, y.m);
-  float sx = (x.m == kNegInf) ? 0.f : x.s * exp2f((x.m - r.m) * kLog2e);
-  float sy = (y.m == kNegInf) ? 0.f : y.s * exp2f((y.m - r.m) * kLog2e);
+  float sx = (x.m == kNegInf) ? 0.f : x.s * exp2_rel((x.m - r.m) * kLog2e);
+  float sy = (y.m == kNegInf) ? 0.f : y.s * exp2_rel((y.m - r.m) * kLog2e);
   r.s = sx + sy;
   r.a = (x.m > y.m) ? x.a : (y.m > x.m) ? y.a : min(x.a, y.a);
   return r;
@@ -90,7 +95,7 @@ __device__ __forceinline__ int wave_min(int x) {
 // must hold a finite m.
 __device__ __forceinline__ Rec rec_wave_reduce_dpp(Rec x) {
   const float M = wave_max(x.m);
-  const float part = x.m == kNegInf ? 0.f : x.s * __builtin_amdgcn_exp2f((x.m - M) * kLog2e);
+  const float part = x.m == kNegInf ? 0.f : x.s * exp2_rel((x.m - M) * kLog2e);
   return Rec{M, wave_sum(part), wave_min(x.m == M ? x.a : kNoIndex)};
 }
 

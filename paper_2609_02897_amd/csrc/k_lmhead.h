@@ -380,7 +380,7 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
     for (int i = 0; i < C::MV; ++i)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const float t = exp2f(fmaf(acc[i][j][e], kLog2e, -mb));
+        const float t = exp2_rel(fmaf(acc[i][j][e], kLog2e, -mb));
         if constexpr (MASK) sum += entry_v(16 * i + e) < V ? t : 0.f;
         else sum += t;
       }

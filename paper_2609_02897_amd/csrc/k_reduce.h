@@ -28,7 +28,7 @@ void k_draft_conf_partial(int N, int V, const int32_t* __restrict__ req_offsets,
     float s = 0.f;
     const float mb = m * kLog2e;
     for (int v = lo + threadIdx.x; v < hi; v += kConfThreads)
-      s += exp2f(fmaf(row[v], kLog2e, -mb));
+      s += exp2_rel(fmaf(row[v], kLog2e, -mb));
     r = Rec{m, s, 0};
   }
   r = rec_wave_reduce(r);
