@@ -62,6 +62,15 @@ __device__ __forceinline__ void dma16(int lds, int voff, __amdgpu_buffer_rsrc_t 
                : "s"(lds), "v"(voff), "s"(r)
                : "memory", "m0");
 }
+// The same with 4 bytes per lane. Used to pull cache lines into L2 ahead of their stage: the
+// destination is a sink region of LDS that is never read (no register is left to be
+// overwritten by a late load).
+__device__ __forceinline__ void dma4(int lds, int voff, __amdgpu_buffer_rsrc_t r) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+               :
+               : "s"(lds), "v"(voff), "s"(r)
+               : "memory", "m0");
+}
 #pragma clang diagnostic pop
 
 // Wait until at most N vector-memory operations of this wave are outstanding and its LDS
@@ -72,13 +81,14 @@ __device__ __forceinline__ void wait_vm_barrier() {
   asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" : : "n"(N) : "memory");
 }
 
-// wait_vm_barrier<newer * L>() for a run-time newer in [0, 3].
-template <int L>
+// wait_vm_barrier<T + newer * L>() for a run-time newer in [0, 3]: each stage issues L
+// operations, the last T of which (the L2 prefetches) need not have completed.
+template <int L, int T = 0>
 __device__ __forceinline__ void wait_stage_barrier(int newer) {
-  if (newer >= 3) wait_vm_barrier<3 * L>();
-  else if (newer == 2) wait_vm_barrier<2 * L>();
-  else if (newer == 1) wait_vm_barrier<L>();
-  else wait_vm_barrier<0>();
+  if (newer >= 3) wait_vm_barrier<T + 3 * L>();
+  else if (newer == 2) wait_vm_barrier<T + 2 * L>();
+  else if (newer == 1) wait_vm_barrier<T + L>();
+  else wait_vm_barrier<T>();
 }
 
 template <int TV, int TR, int WV, int WR, int BK, int NST>
@@ -117,7 +127,10 @@ __device__ __forceinline__ int xcd_tile(int bid, int G) {
   return xcd * q + min(xcd, rem) + loc;
 }
 
-template <int TV, int TR, int WV, int WR, int BK, int NST, int OCC = 1, int ORDER = 0>
+// PF > 0: every stage also pulls the W lines of stage k + PF into L2 (one 4-byte LDS-sink
+// load per W row), so the stage copies that follow hit L2 instead of waiting on HBM.
+template <int TV, int TR, int WV, int WR, int BK, int NST, int OCC = 1, int ORDER = 0,
+          int PF = 0, bool PFX = false>
 __global__ __launch_bounds__(WV * WR * kWave, OCC)
 void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                       const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
@@ -128,7 +141,18 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
   constexpr int CPR = C::CPR;
   constexpr int T = C::kThreads;
-  __shared__ uint4 smem[C::kLds / 16];
+  constexpr int kPfRows = TV / C::kWaves;             // W rows each wave prefetches
+  constexpr int kPfRowsX = TR / C::kWaves;            // X rows each wave prefetches (PFX)
+  constexpr int kPfW = PF > 0 ? kPfRows / kWave : 0;
+  constexpr int kPfX = PF > 0 && PFX ? kPfRowsX / kWave : 0;
+  constexpr int kPf = kPfW + kPfX;                    // prefetch loads per wave per stage
+  constexpr int kSink = PF > 0 ? C::kWaves * 1024 : 0;
+  constexpr int kGroup = C::kLoads + kPf;             // vector-memory ops per wave per stage
+  static_assert(PF == 0 || (kPfRows % kWave == 0 && (!PFX || kPfRowsX % kWave == 0)),
+                "whole prefetch rows per lane");
+  static_assert((NST - 2) * kGroup + kPf <= 63, "vmcnt range");
+  static_assert(C::kLds + kSink <= 160 * 1024, "LDS per workgroup");
+  __shared__ uint4 smem[(C::kLds + kSink) / 16];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -165,6 +189,7 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
   for (int i = 0; i < C::DW; ++i) w_voff[i] = copy_voff(i * C::kWaves + wave);
 #pragma unroll
   for (int i = 0; i < C::DX; ++i) x_voff[i] = copy_voff(i * C::kWaves + wave);
+  const int KT = H / BK;
   auto issue_stage = [&](int ks) {
     const int k2 = ks * BK * 2;
     const int base = lds0 + (ks % NST) * C::kStage;
@@ -174,6 +199,18 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
 #pragma unroll
     for (int i = 0; i < C::DX; ++i)
       dma16(base + C::kStageW + (i * C::kWaves + wave) * 1024, x_voff[i] + k2, x_rsrc);
+    if constexpr (PF > 0) {
+      // always issued (clamped to the last stage) so every stage has kGroup operations
+      const int kp2 = min(ks + PF, KT - 1) * BK * 2;
+#pragma unroll
+      for (int i = 0; i < kPfW; ++i)
+        dma4(lds0 + C::kLds + wave * 1024,
+             ((wave * kPfW + i) * kWave + lane) * H * 2 + kp2, w_rsrc);
+#pragma unroll
+      for (int i = 0; i < kPfX; ++i)
+        dma4(lds0 + C::kLds + wave * 1024,
+             ((wave * kPfX + i) * kWave + lane) * H * 2 + kp2, x_rsrc);
+    }
   };
 
   // ---- prefetch what the drafted-logit gather needs: the request offsets (to find the end
@@ -205,7 +242,6 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  const int KT = H / BK;
   const int frag_row = lane & 31, frag_half = lane >> 5;
   const uint4* const lds_u4 = smem;
   bf16x8 a0[C::MV], b0[C::MR], a1[C::MV], b1[C::MR];
@@ -233,7 +269,7 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
   // Prologue: fill the whole ring, then wait for stage 0.
   const int pro = min(NST, KT);
   for (int ks = 0; ks < pro; ++ks) issue_stage(ks);
-  wait_stage_barrier<C::kLoads>(pro - 1);
+  wait_stage_barrier<kGroup, kPf>(pro - 1);
   load_frags(0, 0, a0, b0);
 
   // Per stage k with K16 steps s = 0 .. BK/16 - 1: read the fragments of step s + 1 while the
@@ -253,7 +289,7 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
         load_frags(slot, s + 1, na, nb);
       } else if (k + 1 < KT) {
         // stage k+1 must have landed; the copies of the newer stages may stay in flight
-        wait_stage_barrier<C::kLoads>(min(NST - 2, KT - 2 - k));
+        wait_stage_barrier<kGroup, kPf>(min(NST - 2, KT - 2 - k));
         if (k + NST < KT) issue_stage(k + NST);
         load_frags((k + 1) % NST, 0, na, nb);
       }
@@ -261,6 +297,9 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
     }
   }
   static_assert(NS16 % 2 == 0, "fragment double buffer alternates within a stage");
+  // the last L2 prefetches may still be in flight: every LDS copy lands before the epilogue
+  // and before the workgroup can exit
+  if constexpr (PF > 0) asm volatile("s_waitcnt vmcnt(0)" : : : "memory");
   __syncthreads();
 
   // Output block (i, j), register e of a lane holds vocab row
