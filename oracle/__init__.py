@@ -4,7 +4,8 @@ Plain, slow, float64 implementation of what the verification path computes, writ
 paper ("Margins, Not Windows: Training-Free Per-Step Lossy Speculative Decoding"): the target
 LM-head logits of every draft-tree row, the per-row max / argmax / log-sum-exp, the margin rule
 of Sec. 3.2 Eq. (1), the tree walk that promotes mismatches, the draft top-1 confidence of
-Sec. 3.3 Eq. (2) and the rolling acceptance history of Sec. 3.3.
+Sec. 3.3 Eq. (2), the rolling acceptance history of Sec. 3.3 and the tree shape the Draft
+Confidence Score selects (Sec. 3.3, Eq. (2)).
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of ``bench.py`` may
 import it. It shares no code with the HIP path (``paper_2609_02897_amd``); both read inputs from
@@ -12,7 +13,8 @@ import it. It shares no code with the HIP path (``paper_2609_02897_amd``); both 
 
 Parity pins live in ``tests/test_oracle_pins.py``. Functions whose result the paper does not fix
 are marked "parity unpinned" in their docstrings (the walk's sibling choice, the promotion
-count, the acceptance observation, the history reset on a breaker trip).
+count, the acceptance observation, the history reset on a breaker trip, the rounding of the
+tree shape and the starting configuration).
 """
 
 from .asv_oracle import (  # noqa: F401
@@ -27,6 +29,7 @@ from .asv_oracle import (  # noqa: F401
     row_top8,
     state_init,
     state_update,
+    tree_shape,
     verify,
     walk,
     walk_bands,

@@ -211,6 +211,10 @@ class Params:
     rar0: float = 1.0           # initial rolling acceptance rate (not given by the paper)
     breaker_n: int = 5          # consecutive zero-accept steps that trip the breaker (Sec. 3.3)
     max_promotions: int = -1    # -1: no cap on promotions along one walk
+    dcs_divisor: float = 0.5    # d of Sec. 3.3 (d = 0.5 for every run of Sec. 4)
+    shape_lo: tuple = (3, 4, 4)     # (nsteps, topk, ndt) at DCS = 0: wide and shallow
+    shape_hi: tuple = (7, 1, 8)     # at DCS = 1: deep and narrow (Sec. 3.3, Table of configs)
+    shape_start: tuple = (3, 4, 4)  # the starting configuration a breaker trip reverts to
 
 
 @dataclass
@@ -224,6 +228,8 @@ class ReqState:
     steps: int = 0
     hist_mean: float = 1.0
     draft_conf: float = 0.0
+    dcs: float = 0.0
+    shape: tuple = (0, 0, 0)
 
 
 def state_init(p: Params) -> ReqState:
@@ -240,6 +246,9 @@ def state_update(s: ReqState, accepted_len: int, n_nodes: int, conf: Optional[fl
     mean. A request with ``breaker_n`` consecutive zero-accept steps trips the circuit breaker:
     the flag is raised and RAR, the ring and the streak restart (the reset itself is a reading,
     parity unpinned). A root-only tree drafts nothing and only advances ``steps``.
+    Finally the next step's tree shape is chosen from the latest draft confidence (this step's
+    when draft logits were given, else the last one stored) and the updated RAR (Eq. (2),
+    :func:`tree_shape`).
     """
     s = replace(s, hist=list(s.hist))
     if n_nodes > 1:
@@ -263,7 +272,34 @@ def state_update(s: ReqState, accepted_len: int, n_nodes: int, conf: Optional[fl
     s.steps += 1
     if conf is not None:
         s.draft_conf = conf
+    s.dcs, s.shape = tree_shape(s.draft_conf, s.rar, s.breaker, p)
     return s
+
+
+def tree_shape(conf: float, rar: float, breaker: int, p: Params):
+    """Draft Confidence Score and the tree shape it selects (Sec. 3.3, Eq. (2)).
+
+    DCS = p_draft(top1) * RAR, rescaled by the divisor d so that it saturates at 1 once the
+    product reaches d: DCS = min(1, p_draft(top1) * RAR / d). Each member of the triplet
+    (nsteps, topk, ndt) moves linearly from ``shape_lo`` at DCS = 0 to ``shape_hi`` at DCS = 1
+    (depth grows with DCS, branching with 1 - DCS), rounded to the nearest integer with halves
+    going to the lower one (a reading: the paper selects among pre-captured integer triplets
+    without naming the rounding; parity unpinned). A request whose breaker tripped reverts to
+    ``shape_start`` (Sec. 3.3; which triplet is "the starting configuration" is a reading,
+    parity unpinned).
+
+    The score decides integers, so it is evaluated in float32, one rounding per operation, as
+    the library does: DCS = min(1, fl(fl(conf * rar) / d)), x = fl(lo + fl((hi - lo) * DCS)).
+    """
+    f = np.float32
+    dcs = min(f(1.0), f(f(f(conf) * f(rar)) / f(p.dcs_divisor)))
+    if breaker:
+        return float(dcs), tuple(int(v) for v in p.shape_start)
+    shape = []
+    for lo, hi in zip(p.shape_lo, p.shape_hi):
+        x = f(f(lo) + f(f(hi - lo) * dcs))
+        shape.append(int(math.ceil(float(x) - 0.5)))
+    return float(dcs), tuple(shape)
 
 
 def _ring_mean(s: ReqState) -> float:

@@ -358,6 +358,60 @@ def check_breaker(orc):
     assert s.breaker == 0 and s.zero_streak == 1
 
 
+def _shape_by_fractions(conf, rar, d, lo, hi):
+    """Eq. (2) mapping in exact rationals of the float32 inputs: DCS = min(1, conf * rar / d),
+    each member lo + (hi - lo) * DCS, nearest integer with halves down."""
+    f = lambda v: Fraction(float(np.float32(v)))
+    dcs = min(Fraction(1), f(conf) * f(rar) / f(d))
+    out = []
+    for a, b in zip(lo, hi):
+        x = a + (b - a) * dcs
+        n = math.floor(x)
+        out.append(n if x - n <= Fraction(1, 2) else n + 1)
+    return dcs, tuple(out)
+
+
+def check_tree_shape(orc):
+    """Sec. 3.3, Eq. (2): DCS = min(1, p_draft(top1) * RAR / d); depth and node count grow
+    linearly with DCS, branching with 1 - DCS, over (3,4,4) <-> (7,1,8); the breaker returns
+    the starting configuration."""
+    p = orc.Params()
+    assert p.dcs_divisor == 0.5 and tuple(p.shape_lo) == (3, 4, 4) and tuple(p.shape_hi) == (7, 1, 8)
+    # the two ends and saturation at p_draft * RAR >= d
+    assert orc.tree_shape(0.0, 1.0, 0, p) == (0.0, (3, 4, 4))
+    for conf, rar in ((0.5, 1.0), (1.0, 0.5), (0.9, 0.9), (1.0, 1.0)):
+        dcs, shape = orc.tree_shape(conf, rar, 0, p)
+        assert dcs == 1.0 and shape == (7, 1, 8), (conf, rar, shape)
+    # the lattice DCS = k/8 (exact in float32) hits every half-way point of the three ranges
+    for k in range(9):
+        conf = k / 8 * 0.5
+        dcs, shape = orc.tree_shape(conf, 1.0, 0, p)
+        want_dcs, want = _shape_by_fractions(conf, 1.0, 0.5, (3, 4, 4), (7, 1, 8))
+        assert dcs == float(want_dcs) == k / 8 and shape == want, (k, shape, want)
+    assert orc.tree_shape(0.25, 1.0, 0, p)[1] == (5, 2, 6)      # topk 2.5 -> 2
+    # random points against the rational formula, and monotonicity along the score
+    rng = np.random.default_rng(21)
+    prev = None
+    for prod in sorted(rng.uniform(0.0, 0.6, 200)):
+        conf, rar = float(prod), 1.0
+        dcs, shape = orc.tree_shape(conf, rar, 0, p)
+        _, want = _shape_by_fractions(conf, rar, 0.5, (3, 4, 4), (7, 1, 8))
+        assert shape == want, (conf, shape, want)
+        if prev is not None:
+            assert shape[0] >= prev[0] and shape[2] >= prev[2] and shape[1] <= prev[1]
+        prev = shape
+    # a smaller divisor saturates sooner; the breaker reverts to the starting configuration
+    q = orc.Params(dcs_divisor=0.25)
+    assert orc.tree_shape(0.25, 1.0, 0, q)[1] == (7, 1, 8)
+    assert orc.tree_shape(0.9, 0.9, 1, p)[1] == tuple(p.shape_start)
+    # the state update picks the shape from the latest confidence and the updated RAR
+    s = orc.state_init(p)
+    s = orc.state_update(s, 2, 9, 0.4, p)
+    assert s.shape == orc.tree_shape(0.4, s.rar, 0, p)[1] and s.draft_conf == 0.4
+    s = orc.state_update(s, 0, 9, None, p)                # no new confidence: keep the last
+    assert s.shape == orc.tree_shape(0.4, s.rar, 0, p)[1]
+
+
 def check_verify_end_to_end(orc):
     """The composed call against brute force on a tiny batch: exact rational logits, a
     Python-loop max / argmax, the library log-sum-exp and softmax, the walk properties of
@@ -414,5 +468,6 @@ ALL_CHECKS = [
     check_margin_is_probability_ratio, check_exact_match_always_accepted,
     check_kappa_one_is_strict, check_kappa_zero_reaches_leaf, check_walk_properties,
     check_len_monotone_in_kappa, check_promotion_cap, check_draft_confidence,
-    check_ema_closed_form, check_ring_mean, check_breaker, check_verify_end_to_end,
+    check_ema_closed_form, check_ring_mean, check_breaker, check_tree_shape,
+    check_verify_end_to_end,
 ]

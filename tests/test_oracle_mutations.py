@@ -104,12 +104,43 @@ def _update_counts_depth(s, acc_len, n, conf, p):
     return ORIG["state_update"](s, acc_len, n + 1 if n > 1 else n, conf, p)
 
 
+def _shape_uses_ring_mean(s, acc_len, n, conf, p):
+    s = ORIG["state_update"](s, acc_len, n, conf, p)
+    s.dcs, s.shape = orc.tree_shape(s.draft_conf, s.hist_mean, s.breaker, p)
+    return s
+
+
+def _shape_halves_up(conf, rar, breaker, p):
+    f = np.float32
+    dcs = min(f(1.0), f(f(f(conf) * f(rar)) / f(p.dcs_divisor)))
+    if breaker:
+        return float(dcs), tuple(p.shape_start)
+    return float(dcs), tuple(int(math.floor(float(f(f(lo) + f(f(hi - lo) * dcs))) + 0.5))
+                             for lo, hi in zip(p.shape_lo, p.shape_hi))
+
+
+def _shape_ends_swapped(conf, rar, breaker, p):
+    return ORIG["tree_shape"](conf, rar, breaker,
+                              orc.Params(shape_lo=p.shape_hi, shape_hi=p.shape_lo,
+                                         shape_start=p.shape_start,
+                                         dcs_divisor=p.dcs_divisor))
+
+
+def _shape_no_saturation(conf, rar, breaker, p):
+    f = np.float32
+    dcs = f(f(f(conf) * f(rar)) / f(p.dcs_divisor))
+    if breaker:
+        return float(dcs), tuple(p.shape_start)
+    return float(dcs), tuple(int(math.ceil(float(f(f(lo) + f(f(hi - lo) * dcs))) - 0.5))
+                             for lo, hi in zip(p.shape_lo, p.shape_hi))
+
+
 def _widen_truncating(bits):
     return np.asarray(bits, dtype=np.uint16).astype(np.float64)
 
 
 ORIG = {name: getattr(orc, name) for name in
-        ("row_stats", "walk", "state_update", "accept_flags", "logits")}
+        ("row_stats", "walk", "state_update", "accept_flags", "logits", "tree_shape")}
 
 MUTANTS = {
     "accept_uses_own_row": ("accept_flags", _accept_own_row),
@@ -126,6 +157,10 @@ MUTANTS = {
     "breaker_one_early": ("state_update", _update_breaker_early),
     "observation_counts_root": ("state_update", _update_counts_depth),
     "widen_as_integer": ("widen_bf16", _widen_truncating),
+    "shape_from_ring_mean": ("state_update", _shape_uses_ring_mean),
+    "shape_halves_up": ("tree_shape", _shape_halves_up),
+    "shape_ends_swapped": ("tree_shape", _shape_ends_swapped),
+    "shape_not_saturated": ("tree_shape", _shape_no_saturation),
 }
 
 
