@@ -31,7 +31,7 @@
 extern "C" {
 #endif
 
-#define ASV_VERSION 100          /* 1.0.0 */
+#define ASV_VERSION 110          /* 1.1.0 */
 
 /* Return codes. */
 #define ASV_OK          0
@@ -54,7 +54,7 @@ extern "C" {
 
 #define ASV_HIST_WINDOW 16
 
-/* Per-request policy state (Sec. 3.3), caller-owned device memory, 96 bytes, in/out.
+/* Per-request policy state (Sec. 3.3), caller-owned device memory, 112 bytes, in/out.
  * Initialise with asv_state_init(); copy the bytes to checkpoint or resume. */
 typedef struct asv_req_state {
   float   rar;                      /* rolling acceptance rate, an EMA of the accept fraction */
@@ -66,6 +66,10 @@ typedef struct asv_req_state {
   int32_t steps;                    /* verify steps seen */
   float   hist_mean;                /* mean of the filled ring slots (rar0 when empty) */
   float   draft_conf;               /* last p_draft(top1) of Eq. (2), when draft logits given */
+  float   dcs;                      /* Draft Confidence Score of Eq. (2),
+                                       min(1, draft_conf * rar / dcs_divisor) */
+  int32_t shape[3];                 /* (nsteps, topk, ndt) the score selects for the next draft
+                                       tree; the starting configuration after a breaker trip */
 } asv_req_state;
 
 /* Policy parameters (Sec. 3.3 and Appendix B). */
@@ -75,6 +79,12 @@ typedef struct asv_params {
   int32_t breaker_n;       /* zero-accept steps that trip the breaker, >= 1; paper: 5 */
   int32_t max_promotions;  /* mismatches one walk may promote; -1 = no limit, 1 = only the
                               first mismatch position */
+  float   dcs_divisor;     /* d of Eq. (2): the score saturates once p_draft * RAR reaches d,
+                              > 0; paper: 0.5 */
+  int32_t shape_lo[3];     /* (nsteps, topk, ndt) at score 0, each >= 1; paper: (3, 4, 4) */
+  int32_t shape_hi[3];     /* the same at score 1; paper: (7, 1, 8) */
+  int32_t shape_start[3];  /* the starting configuration: the shape before the first step and
+                              after a breaker trip; (3, 4, 4) here */
 } asv_params;
 
 /* Arguments of asv_verify. Shapes use B requests and N tree rows in total. Request b owns the
@@ -131,8 +141,20 @@ const char *asv_last_error(void);
  * overwritten by every call. Returns ASV_EINVAL for sizes asv_verify would reject. */
 int asv_workspace_bytes(int32_t B, int32_t N, int32_t H, int32_t V, uint64_t *bytes);
 
+/* Tree shape for the next draft (Sec. 3.3, Eq. (2)). For each request b: if conf is not NULL,
+ * state[b].draft_conf = conf[b] (a fresh p_draft(top1), e.g. from the next step's first draft
+ * forward); then state[b].dcs = min(1, draft_conf * rar / d) and state[b].shape = each member
+ * of the triplet moved linearly from shape_lo (score 0) to shape_hi (score 1), rounded to the
+ * nearest integer with halves down, or shape_start when state[b].breaker is set. The score is
+ * computed in float32 with one rounding per operation. asv_verify applies the same rule after
+ * its history update, with the step's own draft confidence. conf: [B] device floats or NULL;
+ * state: [B] device, in/out. Enqueued on `stream`. Returns ASV_EINVAL for B < 0, a NULL state
+ * with B > 0 or invalid parameters, ASV_EHIP if the launch fails. */
+int asv_tree_policy(const float *conf, asv_req_state *state, int32_t B, const asv_params *p,
+                    void *stream);
+
 /* Fill state[0..B) with the initial policy state for params *p (rar = hist_mean = rar0,
- * empty ring, zero counters) on `stream`. */
+ * empty ring, zero counters, dcs 0, shape = shape_start) on `stream`. */
 int asv_state_init(asv_req_state *state, int32_t B, const asv_params *p, void *stream);
 
 /* One verification step for a batch (Sec. 3.2, Eq. (1); Sec. 3.3, Eq. (2)):

@@ -233,7 +233,8 @@ class ReqState:
 
 
 def state_init(p: Params) -> ReqState:
-    return ReqState(rar=p.rar0, hist_mean=p.rar0)
+    """Before the first step a request drafts with the starting configuration."""
+    return ReqState(rar=p.rar0, hist_mean=p.rar0, shape=tuple(p.shape_start))
 
 
 def state_update(s: ReqState, accepted_len: int, n_nodes: int, conf: Optional[float],

@@ -42,9 +42,13 @@ class AsvError(RuntimeError):
 
 
 def make_params(alpha: float = 0.3, rar0: float = 1.0, breaker_n: int = 5,
-                max_promotions: int = -1) -> AsvParams:
-    """Policy parameters; defaults are the paper's (EMA alpha 0.3, breaker after 5 steps)."""
-    return AsvParams(alpha, rar0, breaker_n, max_promotions)
+                max_promotions: int = -1, dcs_divisor: float = 0.5,
+                shape_lo=(3, 4, 4), shape_hi=(7, 1, 8), shape_start=(3, 4, 4)) -> AsvParams:
+    """Policy parameters; defaults are the paper's (EMA alpha 0.3, breaker after 5 steps,
+    DCS divisor 0.5, tree shapes (3,4,4) <-> (7,1,8))."""
+    tri = ctypes.c_int32 * 3
+    return AsvParams(alpha, rar0, breaker_n, max_promotions, dcs_divisor, tri(*shape_lo),
+                     tri(*shape_hi), tri(*shape_start))
 
 
 def _check(code: int):
@@ -76,8 +80,23 @@ def alloc_workspace(B: int, N: int, H: int, V: int, device):
     return ws
 
 
+def tree_policy(state, conf=None, params: Optional[AsvParams] = None):
+    """``asv_tree_policy``: the Draft Confidence Score and tree shape of every request, from a
+    fresh draft confidence ``conf`` (f32 [B], optional) and the state's RAR (in place)."""
+    import torch
+    B = state.shape[0]
+    _need(state, "state", torch.uint8, (B, STATE_BYTES))
+    if conf is not None:
+        _need(conf, "conf", torch.float32, (B,))
+    p = params or make_params()
+    _check(load().asv_tree_policy(_ptr(conf), _ptr(state), B, ctypes.byref(p),
+                                  _stream_handle(state.device)))
+    return state
+
+
 def state_init(B: int, params: Optional[AsvParams] = None, device="cuda"):
-    """Per-request policy state, one 96-byte ``asv_req_state`` per row of a [B, 96] u8 tensor."""
+    """Per-request policy state, one 112-byte ``asv_req_state`` per row of a [B, 112] u8
+    tensor."""
     import torch
     p = params or make_params()
     st = torch.empty((B, STATE_BYTES), dtype=torch.uint8, device=device)
@@ -118,7 +137,7 @@ def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None,
     """One verification step through ``asv_verify`` on torch's current stream.
 
     hidden bf16 [N, H]; w_lm bf16 [V, H]; draft_tok, parent int32 [N]; req_offsets int32
-    [B+1]; tau float32 [B]; draft_logits float32 [N, V] or None; state u8 [B, 96] (in/out) or
+    [B+1]; tau float32 [B]; draft_logits float32 [N, V] or None; state u8 [B, 112] (in/out) or
     None. ``out`` and ``workspace`` may be passed to reuse buffers. ``k1_events`` is an
     optional pair of raw hipEvent_t handles recorded around the LM-head kernel.
     """

@@ -14,7 +14,7 @@ HIST_WINDOW = 16
 
 # Every entry point include/asv.h declares.
 EXPORTS = ("asv_version", "asv_status_string", "asv_last_error", "asv_workspace_bytes",
-           "asv_state_init", "asv_verify")
+           "asv_tree_policy", "asv_state_init", "asv_verify")
 
 
 class AsvReqState(ctypes.Structure):
@@ -22,12 +22,15 @@ class AsvReqState(ctypes.Structure):
                 ("hist_head", ctypes.c_int32), ("hist_count", ctypes.c_int32),
                 ("zero_streak", ctypes.c_int32), ("breaker", ctypes.c_int32),
                 ("steps", ctypes.c_int32), ("hist_mean", ctypes.c_float),
-                ("draft_conf", ctypes.c_float)]
+                ("draft_conf", ctypes.c_float), ("dcs", ctypes.c_float),
+                ("shape", ctypes.c_int32 * 3)]
 
 
 class AsvParams(ctypes.Structure):
     _fields_ = [("alpha", ctypes.c_float), ("rar0", ctypes.c_float),
-                ("breaker_n", ctypes.c_int32), ("max_promotions", ctypes.c_int32)]
+                ("breaker_n", ctypes.c_int32), ("max_promotions", ctypes.c_int32),
+                ("dcs_divisor", ctypes.c_float), ("shape_lo", ctypes.c_int32 * 3),
+                ("shape_hi", ctypes.c_int32 * 3), ("shape_start", ctypes.c_int32 * 3)]
 
 
 _P = ctypes.c_void_p
@@ -46,7 +49,7 @@ class AsvVerifyArgs(ctypes.Structure):
                 ("k1_begin_event", _P), ("k1_end_event", _P)]
 
 
-assert ctypes.sizeof(AsvReqState) == 96
+assert ctypes.sizeof(AsvReqState) == 112
 
 
 class LibraryMissing(RuntimeError):
@@ -81,6 +84,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.asv_last_error.argtypes = []
     lib.asv_workspace_bytes.restype = ctypes.c_int
     lib.asv_workspace_bytes.argtypes = [ctypes.c_int32] * 4 + [ctypes.POINTER(ctypes.c_uint64)]
+    lib.asv_tree_policy.restype = ctypes.c_int
+    lib.asv_tree_policy.argtypes = [_P, _P, ctypes.c_int32, ctypes.POINTER(AsvParams), _P]
     lib.asv_state_init.restype = ctypes.c_int
     lib.asv_state_init.argtypes = [_P, ctypes.c_int32, ctypes.POINTER(AsvParams), _P]
     lib.asv_verify.restype = ctypes.c_int

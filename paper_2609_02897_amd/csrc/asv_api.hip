@@ -83,6 +83,15 @@ bool sizes_ok(int B, int N, int H, int V) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+bool params_ok(const asv_params& p) {
+  if (!(p.alpha > 0.f && p.alpha <= 1.f) || p.breaker_n < 1 || p.max_promotions < -1)
+    return false;
+  if (!(p.dcs_divisor > 0.f && p.dcs_divisor < __builtin_inff())) return false;
+  for (int k = 0; k < 3; ++k)
+    if (p.shape_lo[k] < 1 || p.shape_hi[k] < 1 || p.shape_start[k] < 1) return false;
+  return true;
+}
+
 template <int TV, int TR, int WV, int WR, int BK, int NST, int PF = 0>
 void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStream_t s) {
   static_assert(TV == kSlab, "tiles span exactly one record slab");
@@ -149,12 +158,22 @@ extern "C" int asv_workspace_bytes(int32_t B, int32_t N, int32_t H, int32_t V,
 
 extern "C" int asv_state_init(asv_req_state* state, int32_t B, const asv_params* p,
                               void* stream) {
-  if (B < 0 || !p || (B > 0 && !state)) return ASV_EINVAL;
+  if (B < 0 || !p || (B > 0 && !state) || !params_ok(*p)) return ASV_EINVAL;
   if (B == 0) return ASV_OK;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   (void)hipGetLastError();
   k_state_init<<<(B + 255) / 256, 256, 0, s>>>(state, B, *p);
   return launch_status("k_state_init");
+}
+
+extern "C" int asv_tree_policy(const float* conf, asv_req_state* state, int32_t B,
+                               const asv_params* p, void* stream) {
+  if (B < 0 || !p || (B > 0 && !state) || !params_ok(*p)) return ASV_EINVAL;
+  if (B == 0) return ASV_OK;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  k_tree_policy<<<(B + 255) / 256, 256, 0, s>>>(conf, state, B, *p);
+  return launch_status("k_tree_policy");
 }
 
 extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t workspace_bytes,
@@ -166,9 +185,7 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
       !a->accepted_len || !a->bonus_token || !a->accepted_path || !a->req_status)
     return ASV_EINVAL;
   if (!aligned16(a->hidden) || !aligned16(a->w_lm)) return ASV_EINVAL;
-  const asv_params& p = a->params;
-  if (!(p.alpha > 0.f && p.alpha <= 1.f) || p.breaker_n < 1 || p.max_promotions < -1)
-    return ASV_EINVAL;
+  if (!params_ok(a->params)) return ASV_EINVAL;
   const Layout L = layout(a->B, a->N, a->V);
   if (!workspace || workspace_bytes < L.bytes ||
       (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)

@@ -12,7 +12,8 @@
 // and counts against params.max_promotions (-1 = unlimited). The bonus token is the argmax of
 // the last accepted node's row (greedy decoding).
 // State (Sec. 3.3): EMA of the accept fraction len / (n - 1), a 16-slot history ring, the
-// zero-accept streak and the circuit breaker.
+// zero-accept streak and the circuit breaker, then the Draft Confidence Score and the tree
+// shape it selects for the next draft (Eq. (2)).
 #pragma once
 
 #include "k_common.h"
@@ -139,7 +140,25 @@ struct WalkSmem {
   uint8_t ok[kWaveStage];     // Eq. (1) verdict of each node
   asv_req_state st;
 };
-static_assert(sizeof(asv_req_state) == 24 * 4, "state layout");
+constexpr int kStateWords = 28;
+static_assert(sizeof(asv_req_state) == kStateWords * 4, "state layout");
+static_assert(kStateWords <= kWave, "one state word per lane");
+
+// Draft Confidence Score and the tree shape it selects (Sec. 3.3, Eq. (2)):
+// dcs = min(1, draft_conf * rar / d); each member of (nsteps, topk, ndt) moves linearly from
+// shape_lo at score 0 to shape_hi at score 1 and is rounded to the nearest integer, halves
+// down; a request whose breaker tripped takes the starting configuration. The score decides
+// integers, so every operation is rounded on its own (no contraction into fused operations).
+__device__ __forceinline__ void tree_shape(asv_req_state& q, const asv_params& prm) {
+  const float dcs = fminf(1.f, __fdiv_rn(__fmul_rn(q.draft_conf, q.rar), prm.dcs_divisor));
+  q.dcs = dcs;
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    const float x = __fadd_rn((float)prm.shape_lo[k],
+                              __fmul_rn((float)(prm.shape_hi[k] - prm.shape_lo[k]), dcs));
+    q.shape[k] = q.breaker ? prm.shape_start[k] : (int)ceilf(x - 0.5f);
+  }
+}
 
 // Per-lane registers of a request's staged inputs (parent, token, drafted logit), loaded ahead
 // of the walk and written to LDS later.
@@ -259,9 +278,10 @@ __device__ __forceinline__ void finish_request(const AcceptArgs& a, int b, int n
     }
     q.steps = q.steps + 1;
     if (a.n_conf > 0) q.draft_conf = conf;
+    tree_shape(q, a.prm);
   }
   wave_lds_sync();
-  if (lane < 24)
+  if (lane < kStateWords)
     reinterpret_cast<uint32_t*>(a.state + b)[lane] = reinterpret_cast<const uint32_t*>(&q)[lane];
 }
 
@@ -287,7 +307,7 @@ __device__ __forceinline__ void stage_inputs(const AcceptArgs& a, int b, int lo,
                                              WalkInputs& in) {
   stage_load(a, lo, lane, in.r);
   in.kappa = a.tau[b];
-  in.st_word = (a.state && lane < 24) ? reinterpret_cast<const uint32_t*>(a.state + b)[lane] : 0u;
+  in.st_word = (a.state && lane < kStateWords) ? reinterpret_cast<const uint32_t*>(a.state + b)[lane] : 0u;
   in.conf = conf_partials(a, b, lane);
 }
 
@@ -318,7 +338,7 @@ __device__ __forceinline__ void accept_staged(const AcceptArgs& a, int b, int lo
       sm.best[i] = 0;
     }
   }
-  if (a.state && lane < 24) reinterpret_cast<uint32_t*>(&sm.st)[lane] = in.st_word;
+  if (a.state && lane < kStateWords) reinterpret_cast<uint32_t*>(&sm.st)[lane] = in.st_word;
   wave_lds_sync();
 
   const int st = (!(kappa >= 0.f && kappa <= 1.f) ? ASV_RS_BAD_TAU : 0) | tree_bits;
@@ -387,7 +407,7 @@ __device__ __forceinline__ void accept_global(const AcceptArgs& a, int b, int lo
   const int n = hi - lo;
   const float kappa = a.tau[b];
   const Rec conf_r = conf_partials(a, b, lane);
-  if (a.state && lane < 24)
+  if (a.state && lane < kStateWords)
     reinterpret_cast<uint32_t*>(&sm.st)[lane] =
         reinterpret_cast<const uint32_t*>(a.state + b)[lane];
   auto Mr = [&](int r) { return ld_device(a.row_max + r); };
@@ -603,6 +623,19 @@ __global__ void k_state_init(asv_req_state* state, int B, asv_params prm) {
   s->steps = 0;
   s->hist_mean = prm.rar0;
   s->draft_conf = 0.f;
+  s->dcs = 0.f;
+  for (int k = 0; k < 3; ++k) s->shape[k] = prm.shape_start[k];
+}
+
+// Grid-stride over requests: optional fresh draft confidence, then the tree shape.
+__global__ void k_tree_policy(const float* __restrict__ conf, asv_req_state* state, int B,
+                              asv_params prm) {
+  for (int b = blockIdx.x * blockDim.x + threadIdx.x; b < B; b += gridDim.x * blockDim.x) {
+    asv_req_state q = state[b];
+    if (conf) q.draft_conf = conf[b];
+    tree_shape(q, prm);
+    state[b] = q;
+  }
 }
 
 }  // namespace asv

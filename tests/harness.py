@@ -36,7 +36,7 @@ def device_inputs(w: Workload, W: np.ndarray, dev, tau=None):
     import torch
 
     def t(x):
-        return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+        return torch.from_numpy(np.array(x, copy=True, order="C")).to(dev)
 
     return dict(
         hidden=t(w.hidden.view(np.int16)).view(torch.bfloat16),
@@ -126,7 +126,7 @@ def compare(w: Workload, ref: dict, got: dict, rows=None) -> Report:
     return rep
 
 
-def compare_state(gpu_states, ref_states, banded_requests=()):
+def compare_state(gpu_states, ref_states, banded_requests=(), params=None):
     for b, (g, r) in enumerate(zip(gpu_states, ref_states)):
         if b in banded_requests:
             continue
@@ -138,3 +138,8 @@ def compare_state(gpu_states, ref_states, banded_requests=()):
         for i in range(16):
             assert abs(g.hist[i] - r.hist[i]) < TOL_STATE, (b, i)
         assert abs(g.draft_conf - r.draft_conf) < 1e-5, (b, g.draft_conf, r.draft_conf)
+        # Eq. (2): the score within tolerance of the float64 state's; the integer shape is
+        # the oracle's float32 decision taken on the library's own confidence and RAR
+        assert abs(g.dcs - r.dcs) < TOL_STATE, (b, g.dcs, r.dcs)
+        assert tuple(g.shape) == oracle.tree_shape(g.draft_conf, g.rar, g.breaker,
+                                                   params or oracle.Params())[1], (b,)

@@ -36,16 +36,33 @@ def test_exports(lib):
 
 
 def test_version_and_status(lib):
-    assert lib.asv_version() == 100
+    assert lib.asv_version() == 110
     for code in (0, -1, -2, -3, 7):
         assert lib.asv_status_string(code)
 
 
 def test_struct_layouts():
-    assert ctypes.sizeof(_abi.AsvReqState) == 96
-    assert ctypes.sizeof(_abi.AsvParams) == 16
-    # 4 ints, 18 pointers, params (16 B), 2 event pointers
-    assert ctypes.sizeof(_abi.AsvVerifyArgs) == 16 + 18 * 8 + 16 + 2 * 8
+    assert ctypes.sizeof(_abi.AsvReqState) == 112
+    assert ctypes.sizeof(_abi.AsvParams) == 56
+    # 4 ints, 18 pointers, params (56 B), 2 event pointers
+    assert ctypes.sizeof(_abi.AsvVerifyArgs) == 16 + 18 * 8 + 56 + 2 * 8
+
+
+def test_param_and_policy_checks_on_host(lib):
+    """Invalid parameters are rejected before anything is enqueued (no GPU needed)."""
+    state = ctypes.c_void_p(0x1000)      # never dereferenced: the call must fail first
+    good = asv.make_params()
+    assert lib.asv_tree_policy(None, None, 0, ctypes.byref(good), None) == asv.ASV_OK
+    assert lib.asv_tree_policy(None, None, 3, ctypes.byref(good), None) == asv.ASV_EINVAL
+    assert lib.asv_tree_policy(None, state, -1, ctypes.byref(good), None) == asv.ASV_EINVAL
+    for bad in (asv.make_params(dcs_divisor=0.0), asv.make_params(dcs_divisor=-1.0),
+                asv.make_params(dcs_divisor=float("nan")),
+                asv.make_params(dcs_divisor=float("inf")),
+                asv.make_params(shape_lo=(0, 4, 4)), asv.make_params(shape_hi=(7, 0, 8)),
+                asv.make_params(shape_start=(3, 4, -1)), asv.make_params(alpha=0.0),
+                asv.make_params(breaker_n=0), asv.make_params(max_promotions=-2)):
+        assert lib.asv_tree_policy(None, state, 4, ctypes.byref(bad), None) == asv.ASV_EINVAL
+        assert lib.asv_state_init(state, 4, ctypes.byref(bad), None) == asv.ASV_EINVAL
 
 
 def test_workspace_bytes(lib):

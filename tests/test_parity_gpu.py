@@ -236,6 +236,49 @@ def test_history_state_over_steps(asv, dev, n_req):
             assert all(s.breaker == 0 and s.zero_streak == step - 5 for s in st_ref)
 
 
+def test_tree_policy_entry_point(asv, dev):
+    """asv_tree_policy against the oracle's float32 decision (Sec. 3.3, Eq. (2)): fresh
+    confidences including exact half-way points of the shape ranges, the stored confidence when
+    none is given, a non-default divisor and range, and breaker-flagged requests."""
+    import ctypes
+    import torch
+    B = 600
+    rng = np.random.default_rng(31)
+    conf = rng.uniform(0.0, 1.0, B).astype(np.float32)
+    conf[:17] = np.arange(17, dtype=np.float32) / 32.0          # DCS = k/16 at RAR 1, d 0.5
+    for params in (oracle.Params(),
+                   oracle.Params(dcs_divisor=0.3, shape_lo=(2, 5, 3), shape_hi=(9, 1, 12),
+                                 shape_start=(4, 2, 6))):
+        cp = asv.make_params(dcs_divisor=params.dcs_divisor, shape_lo=params.shape_lo,
+                             shape_hi=params.shape_hi, shape_start=params.shape_start)
+        st = asv.state_init(B, cp, device=dev)
+        raw = st.cpu().numpy().copy()
+        # set RAR and the breaker flag on the host: rar is word 0, breaker word 20
+        words = raw.view(np.int32).reshape(B, -1)
+        fl = raw.view(np.float32).reshape(B, -1)
+        rar = rng.uniform(0.0, 1.0, B).astype(np.float32)
+        rar[:17] = 1.0
+        fl[:, 0] = rar
+        brk = (rng.random(B) < 0.1).astype(np.int32)
+        brk[:17] = 0
+        words[:, 20] = brk
+        st.copy_(torch.from_numpy(raw).to(dev))
+        asv.tree_policy(st, torch.from_numpy(conf).to(dev), cp)
+        torch.cuda.synchronize()
+        got = asv.state_fields(st)
+        for b in range(B):
+            dcs, shape = oracle.tree_shape(float(conf[b]), float(rar[b]), int(brk[b]), params)
+            assert got[b].draft_conf == conf[b] and got[b].dcs == np.float32(dcs), b
+            assert tuple(got[b].shape) == shape, (b, tuple(got[b].shape), shape)
+        # without a fresh confidence the stored one is used
+        asv.tree_policy(st, None, cp)
+        torch.cuda.synchronize()
+        again = asv.state_fields(st)
+        assert all(tuple(a.shape) == tuple(g.shape) and a.dcs == g.dcs
+                   for a, g in zip(again, got))
+    assert ctypes.sizeof(asv.AsvReqState) == asv.STATE_BYTES == 112
+
+
 def test_malformed_inputs_are_reported(asv, dev):
     """Bad trees, tokens, thresholds and offsets set req_status bits; other requests are
     unaffected and nothing faults."""
