@@ -147,14 +147,21 @@ def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents):
     return res, w, W
 
 
-def roofline(r: dict) -> dict:
+def roofline(r: dict, ceilings: dict = None) -> dict:
+    """Roofline of K1 against the published peak; with ``ceilings`` (measured_ceilings) also
+    against the peak a microbenchmark reaches on this GPU."""
     bound_hbm = r["bytes_alg"] / (HBM_PEAK_GBS * 1e9) >= r["flops_alg"] / (BF16_PEAK_TFLOPS * 1e12)
     if bound_hbm:
         ro = dict(bound="hbm", achieved=round(r["hbm_gbs"], 1), peak=HBM_PEAK_GBS, unit="GB/s",
                   frac=round(r["hbm_gbs"] / HBM_PEAK_GBS, 4))
+        measured = (ceilings or {}).get("stream_read_gbps")
     else:
         ro = dict(bound="mfma", achieved=round(r["mfma_tflops"], 1), peak=BF16_PEAK_TFLOPS,
                   unit="TFLOP/s", frac=round(r["mfma_tflops"] / BF16_PEAK_TFLOPS, 4))
+        measured = (ceilings or {}).get("mfma_bf16_tflops")
+    if measured:
+        ro["measured_peak"] = measured
+        ro["frac_of_measured"] = round(ro["achieved"] / measured, 4)
     ro["kernel"] = "k_lmhead_partial"
     ro["k1_avg_us"] = round(1e3 * r["k1_avg_ms"], 2)
     ro["traffic"] = measured_traffic(r["cfg"])
@@ -195,6 +202,48 @@ def cpu_baseline(w, W, budget_s: float = 12.0) -> dict:
                 sample=f"{n} full verify steps of the headline workload ({w.N} rows each; "
                        f"float64 logits via BLAS, weights pre-widened outside the timing), "
                        f"{dt:.1f} s")
+
+
+def measured_ceilings(dev) -> dict:
+    """Achievable peaks on this GPU from the microbenchmark library (include/asv_microbench.h):
+    a streaming read of 2 GiB (larger than the 256 MB last-level cache), best of two grid
+    sizes, and a register-only bf16 MFMA loop on every SIMD. Timed with HIP events on the
+    stream the kernels are launched on."""
+    import torch
+    torch.cuda.init()
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_02897_amd", "libasv_microbench.so"))
+    lib.asvb_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p,
+                                     ctypes.c_int32, ctypes.c_void_p]
+    lib.asvb_mfma_loop.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                   ctypes.c_void_p]
+    stream = torch.cuda.current_stream(dev)
+    handle = stream.cuda_stream
+
+    def timed(launch, reps):
+        for _ in range(3):
+            assert launch() == 0
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            assert launch() == 0
+        b.record(stream)
+        b.synchronize()
+        return a.elapsed_time(b) * 1e-3 / reps
+
+    nbytes = 2 << 30
+    buf = torch.full((nbytes // 4,), 0x01020304, dtype=torch.int32, device=dev)
+    sink = torch.zeros(1 << 16, dtype=torch.int32, device=dev)
+    best = 0.0
+    for grid in (1024, 2048):
+        sec = timed(lambda: lib.asvb_stream_read(buf.data_ptr(), nbytes, sink.data_ptr(),
+                                                 grid, handle), 10)
+        best = max(best, nbytes / sec / 1e9)
+    del buf
+    grid, iters = 256, 16384
+    fsink = torch.zeros(grid * 256, dtype=torch.float32, device=dev)
+    sec = timed(lambda: lib.asvb_mfma_loop(fsink.data_ptr(), iters, grid, handle), 5)
+    tflops = grid * 4 * iters * 8 * 32768 / sec / 1e12
+    return {"stream_read_gbps": round(best, 1), "mfma_bf16_tflops": round(tflops, 1)}
 
 
 def vendor_reference() -> dict:
@@ -257,7 +306,10 @@ def main():
         print(json.dumps({"copy_calibration_bytes": n, "dispatches": 5}))
         return
     if args.reference:
-        print(json.dumps(vendor_reference()))
+        import torch
+        ref = vendor_reference()
+        ref.update(measured_ceilings(torch.device("cuda:0")))
+        print(json.dumps(ref))
         return
     if args.gpus != 1:
         print(json.dumps({"error": "this build measures one GPU only: the verification path "
@@ -282,7 +334,7 @@ def main():
         "data": "synthetic (seeded bf16 W~N(0,0.02), hidden~N(0,1), EAGLE-style trees)",
         "config": {"workload": r["name"], "H": r["H"], "V": r["V"], "rows": r["N"],
                    "requests": r["B"], "tau": r["tau"], "parallelism": "single GPU"},
-        "roofline": roofline(r),
+        "roofline": None,
     }
     if args.secondary != "none" and int(args.secondary) != args.config:
         del w, W
@@ -292,10 +344,18 @@ def main():
               file=sys.stderr, flush=True)
         line["secondary"] = {"workload": r2["name"], "rows": r2["N"], "requests": r2["B"],
                              "value": round(r2["value"], 1), "unit": "nodes/s",
-                             "ms_per_step": round(r2["ms_per_step"], 4),
-                             "roofline": roofline(r2)}
+                             "ms_per_step": round(r2["ms_per_step"], 4)}
         w, _ = load_workload(args.config)
         W = w.weights()
+    try:
+        ceilings = measured_ceilings(dev)
+        print(f"# measured ceilings: {ceilings}", file=sys.stderr, flush=True)
+    except OSError as e:      # microbenchmark library not built: published peaks only
+        print(f"# measured ceilings unavailable: {e}", file=sys.stderr, flush=True)
+        ceilings = None
+    line["roofline"] = roofline(r, ceilings)
+    if "secondary" in line:
+        line["secondary"]["roofline"] = roofline(r2, ceilings)
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(w, W)
     print(json.dumps(line), flush=True)

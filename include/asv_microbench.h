@@ -1,0 +1,34 @@
+/* Achievable-peak microbenchmarks for MI355X (gfx950), measurement only: they give the
+ * measured ceilings that the verification kernels' roofline fractions are read against, next
+ * to the published peaks. Not part of the verification path; libasv_microbench.so is a
+ * separate library. Each call enqueues one kernel on `stream` (a hipStream_t) and returns 0,
+ * or -1 for invalid arguments, -3 if the launch fails.
+ */
+#ifndef ASV_MICROBENCH_H_
+#define ASV_MICROBENCH_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Streaming read of `bytes` bytes of device memory at `buf` (16-byte aligned, bytes a multiple
+ * of 16): `grid` workgroups of 256 threads, each reading one contiguous chunk with 16-byte
+ * loads, eight in flight per lane, folded into one word written to sink[workgroup] only when
+ * it equals a constant that random data never produce (so the loads cannot be removed).
+ * sink: [grid] device words. Bytes moved: `bytes`. */
+int asvb_stream_read(const void *buf, uint64_t bytes, uint32_t *sink, int32_t grid,
+                     void *stream);
+
+/* Dense bf16 MFMA loop: `grid` workgroups of 256 threads; each wave runs `iters` rounds of
+ * eight independent v_mfma_f32_32x32x16_bf16 on register operands (no memory traffic) and
+ * writes one float per lane to sink[(workgroup * 256) + thread] at the end.
+ * sink: [grid * 256] device floats. FLOPs: grid * 4 * iters * 8 * 32768. */
+int asvb_mfma_loop(float *sink, int32_t iters, int32_t grid, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ASV_MICROBENCH_H_ */

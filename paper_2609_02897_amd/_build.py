@@ -12,6 +12,9 @@ HEADERS = [os.path.join(ROOT, "include", "asv.h")] + [
     os.path.join(_HERE, "csrc", f) for f in ("k_common.h", "k_lmhead.h", "k_reduce.h",
                                                "k_accept.h")]
 OUT = os.path.join(_HERE, "libasv.so")
+# measurement-only library (achievable-peak microbenchmarks), separate from libasv
+MICROBENCH_SOURCES = [os.path.join(_HERE, "csrc", "microbench.hip")]
+MICROBENCH_OUT = os.path.join(_HERE, "libasv_microbench.so")
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
@@ -27,10 +30,11 @@ def hipcc() -> str:
     return cand if os.path.exists(cand) else "hipcc"
 
 
-def build_library(out: str = OUT, verbose: bool = False) -> str:
-    """Compile every HIP source into ``out`` (written atomically)."""
+def build_library(out: str = OUT, verbose: bool = False, sources=None) -> str:
+    """Compile the HIP sources (libasv's by default) into ``out`` (written atomically)."""
     tmp = out + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-o", tmp, *SOURCES]
+    cmd = [hipcc(), *HIPCC_FLAGS, "-I", os.path.join(ROOT, "include"), "-o", tmp,
+           *(sources or SOURCES)]
     res = subprocess.run(cmd, capture_output=True, text=True)
     msgs = "\n".join(l for l in (res.stdout + res.stderr).splitlines()
                      if "packed-fp32-ops" not in l)
@@ -40,6 +44,10 @@ def build_library(out: str = OUT, verbose: bool = False) -> str:
         print(msgs)
     os.replace(tmp, out)
     return out
+
+
+def build_microbench(verbose: bool = False) -> str:
+    return build_library(MICROBENCH_OUT, verbose, MICROBENCH_SOURCES)
 
 
 def is_built(out: str = OUT) -> bool:

@@ -129,12 +129,8 @@ __device__ __forceinline__ int xcd_tile(int bid, int G) {
 
 // PF > 0: every stage also pulls the W lines of stage k + PF into L2 (one 4-byte LDS-sink
 // load per W row), so the stage copies that follow hit L2 instead of waiting on HBM.
-// SCHED 1: the main loop's instruction order is pinned (sched_barrier): each MFMA of a K16
-// step is followed by one fragment read of the next step, and the last step of a stage runs
-// four MFMAs before the stage barrier and spreads the ring refill over the remaining ones, so
-// the MFMA pipe is never left idle behind a burst of copies or reads.
 template <int TV, int TR, int WV, int WR, int BK, int NST, int OCC = 1, int ORDER = 0,
-          int PF = 0, bool PFX = false, int SCHED = 0>
+          int PF = 0, bool PFX = false>
 __global__ __launch_bounds__(WV * WR * kWave, OCC)
 void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                       const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
@@ -270,45 +266,6 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
   };
 
-  // Single operations for the pinned schedule: MFMA t of a step (block t / MR, t % MR),
-  // fragment read t of a step (A fragments first), copy t of a stage's refill (W copies, X
-  // copies, then the L2 prefetches, the order the vmcnt accounting assumes).
-  auto read1 = [&](int slot, int half, bf16x8* a, bf16x8* b, int t) {
-    const uint4* w = lds_u4 + slot * (C::kStage / 16);
-    const uint4* x = w + C::kStageW / 16;
-    if (t < C::MV)
-      a[t] = __builtin_bit_cast(
-          bf16x8, w[swz<CPR>(wv * C::kWaveV + 32 * t + frag_row, 2 * half + frag_half)]);
-    else
-      b[t - C::MV] = __builtin_bit_cast(
-          bf16x8, x[swz<CPR>(wr * C::kWaveR + 32 * (t - C::MV) + frag_row,
-                             2 * half + frag_half)]);
-  };
-  auto copy1 = [&](int ks, int t) {
-    const int k2 = ks * BK * 2;
-    const int base = lds0 + (ks % NST) * C::kStage;
-    if (t < C::DW) {
-      dma16(base + (t * C::kWaves + wave) * 1024, w_voff[t] + k2, w_rsrc);
-    } else if (t < C::DW + C::DX) {
-      const int i = t - C::DW;
-      dma16(base + C::kStageW + (i * C::kWaves + wave) * 1024, x_voff[i] + k2, x_rsrc);
-    } else if constexpr (PF > 0) {
-      const int kp2 = min(ks + PF, KT - 1) * BK * 2;
-      const int i = t - C::DW - C::DX;
-      if (i < kPfW)
-        dma4(lds0 + C::kLds + wave * 1024, ((wave * kPfW + i) * kWave + lane) * H * 2 + kp2,
-             w_rsrc);
-      else
-        dma4(lds0 + C::kLds + wave * 1024,
-             ((wave * kPfX + i - kPfW) * kWave + lane) * H * 2 + kp2, x_rsrc);
-    }
-  };
-  constexpr int kMf = C::MV * C::MR;      // MFMAs per K16 step
-  constexpr int kRd = C::MV + C::MR;      // fragment reads per K16 step
-  constexpr int kHead = kMf >= 8 ? 4 : 1;  // MFMAs issued ahead of the stage barrier
-  constexpr int kFloat = 0x6;             // VALU and SALU may cross the pinning barriers
-  static_assert(SCHED == 0 || (kRd <= kMf && kMf > kHead), "pinned schedule shape");  // bits: 1 steps, 2 stage end
-
   // Prologue: fill the whole ring, then wait for stage 0.
   const int pro = min(NST, KT);
   for (int ks = 0; ks < pro; ++ks) issue_stage(ks);
@@ -328,102 +285,15 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
       bf16x8* cb = (s & 1) ? b1 : b0;
       bf16x8* na = (s & 1) ? a0 : a1;
       bf16x8* nb = (s & 1) ? b0 : b1;
-      if constexpr (SCHED == 5) {
-        if (s + 1 < NS16) {
-          load_frags(slot, s + 1, na, nb);
-          mfmas(ca, cb);
-        } else if (k + 1 < KT) {
-          // the last step's MFMAs first: they drain while the wave waits at the barrier and
-          // issues the refill
-          mfmas(ca, cb);
-          wait_stage_barrier<kGroup, kPf>(min(NST - 2, KT - 2 - k));
-          if (k + NST < KT) issue_stage(k + NST);
-          load_frags((k + 1) % NST, 0, na, nb);
-        } else {
-          mfmas(ca, cb);
-        }
-      } else if constexpr (SCHED == 4) {
-        if (s + 1 < NS16) {
-          load_frags(slot, s + 1, na, nb);
-          mfmas(ca, cb);
-          // scheduling hint: alternate one MFMA and one fragment read of the next step
-#pragma unroll
-          for (int t = 0; t < kRd; ++t) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-          }
-          __builtin_amdgcn_sched_group_barrier(0x008, kMf - kRd, 0);
-        } else if (k + 1 < KT) {
-          wait_stage_barrier<kGroup, kPf>(min(NST - 2, KT - 2 - k));
-          if (k + NST < KT) issue_stage(k + NST);
-          load_frags((k + 1) % NST, 0, na, nb);
-          mfmas(ca, cb);
-        } else {
-          mfmas(ca, cb);
-        }
-      } else if constexpr (SCHED != 0) {
-        if (s + 1 < NS16 && !(SCHED & 1)) {
-          load_frags(slot, s + 1, na, nb);
-          mfmas(ca, cb);
-        } else if (s + 1 >= NS16 && k + 1 < KT && !(SCHED & 2)) {
-          wait_stage_barrier<kGroup, kPf>(min(NST - 2, KT - 2 - k));
-          if (k + NST < KT) issue_stage(k + NST);
-          load_frags((k + 1) % NST, 0, na, nb);
-          mfmas(ca, cb);
-        } else if (s + 1 < NS16) {
-#pragma unroll
-          for (int i = 0; i < C::MV; ++i)
-#pragma unroll
-            for (int j = 0; j < C::MR; ++j) {
-              const int t = i * C::MR + j;
-              acc[i][j] =
-                  __builtin_amdgcn_mfma_f32_32x32x16_bf16(ca[i], cb[j], acc[i][j], 0, 0, 0);
-              if (t < kRd) read1(slot, s + 1, na, nb, t);
-              __builtin_amdgcn_sched_barrier(kFloat);
-            }
-        } else if (k + 1 < KT) {
-#pragma unroll
-          for (int i = 0; i < C::MV; ++i)
-#pragma unroll
-            for (int j = 0; j < C::MR; ++j)
-              if (i * C::MR + j < kHead) {
-                acc[i][j] =
-                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(ca[i], cb[j], acc[i][j], 0, 0, 0);
-                __builtin_amdgcn_sched_barrier(kFloat);
-              }
-          // stage k+1 must have landed; the copies of the newer stages may stay in flight
-          wait_stage_barrier<kGroup, kPf>(min(NST - 2, KT - 2 - k));
-          const bool refill = k + NST < KT;
-          constexpr int kPer = (kGroup + (kMf - kHead) - 1) / (kMf - kHead);
-#pragma unroll
-          for (int i = 0; i < C::MV; ++i)
-#pragma unroll
-            for (int j = 0; j < C::MR; ++j) {
-              const int u = i * C::MR + j - kHead;
-              if (u >= 0) {
-                acc[i][j] =
-                    __builtin_amdgcn_mfma_f32_32x32x16_bf16(ca[i], cb[j], acc[i][j], 0, 0, 0);
-                if (u < kRd) read1((k + 1) % NST, 0, na, nb, u);
-#pragma unroll
-                for (int q = 0; q < kPer; ++q)
-                  if (u * kPer + q < kGroup && refill) copy1(k + NST, u * kPer + q);
-                __builtin_amdgcn_sched_barrier(kFloat);
-              }
-            }
-        } else {
-          mfmas(ca, cb);
-        }
-      } else {
-        if (s + 1 < NS16) {
-          load_frags(slot, s + 1, na, nb);
-        } else if (k + 1 < KT) {
-          // stage k+1 must have landed; the copies of the newer stages may stay in flight
-          wait_stage_barrier<kGroup, kPf>(min(NST - 2, KT - 2 - k));
-          if (k + NST < KT) issue_stage(k + NST);
-          load_frags((k + 1) % NST, 0, na, nb);
-        }
-        mfmas(ca, cb);
+      if (s + 1 < NS16) {
+        load_frags(slot, s + 1, na, nb);
+      } else if (k + 1 < KT) {
+        // stage k+1 must have landed; the copies of the newer stages may stay in flight
+        wait_stage_barrier<kGroup, kPf>(min(NST - 2, KT - 2 - k));
+        if (k + NST < KT) issue_stage(k + NST);
+        load_frags((k + 1) % NST, 0, na, nb);
       }
+      mfmas(ca, cb);
     }
   }
   static_assert(NS16 % 2 == 0, "fragment double buffer alternates within a stage");

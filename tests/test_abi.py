@@ -117,3 +117,29 @@ def test_state_init_rejects(lib):
     p = asv.make_params()
     assert lib.asv_state_init(None, 3, ctypes.byref(p), None) == asv.ASV_EINVAL
     assert lib.asv_state_init(None, 0, ctypes.byref(p), None) == asv.ASV_OK
+
+
+def test_microbench_library_exports_and_checks():
+    """The measurement-only library exports what include/asv_microbench.h declares and rejects
+    bad arguments before launching."""
+    if not _build.is_built(_build.MICROBENCH_OUT):
+        _build.build_microbench()
+    asv.load()      # binds the HIP runtime the process already uses
+    mb = ctypes.CDLL(_build.MICROBENCH_OUT)
+    src = open(os.path.join(ROOT, "include", "asv_microbench.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    names = sorted(set(re.findall(r"\b(asvb_[a-z_]+)\s*\(", src)))
+    assert names == ["asvb_mfma_loop", "asvb_stream_read"]
+    for n in names:
+        assert hasattr(mb, n), n
+    mb.asvb_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p,
+                                    ctypes.c_int32, ctypes.c_void_p]
+    mb.asvb_mfma_loop.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
+                                  ctypes.c_void_p]
+    p = ctypes.c_void_p(0x1000)
+    assert mb.asvb_stream_read(None, 64, p, 4, None) == -1
+    assert mb.asvb_stream_read(p, 65, p, 4, None) == -1           # not a multiple of 16
+    assert mb.asvb_stream_read(ctypes.c_void_p(0x1004), 64, p, 4, None) == -1
+    assert mb.asvb_stream_read(p, 64, p, 0, None) == -1
+    assert mb.asvb_mfma_loop(None, 4, 4, None) == -1
+    assert mb.asvb_mfma_loop(p, 0, 4, None) == -1
