@@ -105,12 +105,15 @@ def drafted_logits(z_rows: Dict[int, np.ndarray], parent: np.ndarray,
 # ----------------------------------------------------------------------------- margin rule
 
 def accept_flags(g: np.ndarray, M: np.ndarray, a: np.ndarray, parent: np.ndarray,
-                 draft_tok: np.ndarray, tau_node: np.ndarray) -> np.ndarray:
+                 draft_tok: np.ndarray, tau_node: np.ndarray,
+                 temperature: float = 1.0) -> np.ndarray:
     """Margin rule of Sec. 3.2, Eq. (1), for every non-root node c with parent p.
 
     margin(c) = p_target(d_c) / p_target(top1) = exp(g_c - M_p), which lies in (0, 1]. The node
     is promoted when margin >= kappa, i.e. g_c - M_p >= ln kappa. An exact match d_c = a_p is
     accepted outright and kappa = 0 accepts every node. Roots are marked accepted.
+    With a temperature T the target distribution is softmax(z / T), so the margin is
+    exp((g_c - M_p) / T) (the paper's variant at T != 1; T = 1 is Eq. (1)).
     ``M`` and ``a`` are indexed by row id; ``tau_node`` is kappa of each node's request.
     """
     acc = np.ones(len(parent), dtype=bool)
@@ -122,7 +125,7 @@ def accept_flags(g: np.ndarray, M: np.ndarray, a: np.ndarray, parent: np.ndarray
         if draft_tok[c] == a[p] or kappa == 0.0:
             acc[c] = True
         else:
-            acc[c] = (g[c] - M[p]) >= math.log(kappa)
+            acc[c] = (g[c] - M[p]) / temperature >= math.log(kappa)
     return acc
 
 
@@ -169,14 +172,14 @@ def walk(root: int, end: int, parent: np.ndarray, draft_tok: np.ndarray, g: np.n
 
 def walk_bands(root: int, end: int, parent: np.ndarray, draft_tok: np.ndarray,
                g: np.ndarray, M: np.ndarray, a: np.ndarray, gap: np.ndarray, kappa: float,
-               path: List[int], band: float = LN_BAND):
+               path: List[int], band: float = LN_BAND, temperature: float = 1.0):
     """Index of the first walk decision that falls inside a tolerance band, or -1.
 
     Decision i (0 <= i <= len(path)) is the step taken at node path[i-1] (the root for i=0):
     the sibling choice, the accept test of the chosen child, and for the last one the bonus.
     A decision is banded when the current row's top-2 gap is below ``band`` (its argmax could
     differ at float32), when the two best children with distinct tokens are within ``band``,
-    or when the chosen mismatched child's log-margin is within ``band`` of ln kappa.
+    or when the chosen mismatched child's logit gap g - M is within ``band`` of T ln kappa.
     """
     kids = _children(parent, root, end)
     nodes = [root] + list(path)
@@ -191,7 +194,7 @@ def walk_bands(root: int, end: int, parent: np.ndarray, draft_tok: np.ndarray,
         if others and g[best] - max(others) < band:
             return i
         if draft_tok[best] != a[cur] and kappa > 0.0:
-            if abs((g[best] - M[cur]) - math.log(kappa)) < band:
+            if abs((g[best] - M[cur]) - temperature * math.log(kappa)) < band:
                 return i
     return -1
 
@@ -211,6 +214,7 @@ class Params:
     rar0: float = 1.0           # initial rolling acceptance rate (not given by the paper)
     breaker_n: int = 5          # consecutive zero-accept steps that trip the breaker (Sec. 3.3)
     max_promotions: int = -1    # -1: no cap on promotions along one walk
+    temperature: float = 1.0    # T of the margin exp((z_d - z_max) / T); 1 is Eq. (1)
     dcs_divisor: float = 0.5    # d of Sec. 3.3 (d = 0.5 for every run of Sec. 4)
     shape_lo: tuple = (3, 4, 4)     # (nsteps, topk, ndt) at DCS = 0: wide and shallow
     shape_hi: tuple = (7, 1, 8)     # at DCS = 1: deep and narrow (Sec. 3.3, Table of configs)
@@ -349,7 +353,7 @@ def finish(M, L, a, gap, g, draft_tok, parent, req_offsets, tau, draft_logits=No
     tau_node = np.empty(N)
     for b in range(B):
         tau_node[req_offsets[b]:req_offsets[b + 1]] = float(np.float32(tau[b]))
-    acc = accept_flags(g, M, a, parent, draft_tok, tau_node)
+    acc = accept_flags(g, M, a, parent, draft_tok, tau_node, params.temperature)
     out_len = np.zeros(B, dtype=np.int64)
     bonus = np.zeros(B, dtype=np.int64)
     path_arr = np.full(N, -1, dtype=np.int64)
@@ -362,7 +366,8 @@ def finish(M, L, a, gap, g, draft_tok, parent, req_offsets, tau, draft_logits=No
         out_len[b], bonus[b] = n_acc, bon
         path_arr[lo:lo + n_acc] = path
         band_at[b] = walk_bands(lo, hi, parent, draft_tok, g, M, a, gap,
-                                float(np.float32(tau[b])), path)
+                                float(np.float32(tau[b])), path,
+                                temperature=params.temperature)
         if draft_logits is not None:
             conf[b] = draft_confidence(draft_logits[lo])
         if new_state is not None:
@@ -370,4 +375,5 @@ def finish(M, L, a, gap, g, draft_tok, parent, req_offsets, tau, draft_logits=No
                                         None if draft_logits is None else conf[b], params)
     return dict(row_max=M, row_lse=L, row_argmax=a, row_gap=gap, drafted_logit=g,
                 accept=acc, accepted_len=out_len, accepted_path=path_arr, bonus_token=bonus,
-                band_at=band_at, draft_conf=conf, state=new_state, tau_node=tau_node)
+                band_at=band_at, draft_conf=conf, state=new_state, tau_node=tau_node,
+                temperature=params.temperature)

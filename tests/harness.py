@@ -90,6 +90,7 @@ def compare(w: Workload, ref: dict, got: dict, rows=None) -> Report:
         with np.errstate(divide="ignore"):
             lnk = np.log(kappa)
         delta = ref["drafted_logit"][nodes] - ref["row_max"][p]
+        lnk = lnk * ref.get("temperature", 1.0)
         in_band = (gap[p] < BAND) | ((kappa > 0) & (np.abs(delta - lnk) < BAND) &
                                      (w.draft_tok[nodes] != ref["row_argmax"][p]))
         rep.banded_nodes = int(in_band.sum())

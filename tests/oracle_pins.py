@@ -136,6 +136,37 @@ def check_margin_is_probability_ratio(orc):
     assert orc.accept_flags(g, M, a, parent, d, np.zeros(N)).all()
 
 
+def check_margin_with_temperature(orc):
+    """The temperature variant: the target distribution is softmax(z / T), so a node passes iff
+    p_T(draft) / p_T(top1) >= kappa; T = 1 is Eq. (1), a large T accepts more, a small T fewer."""
+    rng = np.random.default_rng(23)
+    N, V = 40, 23
+    z = rng.standard_normal((N, V)) * 2.0
+    parent = _random_rows_tree(rng, N, V)
+    d = rng.integers(0, V, size=N)
+    d[0] = -1
+    M, a, L, gap = orc.row_stats(z)
+    g = np.array([np.nan] + [z[parent[c], d[c]] for c in range(1, N)])
+    checked = 0
+    for T in (0.25, 0.7, 1.0, 2.0, 5.0):
+        probs = softmax(z / T, axis=1)
+        for kappa in (0.05, 0.2, 0.5, 0.9):
+            acc = orc.accept_flags(g, M, a, parent, d, np.full(N, kappa), T)
+            for c in range(1, N):
+                p = parent[c]
+                margin = probs[p, d[c]] / probs[p].max()
+                if abs(margin - kappa) < 1e-9:
+                    continue
+                want = d[c] == a[p] or margin >= kappa
+                assert acc[c] == want, (T, kappa, c)
+                checked += 1
+    assert checked > 500
+    base = orc.accept_flags(g, M, a, parent, d, np.full(N, 0.3), 1.0)
+    hot = orc.accept_flags(g, M, a, parent, d, np.full(N, 0.3), 3.0)
+    cold = orc.accept_flags(g, M, a, parent, d, np.full(N, 0.3), 0.3)
+    assert (hot >= base).all() and (cold <= base).all() and hot.sum() > base.sum() > cold.sum()
+
+
 def check_exact_match_always_accepted(orc):
     # d_c is the parent's argmax: accepted for every kappa in [0, 1], including kappa = 1.
     rng = np.random.default_rng(3)
@@ -465,7 +496,8 @@ def check_verify_end_to_end(orc):
 
 ALL_CHECKS = [
     check_widen, check_logits_exact, check_row_stats, check_top8,
-    check_margin_is_probability_ratio, check_exact_match_always_accepted,
+    check_margin_is_probability_ratio, check_margin_with_temperature,
+    check_exact_match_always_accepted,
     check_kappa_one_is_strict, check_kappa_zero_reaches_leaf, check_walk_properties,
     check_len_monotone_in_kappa, check_promotion_cap, check_draft_confidence,
     check_ema_closed_form, check_ring_mean, check_breaker, check_tree_shape,

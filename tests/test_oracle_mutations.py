@@ -13,36 +13,44 @@ import oracle.asv_oracle as orc
 from oracle_pins import ALL_CHECKS
 
 
-def _accept_own_row(g, M, a, parent, d, tau_node):
+def _accept_own_row(g, M, a, parent, d, tau_node, temperature=1.0):
     acc = np.ones(len(parent), dtype=bool)
     for c in range(len(parent)):
         if parent[c] < 0:
             continue
         k = float(tau_node[c])
-        acc[c] = d[c] == a[c] or k == 0.0 or (g[c] - M[c]) >= math.log(k)
+        acc[c] = d[c] == a[c] or k == 0.0 or (g[c] - M[c]) / temperature >= math.log(k)
     return acc
 
 
-def _accept_sign(g, M, a, parent, d, tau_node):
+def _accept_sign(g, M, a, parent, d, tau_node, temperature=1.0):
     acc = np.ones(len(parent), dtype=bool)
     for c in range(len(parent)):
         p = parent[c]
         if p < 0:
             continue
         k = float(tau_node[c])
-        acc[c] = d[c] == a[p] or k == 0.0 or (M[p] - g[c]) >= math.log(k)
+        acc[c] = d[c] == a[p] or k == 0.0 or (M[p] - g[c]) / temperature >= math.log(k)
     return acc
 
 
-def _accept_strict_gt(g, M, a, parent, d, tau_node):
+def _accept_strict_gt(g, M, a, parent, d, tau_node, temperature=1.0):
     acc = np.ones(len(parent), dtype=bool)
     for c in range(len(parent)):
         p = parent[c]
         if p < 0:
             continue
         k = float(tau_node[c])
-        acc[c] = k == 0.0 or (g[c] - M[p]) > math.log(k)      # drops the exact-match clause
+        acc[c] = k == 0.0 or (g[c] - M[p]) / temperature > math.log(k)   # no exact-match clause
     return acc
+
+
+def _accept_ignores_temperature(g, M, a, parent, d, tau_node, temperature=1.0):
+    return ORIG["accept_flags"](g, M, a, parent, d, tau_node, 1.0)
+
+
+def _accept_temperature_inverted(g, M, a, parent, d, tau_node, temperature=1.0):
+    return ORIG["accept_flags"](g, M, a, parent, d, tau_node, 1.0 / temperature)
 
 
 def _logits_transposed(x64, w64):
@@ -146,6 +154,8 @@ MUTANTS = {
     "accept_uses_own_row": ("accept_flags", _accept_own_row),
     "accept_sign_flipped": ("accept_flags", _accept_sign),
     "accept_drops_exact_match": ("accept_flags", _accept_strict_gt),
+    "accept_ignores_temperature": ("accept_flags", _accept_ignores_temperature),
+    "accept_temperature_inverted": ("accept_flags", _accept_temperature_inverted),
     "logits_transposed": ("logits", _logits_transposed),
     "argmax_last_occurrence": ("row_stats", _row_stats_last_argmax),
     "lse_drops_max_term": ("row_stats", _row_stats_no_shift),
