@@ -79,6 +79,8 @@ typedef struct asv_params {
   int32_t breaker_n;       /* zero-accept steps that trip the breaker, >= 1; paper: 5 */
   int32_t max_promotions;  /* mismatches one walk may promote; -1 = no limit, 1 = only the
                               first mismatch position */
+  float   temperature;     /* T > 0 of the margin exp((z_d - z_max) / T) >= kappa, the target
+                              distribution taken as softmax(z / T); 1 is Eq. (1) */
   float   dcs_divisor;     /* d of Eq. (2): the score saturates once p_draft * RAR reaches d,
                               > 0; paper: 0.5 */
   int32_t shape_lo[3];     /* (nsteps, topk, ndt) at score 0, each >= 1; paper: (3, 4, 4) */
@@ -162,7 +164,7 @@ int asv_state_init(asv_req_state *state, int32_t B, const asv_params *p, void *s
  *      reduced on the fly to row_max / row_lse / row_argmax and the drafted logits — the
  *      [N][V] logits matrix is never written to memory;
  *   2. accept[c] = (draft_tok[c] == row_argmax[p]) || tau == 0 ||
- *      (drafted_logit[c] - row_max[p] >= ln tau), with p = parent[c];
+ *      (drafted_logit[c] - row_max[p] >= T ln tau), with p = parent[c], T = params.temperature;
  *   3. per request, from the root repeatedly take the child with the highest drafted logit
  *      (lowest row id on ties) while it is accepted and the promotion budget allows, then
  *      bonus = row_argmax of the last accepted node;

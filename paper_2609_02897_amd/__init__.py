@@ -42,13 +42,13 @@ class AsvError(RuntimeError):
 
 
 def make_params(alpha: float = 0.3, rar0: float = 1.0, breaker_n: int = 5,
-                max_promotions: int = -1, dcs_divisor: float = 0.5,
+                max_promotions: int = -1, temperature: float = 1.0, dcs_divisor: float = 0.5,
                 shape_lo=(3, 4, 4), shape_hi=(7, 1, 8), shape_start=(3, 4, 4)) -> AsvParams:
     """Policy parameters; defaults are the paper's (EMA alpha 0.3, breaker after 5 steps,
-    DCS divisor 0.5, tree shapes (3,4,4) <-> (7,1,8))."""
+    margin at temperature 1, DCS divisor 0.5, tree shapes (3,4,4) <-> (7,1,8))."""
     tri = ctypes.c_int32 * 3
-    return AsvParams(alpha, rar0, breaker_n, max_promotions, dcs_divisor, tri(*shape_lo),
-                     tri(*shape_hi), tri(*shape_start))
+    return AsvParams(alpha, rar0, breaker_n, max_promotions, temperature, dcs_divisor,
+                     tri(*shape_lo), tri(*shape_hi), tri(*shape_start))
 
 
 def _check(code: int):

@@ -29,7 +29,7 @@ class AsvReqState(ctypes.Structure):
 class AsvParams(ctypes.Structure):
     _fields_ = [("alpha", ctypes.c_float), ("rar0", ctypes.c_float),
                 ("breaker_n", ctypes.c_int32), ("max_promotions", ctypes.c_int32),
-                ("dcs_divisor", ctypes.c_float), ("shape_lo", ctypes.c_int32 * 3),
+                ("temperature", ctypes.c_float), ("dcs_divisor", ctypes.c_float), ("shape_lo", ctypes.c_int32 * 3),
                 ("shape_hi", ctypes.c_int32 * 3), ("shape_start", ctypes.c_int32 * 3)]
 
 

@@ -87,6 +87,7 @@ bool params_ok(const asv_params& p) {
   if (!(p.alpha > 0.f && p.alpha <= 1.f) || p.breaker_n < 1 || p.max_promotions < -1)
     return false;
   if (!(p.dcs_divisor > 0.f && p.dcs_divisor < __builtin_inff())) return false;
+  if (!(p.temperature > 0.f && p.temperature < __builtin_inff())) return false;
   for (int k = 0; k < 3; ++k)
     if (p.shape_lo[k] < 1 || p.shape_hi[k] < 1 || p.shape_start[k] < 1) return false;
   return true;

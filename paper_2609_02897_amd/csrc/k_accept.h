@@ -6,7 +6,9 @@
 //
 // Margin rule (Sec. 3.2, Eq. (1)): a node c with parent p and drafted token d is accepted when
 // p_target(d) / p_target(top1) = exp(z_p[d] - max z_p) >= kappa, i.e. z_p[d] - max >= ln kappa;
-// an exact match d == argmax z_p is accepted outright, kappa == 0 accepts everything.
+// an exact match d == argmax z_p is accepted outright, kappa == 0 accepts everything. With a
+// temperature T (params.temperature) the target distribution is softmax(z / T) and the test
+// becomes z_p[d] - max >= T ln kappa.
 // Walk: from the root, repeatedly take the child with the highest drafted logit (lowest row id
 // on ties) while it is accepted; a child that is not the current row's argmax is a promotion
 // and counts against params.max_promotions (-1 = unlimited). The bonus token is the argmax of
@@ -352,7 +354,7 @@ __device__ __forceinline__ void accept_staged(const AcceptArgs& a, int b, int lo
   }
 
   // ---- Eq. (1) for every node, and each node's best child (one LDS max per child)
-  const float ln_kappa = kappa > 0.f ? logf(kappa) : kNegInf;
+  const float ln_kappa = kappa > 0.f ? a.prm.temperature * logf(kappa) : kNegInf;
   if (lane == 0) a.accept[lo] = 1;
   for (int i = 1 + lane; i < n; i += kWave) {
     const int p = sm.par[i] - lo;
@@ -432,7 +434,7 @@ __device__ __forceinline__ void accept_global(const AcceptArgs& a, int b, int lo
     return;
   }
 
-  const float ln_kappa = kappa > 0.f ? logf(kappa) : kNegInf;
+  const float ln_kappa = kappa > 0.f ? a.prm.temperature * logf(kappa) : kNegInf;
   for (int c = lo + lane; c < hi; c += kWave) {
     uint8_t ok = 1;
     if (c != lo) {

@@ -43,9 +43,9 @@ def test_version_and_status(lib):
 
 def test_struct_layouts():
     assert ctypes.sizeof(_abi.AsvReqState) == 112
-    assert ctypes.sizeof(_abi.AsvParams) == 56
-    # 4 ints, 18 pointers, params (56 B), 2 event pointers
-    assert ctypes.sizeof(_abi.AsvVerifyArgs) == 16 + 18 * 8 + 56 + 2 * 8
+    assert ctypes.sizeof(_abi.AsvParams) == 60
+    # 4 ints, 18 pointers, params (60 B, padded to 64), 2 event pointers
+    assert ctypes.sizeof(_abi.AsvVerifyArgs) == 16 + 18 * 8 + 64 + 2 * 8
 
 
 def test_param_and_policy_checks_on_host(lib):
@@ -60,7 +60,8 @@ def test_param_and_policy_checks_on_host(lib):
                 asv.make_params(dcs_divisor=float("inf")),
                 asv.make_params(shape_lo=(0, 4, 4)), asv.make_params(shape_hi=(7, 0, 8)),
                 asv.make_params(shape_start=(3, 4, -1)), asv.make_params(alpha=0.0),
-                asv.make_params(breaker_n=0), asv.make_params(max_promotions=-2)):
+                asv.make_params(breaker_n=0), asv.make_params(max_promotions=-2),
+                asv.make_params(temperature=0.0), asv.make_params(temperature=float("inf"))):
         assert lib.asv_tree_policy(None, state, 4, ctypes.byref(bad), None) == asv.ASV_EINVAL
         assert lib.asv_state_init(state, 4, ctypes.byref(bad), None) == asv.ASV_EINVAL
 

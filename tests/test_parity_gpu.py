@@ -156,6 +156,26 @@ def test_promotion_cap(asv, dev, max_promotions, name):
     compare(w, ref, got)
 
 
+@pytest.mark.parametrize("temperature", [0.5, 2.0])
+@pytest.mark.parametrize("name", ["rows64_eagle60_ragged_vocab", "rows256_three_tiles"])
+def test_margin_temperature(asv, dev, name, temperature):
+    """The temperature variant of the margin rule: exp((z_d - z_max) / T) >= kappa."""
+    print(f"[temperature] case={name} T={temperature}", flush=True)
+    w = _case(name)
+    W = w.weights()
+    w64 = oracle.widen_weights(W)
+    resolve_with_oracle(w, w64)
+    ref = reference(w, w64, params=oracle.Params(temperature=temperature))
+    got = _run(asv, w, W, dev, params=asv.make_params(temperature=temperature))
+    rep = compare(w, ref, got)
+    print(f"  {rep}", flush=True)
+    base = reference(w, w64)
+    if temperature > 1:
+        assert ref["accept"].sum() >= base["accept"].sum()
+    else:
+        assert ref["accept"].sum() <= base["accept"].sum()
+
+
 def test_exact_ties_lowest_index(asv, dev):
     """Bit-identical W rows give bit-identical logits in both implementations; the argmax, the
     bonus and the sibling choice must take the lowest index, across lanes, waves and slabs."""
