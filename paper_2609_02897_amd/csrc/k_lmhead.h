@@ -129,8 +129,10 @@ __device__ __forceinline__ int xcd_tile(int bid, int G) {
 
 // PF > 0: every stage also pulls the W lines of stage k + PF into L2 (one 4-byte LDS-sink
 // load per W row), so the stage copies that follow hit L2 instead of waiting on HBM.
+// IGLP >= 0: the compiler's MFMA / LDS-read interleaving strategy of that number is applied to
+// each K16 step that reads the next step's fragments (-1: the default schedule).
 template <int TV, int TR, int WV, int WR, int BK, int NST, int OCC = 1, int ORDER = 0,
-          int PF = 0, bool PFX = false>
+          int PF = 0, bool PFX = false, int IGLP = -1>
 __global__ __launch_bounds__(WV * WR * kWave, OCC)
 void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                       const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
@@ -287,6 +289,7 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
       bf16x8* nb = (s & 1) ? b0 : b1;
       if (s + 1 < NS16) {
         load_frags(slot, s + 1, na, nb);
+        if constexpr (IGLP >= 0) __builtin_amdgcn_iglp_opt(IGLP);
       } else if (k + 1 < KT) {
         // stage k+1 must have landed; the copies of the newer stages may stay in flight
         wait_stage_barrier<kGroup, kPf>(min(NST - 2, KT - 2 - k));
