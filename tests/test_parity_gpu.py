@@ -102,12 +102,21 @@ def _case(name):
         trees = [_rand_tree(rng, int(rng.integers(1, 4)), 2, 2) for _ in range(1030)]
         trees[517] = _rand_tree(rng, 290, 10, 4)
         return custom_workload(name, 64, 600, trees, 0.3, seed=9, w_std=0.16)
+    if name == "single_row_single_slab":
+        # N = 1 (a root-only request) and V < 256: one ragged vocabulary slab
+        return custom_workload(name, 64, 100, [[-1]], 0.3, seed=10, w_std=0.16)
+    if name == "vocab_over_one_merge_round":
+        # V = 170000: 665 slabs, more than one round of record loads in the row merge
+        trees = [_rand_tree(rng, 20, 5, 3), _rand_tree(rng, 11, 4, 3)]
+        return custom_workload(name, 64, 170000, trees, 0.2, seed=11, w_std=0.16,
+                               draft_logits=True)
     raise KeyError(name)
 
 
 CASES = ["tiny_config", "rows64_eagle60_ragged_vocab", "rows128_mixed", "rows256_three_tiles",
          "deep_chain_and_wide", "root_only_requests", "many_tiny_requests",
-         "unfused_large_batch", "request_over_lds_stage", "unfused_with_large_request"]
+         "unfused_large_batch", "request_over_lds_stage", "unfused_with_large_request",
+         "single_row_single_slab", "vocab_over_one_merge_round"]
 
 
 @pytest.mark.parametrize("tau", [None, 0.0, 0.05, 0.3, 1.0])
