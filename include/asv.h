@@ -31,7 +31,7 @@
 extern "C" {
 #endif
 
-#define ASV_VERSION 110          /* 1.1.0 */
+#define ASV_VERSION 120          /* 1.2.0 */
 
 /* Return codes. */
 #define ASV_OK          0
@@ -51,6 +51,10 @@ extern "C" {
                                     increasing, req_offsets[0] != 0 or req_offsets[B] != N.
                                     Set on every request of the batch. */
 #define ASV_RS_BAD_TAU     32    /* tau[b] outside [0, 1] or NaN */
+#define ASV_RS_MASK_SMALL  64    /* asv_tree_meta: the request has more than 32 * mask_words
+                                    nodes; its positions are written, its mask rows are not */
+#define ASV_RS_BAD_PATH    128   /* asv_commit: accepted_len[b] outside [0, n_b - 1] or an
+                                    accepted_path entry that is not a node of request b */
 
 #define ASV_HIST_WINDOW 16
 
@@ -125,6 +129,130 @@ typedef struct asv_verify_args {
                                      kernel, or NULL */
   void *k1_end_event;             /* optional hipEvent_t recorded just after it, or NULL */
 } asv_verify_args;
+
+/* ---- Draft side (Sec. 2, "Draft"): the draft model runs nsteps forwards, every frontier node
+ * branches topk ways, and the tree is pruned to a verification budget of ndt tokens (ndt counts
+ * the root). The tree grows as in EAGLE-2 (the drafter the paper adopts, EAGLE-3, grows its tree
+ * this way): a node's score is the float32 sum of the draft log-probabilities along its path;
+ * each step appends all frontier x topk children to the node pool (frontier slot major, child
+ * rank minor) and keeps the topk best as the next frontier (best first, the earlier candidate on
+ * equal scores); pruning keeps the root and the ndt - 1 best pool nodes (the earlier pool entry
+ * on equal scores) in pool order, so parents precede children. */
+
+#define ASV_TOPK_MAX 4           /* largest topk of a draft tree = width of the draft top-k */
+#define ASV_POOL_MAX 256         /* drafted nodes one tree can hold: topk + (nsteps-1) topk^2 */
+
+/* asv_draft_tree.status and asv_draft_prune req_status bits. */
+#define ASV_DS_BAD_SHAPE 1       /* shape outside nsteps >= 1, 1 <= topk <= 4, ndt >= 1, or a
+                                    pool larger than ASV_POOL_MAX: the tree stays root-only */
+#define ASV_DS_OVERFLOW  2       /* asv_draft_prune: the request's rows end past n_cap; none of
+                                    them is written */
+
+/* One request's draft tree while it grows. Caller-owned device memory, 3136 bytes, written by
+ * asv_draft_step (initialised at step 0) and read by asv_draft_prune. */
+typedef struct asv_draft_tree {
+  int32_t nsteps, topk, ndt;        /* the shape the tree grows to, fixed at step 0 */
+  int32_t steps;                    /* draft steps applied so far */
+  int32_t n_pool;                   /* drafted nodes in the pool */
+  int32_t n_front;                  /* frontier slots; 1 (the root) before the first step */
+  int32_t status;                   /* ASV_DS_* bits, 0 when the shape was valid */
+  int32_t reserved;
+  int32_t front[ASV_TOPK_MAX];      /* pool index of each frontier slot, best first; -1 = root */
+  float   front_score[ASV_TOPK_MAX];
+  int32_t tok[ASV_POOL_MAX];        /* drafted token of each pool node (a target id) */
+  int32_t par[ASV_POOL_MAX];        /* pool index of its parent, -1 for a child of the root */
+  float   score[ASV_POOL_MAX];       /* sum of the float32 log-probabilities along its path */
+} asv_draft_tree;
+
+/* Arguments of asv_draft_step. Draft rows use a fixed stride of ASV_TOPK_MAX per request: row
+ * 4b + j holds the draft model's final hidden state for frontier slot j of request b (at step 0
+ * only slot 0, the root, is read by the tree update). Rows of unused slots are computed like any
+ * other row and then ignored, so they may hold anything. */
+typedef struct asv_draft_args {
+  int32_t B, H, V;                /* host ints: B >= 0, H > 0 with H % 64 == 0, V >= 4 */
+  int32_t step;                   /* host int: 0 (re)starts every tree from its shape */
+  const uint16_t *hidden;         /* [4B][H] bf16 draft hidden states, 16-byte aligned */
+  const uint16_t *w_draft;        /* [V][H] bf16 draft LM-head weight, 16-byte aligned */
+  const int32_t  *vocab_map;      /* [V] draft id -> target id, or NULL for the identity */
+  const asv_req_state *state;     /* [B]: at step 0 tree b takes state[b].shape; or NULL */
+  int32_t shape[3];               /* (nsteps, topk, ndt) for every tree when state is NULL */
+  asv_draft_tree *tree;           /* [B] in/out */
+  /* outputs */
+  int32_t *topk_id;               /* [4B][4] the 4 most probable tokens of each row, best first
+                                     (lowest draft id on equal logits; a non-number logit
+                                     counts as -inf), mapped through vocab_map */
+  float   *topk_logp;             /* [4B][4] their log-probabilities z - lse (non-number: -inf) */
+  float   *row_lse;               /* [4B] log sum_v exp(z[v]) over the draft vocabulary */
+  int32_t *front_tok;             /* [B][4] token of each new frontier slot (the next draft
+                                     forward's inputs); -1 for slots past the frontier and for
+                                     trees that are done or invalid */
+  float   *draft_conf;            /* [B] or NULL; at step 0, p_draft(top1) = exp(best log-prob of
+                                     the root row), the confidence Eq. (2) reads */
+  void *k_begin_event;            /* optional hipEvent_t recorded around the LM-head kernel */
+  void *k_end_event;
+} asv_draft_args;
+
+/* Workspace asv_draft_step needs (per-vocabulary-slab top-4 records); 256-byte aligned, no
+ * initialisation needed. Returns ASV_EINVAL for sizes asv_draft_step would reject. */
+int asv_draft_workspace_bytes(int32_t B, int32_t H, int32_t V, uint64_t *bytes);
+
+/* One draft step for a batch (Sec. 2, "Draft"): the draft LM head over all 4B rows (bf16 inputs,
+ * fp32 accumulation) reduced on the fly to each row's top-4 and log-sum-exp (the [4B][V] logits
+ * never reach memory), then one growth step of every tree that has not taken its nsteps steps.
+ * Returns ASV_EINVAL for bad sizes, null or misaligned pointers or (state NULL) a bad shape,
+ * ASV_EWORKSPACE, or ASV_EHIP. A bad shape read from state marks that tree ASV_DS_BAD_SHAPE. */
+int asv_draft_step(const asv_draft_args *args, void *workspace, uint64_t workspace_bytes,
+                   void *stream);
+
+/* Prune every tree to its verification budget and lay the batch out as asv_verify reads it:
+ * request b gets n_b = 1 + min(ndt - 1, n_pool) rows at [req_offsets[b], req_offsets[b+1]),
+ * the root first (parent -1, draft_tok = root_tok[b], or -1 when root_tok is NULL), then the
+ * kept pool nodes in pool order with global parent ids. An invalid tree gives n_b = 1.
+ * tree: [B]; root_tok: [B] or NULL; parent, draft_tok: [n_cap]; req_offsets: [B+1] (always
+ * written, also past n_cap); req_status: [B] ASV_DS_* bits. Returns ASV_EINVAL for B < 0,
+ * n_cap < 0 or null outputs, ASV_EHIP if a launch fails. */
+int asv_draft_prune(const asv_draft_tree *tree, int32_t B, const int32_t *root_tok,
+                    int32_t n_cap, int32_t *parent, int32_t *draft_tok, int32_t *req_offsets,
+                    int32_t *req_status, void *stream);
+
+/* ---- Around the target forward. */
+
+/* Tree-attention metadata (Sec. 1, Sec. 2: the target scores the whole tree in one forward).
+ * For node c of request b: pos[c] = pos_base[b] + depth(c) (pos_base NULL: 0), depth being the
+ * number of parent links to the root; mask row c, mask_words 32-bit words at mask + c *
+ * mask_words, has bit (j - req_offsets[b]) set iff node j is c or an ancestor of c (bit k of
+ * word k / 32 at position k % 32). pos or mask may be NULL to skip them. Requests whose
+ * offsets or parents are malformed (ASV_RS_BAD_OFFSETS, ASV_RS_BAD_ROOT, ASV_RS_BAD_PARENT)
+ * get neither; a request with more than 32 * mask_words nodes gets ASV_RS_MASK_SMALL and its
+ * positions only. req_status: [B]. Returns ASV_EINVAL for bad sizes or null arguments. */
+int asv_tree_meta(const int32_t *parent, const int32_t *req_offsets, int32_t B, int32_t N,
+                  const int32_t *pos_base, int32_t mask_words, int32_t *pos, uint32_t *mask,
+                  int32_t *req_status, void *stream);
+
+/* Arguments of asv_commit: what one verification step commits (Sec. 2, "Verify"). */
+typedef struct asv_commit_args {
+  int32_t B, N;                   /* host ints, as in asv_verify */
+  const int32_t *req_offsets;     /* [B+1] the verified batch's offsets */
+  const int32_t *draft_tok;       /* [N] */
+  const int32_t *accepted_len;    /* [B] asv_verify outputs */
+  const int32_t *accepted_path;   /* [N] */
+  const int32_t *bonus_token;     /* [B] */
+  int32_t *commit_off;            /* [B+1] prefix sums of accepted_len + 1 */
+  int32_t *commit_tok;            /* [N] request b's accepted drafted tokens then its bonus,
+                                     at [commit_off[b], commit_off[b+1]) */
+  int32_t *commit_row;            /* [N] the rows that stay valid: the root, then the accepted
+                                     nodes (global ids) */
+  const void *row_src;            /* [N][row_bytes] per-node data to keep (hidden states, KV
+                                     slot ids), or NULL */
+  void    *row_dst;               /* [N][row_bytes]: row_src[commit_row[i]] lands at row i */
+  int64_t row_bytes;              /* > 0 and a multiple of 4 when row_src is given */
+  int32_t *req_status;            /* [B] ASV_RS_BAD_OFFSETS / ASV_RS_BAD_PATH bits */
+} asv_commit_args;
+
+/* Commit one verification step. A request with ASV_RS_BAD_PATH commits only its root row and
+ * bonus (length 0); entries that would land at index >= N are not written. Returns ASV_EINVAL
+ * for bad sizes, null or misaligned pointers, ASV_EHIP if a launch fails. */
+int asv_commit(const asv_commit_args *args, void *stream);
 
 /* ASV_VERSION of the loaded library. */
 int asv_version(void);

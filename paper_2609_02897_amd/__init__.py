@@ -12,11 +12,13 @@ import ctypes
 from typing import NamedTuple, Optional
 
 from ._abi import (  # noqa: F401
-    ASV_EHIP, ASV_EINVAL, ASV_EWORKSPACE, ASV_OK, EXPORTS, LIB_PATH, RS_BAD_OFFSETS,
-    RS_BAD_PARENT, RS_BAD_ROOT, RS_BAD_TAU, RS_BAD_TOKEN, AsvParams, AsvReqState,
-    AsvVerifyArgs, LibraryMissing, load)
+    ASV_EHIP, ASV_EINVAL, ASV_EWORKSPACE, ASV_OK, DS_BAD_SHAPE, DS_OVERFLOW, EXPORTS, LIB_PATH,
+    POOL_MAX, RS_BAD_OFFSETS, RS_BAD_PARENT, RS_BAD_PATH, RS_BAD_ROOT, RS_BAD_TAU,
+    RS_BAD_TOKEN, RS_MASK_SMALL, TOPK_MAX, AsvCommitArgs, AsvDraftArgs, AsvDraftTree,
+    AsvParams, AsvReqState, AsvVerifyArgs, LibraryMissing, load)
 
 STATE_BYTES = ctypes.sizeof(AsvReqState)
+TREE_BYTES = ctypes.sizeof(AsvDraftTree)
 
 
 class VerifyOut(NamedTuple):
@@ -187,3 +189,157 @@ def state_fields(state) -> list:
     raw = state.detach().cpu().contiguous().numpy().tobytes()
     return [AsvReqState.from_buffer_copy(raw[i * STATE_BYTES:(i + 1) * STATE_BYTES])
             for i in range(state.shape[0])]
+
+
+# ----------------------------------------------------------------------------- draft side
+
+class DraftOut(NamedTuple):
+    topk_id: "torch.Tensor"          # i32 [4B, 4]
+    topk_logp: "torch.Tensor"        # f32 [4B, 4]
+    row_lse: "torch.Tensor"          # f32 [4B]
+    front_tok: "torch.Tensor"        # i32 [B, 4]
+    draft_conf: Optional["torch.Tensor"]  # f32 [B] or None
+
+
+def draft_workspace_bytes(B: int, H: int, V: int) -> int:
+    out = ctypes.c_uint64(0)
+    _check(load().asv_draft_workspace_bytes(B, H, V, ctypes.byref(out)))
+    return int(out.value)
+
+
+def alloc_draft_trees(B: int, device="cuda"):
+    """Storage for B growing draft trees (``asv_draft_tree``, 3136 bytes each); asv_draft_step
+    initialises them at step 0."""
+    import torch
+    return torch.empty((B, TREE_BYTES), dtype=torch.uint8, device=device)
+
+
+def draft_step(hidden, w_draft, trees, step: int, state=None, shape=None, vocab_map=None,
+               with_conf: bool = False, out: Optional[DraftOut] = None, workspace=None,
+               events=None) -> DraftOut:
+    """One draft step through ``asv_draft_step`` on torch's current stream.
+
+    hidden bf16 [4B, H] (row 4b + j = frontier slot j of request b); w_draft bf16 [V, H];
+    trees u8 [B, 3136] (in/out); state u8 [B, 112] supplies each tree's shape at step 0, else
+    ``shape`` = (nsteps, topk, ndt) for all; vocab_map int32 [V] or None.
+    """
+    import torch
+    R, H = hidden.shape
+    V = w_draft.shape[0]
+    B = trees.shape[0]
+    if R != TOPK_MAX * B:
+        raise ValueError(f"hidden: expected {TOPK_MAX * B} rows (4 per request), got {R}")
+    _need(hidden, "hidden", torch.bfloat16, (R, H))
+    _need(w_draft, "w_draft", torch.bfloat16, (V, H))
+    _need(trees, "trees", torch.uint8, (B, TREE_BYTES))
+    if vocab_map is not None:
+        _need(vocab_map, "vocab_map", torch.int32, (V,))
+    if state is not None:
+        _need(state, "state", torch.uint8, (B, STATE_BYTES))
+    dev = hidden.device
+    if out is None:
+        out = DraftOut(torch.empty((R, TOPK_MAX), dtype=torch.int32, device=dev),
+                       torch.empty((R, TOPK_MAX), dtype=torch.float32, device=dev),
+                       torch.empty(R, dtype=torch.float32, device=dev),
+                       torch.empty((B, TOPK_MAX), dtype=torch.int32, device=dev),
+                       torch.empty(B, dtype=torch.float32, device=dev) if with_conf else None)
+    if workspace is None:
+        workspace = torch.empty(max(draft_workspace_bytes(B, H, V), 256), dtype=torch.uint8,
+                                device=dev)
+    a = AsvDraftArgs()
+    a.B, a.H, a.V, a.step = B, H, V, step
+    a.hidden, a.w_draft = hidden.data_ptr(), w_draft.data_ptr()
+    a.vocab_map, a.state = _ptr(vocab_map), _ptr(state)
+    a.shape = (ctypes.c_int32 * 3)(*(shape or (1, 1, 1)))
+    a.tree = trees.data_ptr()
+    a.topk_id, a.topk_logp = out.topk_id.data_ptr(), out.topk_logp.data_ptr()
+    a.row_lse, a.front_tok = out.row_lse.data_ptr(), out.front_tok.data_ptr()
+    a.draft_conf = _ptr(out.draft_conf)
+    if events is not None:
+        a.k_begin_event, a.k_end_event = events
+    _check(load().asv_draft_step(ctypes.byref(a), workspace.data_ptr(), workspace.numel(),
+                                 _stream_handle(dev)))
+    return out
+
+
+def draft_prune(trees, n_cap: int, root_tok=None):
+    """``asv_draft_prune``: (parent [n_cap], draft_tok [n_cap], req_offsets [B+1], req_status
+    [B]) in the layout asv_verify reads; rows past req_offsets[B] are untouched."""
+    import torch
+    B = trees.shape[0]
+    _need(trees, "trees", torch.uint8, (B, TREE_BYTES))
+    if root_tok is not None:
+        _need(root_tok, "root_tok", torch.int32, (B,))
+    dev = trees.device
+    parent = torch.empty(max(n_cap, 1), dtype=torch.int32, device=dev)
+    tok = torch.empty(max(n_cap, 1), dtype=torch.int32, device=dev)
+    off = torch.empty(B + 1, dtype=torch.int32, device=dev)
+    status = torch.empty(B, dtype=torch.int32, device=dev)
+    _check(load().asv_draft_prune(trees.data_ptr(), B, _ptr(root_tok), n_cap,
+                                  parent.data_ptr(), tok.data_ptr(), off.data_ptr(),
+                                  status.data_ptr(), _stream_handle(dev)))
+    return parent, tok, off, status
+
+
+def draft_tree_fields(trees) -> list:
+    """Decode a [B, 3136] u8 tree tensor (copied to the host) into AsvDraftTree structs."""
+    raw = trees.detach().cpu().contiguous().numpy().tobytes()
+    return [AsvDraftTree.from_buffer_copy(raw[i * TREE_BYTES:(i + 1) * TREE_BYTES])
+            for i in range(trees.shape[0])]
+
+
+# ----------------------------------------------------------------------------- around the target
+
+def tree_meta(parent, req_offsets, pos_base=None, mask_words: int = 0):
+    """``asv_tree_meta``: (pos [N], mask [N, mask_words] u32 as int32 or None, req_status [B])."""
+    import torch
+    N = parent.shape[0]
+    B = req_offsets.shape[0] - 1
+    _need(parent, "parent", torch.int32, (N,))
+    _need(req_offsets, "req_offsets", torch.int32, (B + 1,))
+    if pos_base is not None:
+        _need(pos_base, "pos_base", torch.int32, (B,))
+    dev = parent.device
+    pos = torch.empty(N, dtype=torch.int32, device=dev)
+    mask = (torch.empty((N, mask_words), dtype=torch.int32, device=dev) if mask_words > 0
+            else None)
+    status = torch.empty(B, dtype=torch.int32, device=dev)
+    _check(load().asv_tree_meta(parent.data_ptr(), req_offsets.data_ptr(), B, N,
+                                _ptr(pos_base), mask_words, pos.data_ptr(), _ptr(mask),
+                                status.data_ptr(), _stream_handle(dev)))
+    return pos, mask, status
+
+
+def commit(req_offsets, draft_tok, accepted_len, accepted_path, bonus_token, row_src=None):
+    """``asv_commit``: (commit_off [B+1], commit_tok [N], commit_row [N], row_dst or None,
+    req_status [B]). row_src: any contiguous [N, ...] tensor whose rows are a multiple of 4
+    bytes; its kept rows are gathered into row_dst (same shape)."""
+    import torch
+    N = draft_tok.shape[0]
+    B = req_offsets.shape[0] - 1
+    _need(req_offsets, "req_offsets", torch.int32, (B + 1,))
+    _need(draft_tok, "draft_tok", torch.int32, (N,))
+    _need(accepted_len, "accepted_len", torch.int32, (B,))
+    _need(accepted_path, "accepted_path", torch.int32, (N,))
+    _need(bonus_token, "bonus_token", torch.int32, (B,))
+    dev = draft_tok.device
+    c_off = torch.empty(B + 1, dtype=torch.int32, device=dev)
+    c_tok = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
+    c_row = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
+    status = torch.empty(B, dtype=torch.int32, device=dev)
+    dst = None
+    a = AsvCommitArgs()
+    a.B, a.N = B, N
+    a.req_offsets, a.draft_tok = req_offsets.data_ptr(), draft_tok.data_ptr()
+    a.accepted_len, a.accepted_path = accepted_len.data_ptr(), accepted_path.data_ptr()
+    a.bonus_token = bonus_token.data_ptr()
+    a.commit_off, a.commit_tok, a.commit_row = c_off.data_ptr(), c_tok.data_ptr(), c_row.data_ptr()
+    if row_src is not None:
+        if row_src.device.type != "cuda" or not row_src.is_contiguous() or row_src.shape[0] != N:
+            raise ValueError("row_src: a contiguous GPU tensor with N rows")
+        dst = torch.empty_like(row_src)
+        a.row_src, a.row_dst = row_src.data_ptr(), dst.data_ptr()
+        a.row_bytes = row_src[0].numel() * row_src.element_size() if N else 4
+    a.req_status = status.data_ptr()
+    _check(load().asv_commit(ctypes.byref(a), _stream_handle(dev)))
+    return c_off, c_tok, c_row, dst, status

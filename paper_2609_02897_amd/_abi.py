@@ -10,11 +10,15 @@ LIB_PATH = os.path.join(_HERE, "libasv.so")
 
 ASV_OK, ASV_EINVAL, ASV_EWORKSPACE, ASV_EHIP = 0, -1, -2, -3
 RS_BAD_ROOT, RS_BAD_PARENT, RS_BAD_TOKEN, RS_BAD_OFFSETS, RS_BAD_TAU = 1, 2, 4, 16, 32
+RS_MASK_SMALL, RS_BAD_PATH = 64, 128
+DS_BAD_SHAPE, DS_OVERFLOW = 1, 2
 HIST_WINDOW = 16
+TOPK_MAX, POOL_MAX = 4, 256
 
 # Every entry point include/asv.h declares.
 EXPORTS = ("asv_version", "asv_status_string", "asv_last_error", "asv_workspace_bytes",
-           "asv_tree_policy", "asv_state_init", "asv_verify")
+           "asv_tree_policy", "asv_state_init", "asv_verify", "asv_draft_workspace_bytes",
+           "asv_draft_step", "asv_draft_prune", "asv_tree_meta", "asv_commit")
 
 
 class AsvReqState(ctypes.Structure):
@@ -49,7 +53,33 @@ class AsvVerifyArgs(ctypes.Structure):
                 ("k1_begin_event", _P), ("k1_end_event", _P)]
 
 
+class AsvDraftTree(ctypes.Structure):
+    _fields_ = [("nsteps", ctypes.c_int32), ("topk", ctypes.c_int32), ("ndt", ctypes.c_int32),
+                ("steps", ctypes.c_int32), ("n_pool", ctypes.c_int32),
+                ("n_front", ctypes.c_int32), ("status", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("front", ctypes.c_int32 * TOPK_MAX),
+                ("front_score", ctypes.c_float * TOPK_MAX), ("tok", ctypes.c_int32 * POOL_MAX),
+                ("par", ctypes.c_int32 * POOL_MAX), ("score", ctypes.c_float * POOL_MAX)]
+
+
+class AsvDraftArgs(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("H", ctypes.c_int32), ("V", ctypes.c_int32),
+                ("step", ctypes.c_int32), ("hidden", _P), ("w_draft", _P), ("vocab_map", _P),
+                ("state", _P), ("shape", ctypes.c_int32 * 3), ("tree", _P), ("topk_id", _P),
+                ("topk_logp", _P), ("row_lse", _P), ("front_tok", _P), ("draft_conf", _P),
+                ("k_begin_event", _P), ("k_end_event", _P)]
+
+
+class AsvCommitArgs(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("N", ctypes.c_int32), ("req_offsets", _P),
+                ("draft_tok", _P), ("accepted_len", _P), ("accepted_path", _P),
+                ("bonus_token", _P), ("commit_off", _P), ("commit_tok", _P),
+                ("commit_row", _P), ("row_src", _P), ("row_dst", _P),
+                ("row_bytes", ctypes.c_int64), ("req_status", _P)]
+
+
 assert ctypes.sizeof(AsvReqState) == 112
+assert ctypes.sizeof(AsvDraftTree) == 3136
 
 
 class LibraryMissing(RuntimeError):
@@ -90,5 +120,17 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.asv_state_init.argtypes = [_P, ctypes.c_int32, ctypes.POINTER(AsvParams), _P]
     lib.asv_verify.restype = ctypes.c_int
     lib.asv_verify.argtypes = [ctypes.POINTER(AsvVerifyArgs), _P, ctypes.c_uint64, _P]
+    lib.asv_draft_workspace_bytes.restype = ctypes.c_int
+    lib.asv_draft_workspace_bytes.argtypes = [ctypes.c_int32] * 3 + [
+        ctypes.POINTER(ctypes.c_uint64)]
+    lib.asv_draft_step.restype = ctypes.c_int
+    lib.asv_draft_step.argtypes = [ctypes.POINTER(AsvDraftArgs), _P, ctypes.c_uint64, _P]
+    lib.asv_draft_prune.restype = ctypes.c_int
+    lib.asv_draft_prune.argtypes = [_P, ctypes.c_int32, _P, ctypes.c_int32, _P, _P, _P, _P, _P]
+    lib.asv_tree_meta.restype = ctypes.c_int
+    lib.asv_tree_meta.argtypes = [_P, _P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_int32,
+                                  _P, _P, _P, _P]
+    lib.asv_commit.restype = ctypes.c_int
+    lib.asv_commit.argtypes = [ctypes.POINTER(AsvCommitArgs), _P]
     _lib = lib
     return lib

@@ -10,7 +10,7 @@ ROOT = os.path.dirname(_HERE)
 SOURCES = [os.path.join(_HERE, "csrc", "asv_api.hip")]
 HEADERS = [os.path.join(ROOT, "include", "asv.h")] + [
     os.path.join(_HERE, "csrc", f) for f in ("k_common.h", "k_lmhead.h", "k_reduce.h",
-                                               "k_accept.h")]
+                                               "k_accept.h", "k_draft.h", "k_tree.h")]
 OUT = os.path.join(_HERE, "libasv.so")
 # measurement-only library (achievable-peak microbenchmarks), separate from libasv
 MICROBENCH_SOURCES = [os.path.join(_HERE, "csrc", "microbench.hip")]

@@ -6,8 +6,10 @@
 
 #include "asv.h"
 #include "k_accept.h"
+#include "k_draft.h"
 #include "k_lmhead.h"
 #include "k_reduce.h"
+#include "k_tree.h"
 
 namespace asv {
 namespace {
@@ -132,6 +134,65 @@ AcceptArgs accept_args(const asv_verify_args* a, const Layout& L, char* ws, bool
   return r;
 }
 
+// ---- draft side
+
+// Tile families of the draft LM head (K5), by draft rows R = 4B. The draft vocabulary is small
+// (tens of thousands of rows), so narrow vocabulary slabs keep the launch above the CU count.
+// Beyond 64 rows the 128-row tile repeats over row tiles (a 256-row tile with the top-4
+// epilogue exceeds the register file).
+enum class DraftTile { kRows32, kRows64, kRows128 };
+
+DraftTile pick_draft_tile(int R) {
+  if (R <= 32) return DraftTile::kRows32;
+  if (R <= 64) return DraftTile::kRows64;
+  return DraftTile::kRows128;
+}
+
+int draft_slab(DraftTile t) { return t == DraftTile::kRows128 ? 128 : 64; }
+
+struct DraftLayout {
+  int S = 0;  // vocabulary slabs of the chosen tile
+  size_t off_v = 0, off_i = 0, off_s = 0, bytes = 0;
+};
+
+DraftLayout draft_layout(int B, int V) {
+  DraftLayout L;
+  const int R = B * kTopK;
+  L.S = (V + draft_slab(pick_draft_tile(R)) - 1) / draft_slab(pick_draft_tile(R));
+  const size_t rec = (size_t)R * L.S;
+  size_t at = 0;
+  L.off_v = at; at += align_up(rec * kTopK * 4);
+  L.off_i = at; at += align_up(rec * kTopK * 4);
+  L.off_s = at; at += align_up(rec * 4);
+  L.bytes = at;
+  return L;
+}
+
+bool draft_sizes_ok(int B, int H, int V) {
+  if (B < 0 || H <= 0 || V < kTopK) return false;
+  if (H % kKAlign != 0 || H > (1 << 20)) return false;
+  // 32-bit offsets inside a tile's buffer resource: all 4B rows of X and one slab of W
+  if ((int64_t)B * kTopK * H * 2 >= (int64_t)1 << 31) return false;
+  return true;
+}
+
+template <int TV, int TR, int WV, int WR, int BK, int NST, int PF = 0>
+void launch_draft(const asv_draft_args* a, const DraftLayout& L, char* ws, hipStream_t s) {
+  const int R = a->B * kTopK;
+  const int RT = (R + TR - 1) / TR;
+  k_draft_partial<TV, TR, WV, WR, BK, NST, PF><<<L.S * RT, WV * WR * kWave, 0, s>>>(
+      a->hidden, a->w_draft, R, a->H, a->V, L.S, RT, reinterpret_cast<float*>(ws + L.off_v),
+      reinterpret_cast<int32_t*>(ws + L.off_i), reinterpret_cast<float*>(ws + L.off_s));
+}
+
+int record_event(void* ev, hipStream_t s, const char* what) {
+  if (!ev) return ASV_OK;
+  const hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev), s);
+  if (e == hipSuccess) return ASV_OK;
+  set_error(what, e);
+  return ASV_EHIP;
+}
+
 }  // namespace
 }  // namespace asv
 
@@ -248,4 +309,119 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
   if (int rc = launch_status("k_slab_merge")) return rc;
   k_tree_accept<<<a->B, kWave, 0, s>>>(cnt + a->B, acc);
   return launch_status("k_tree_accept");
+}
+
+extern "C" int asv_draft_workspace_bytes(int32_t B, int32_t H, int32_t V, uint64_t* bytes) {
+  if (!bytes || !draft_sizes_ok(B, H, V)) return ASV_EINVAL;
+  *bytes = draft_layout(B, V).bytes;
+  return ASV_OK;
+}
+
+extern "C" int asv_draft_step(const asv_draft_args* a, void* workspace, uint64_t workspace_bytes,
+                              void* stream) {
+  if (!a || !draft_sizes_ok(a->B, a->H, a->V) || a->step < 0) return ASV_EINVAL;
+  if (a->B == 0) return ASV_OK;
+  if (!a->hidden || !a->w_draft || !a->tree || !a->topk_id || !a->topk_logp || !a->row_lse ||
+      !a->front_tok)
+    return ASV_EINVAL;
+  if (!aligned16(a->hidden) || !aligned16(a->w_draft)) return ASV_EINVAL;
+  if (!a->state && a->step == 0) {
+    const int ns = a->shape[0], tk = a->shape[1], nd = a->shape[2];
+    if (!(ns >= 1 && tk >= 1 && tk <= kTopK && nd >= 1 && ns <= kPoolMax &&
+          tk + (ns - 1) * tk * tk <= kPoolMax))
+      return ASV_EINVAL;
+  }
+  const DraftLayout L = draft_layout(a->B, a->V);
+  if (!workspace || workspace_bytes < L.bytes ||
+      (reinterpret_cast<uintptr_t>(workspace) % kAlign) != 0)
+    return ASV_EWORKSPACE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  (void)hipGetLastError();
+  if (int rc = record_event(a->k_begin_event, s, "hipEventRecord(k_begin_event)")) return rc;
+  switch (pick_draft_tile(a->B * kTopK)) {
+    // <vocab rows, draft rows, waves along vocab, waves along rows, K per stage, ring depth,
+    // W L2-prefetch distance>
+    case DraftTile::kRows32: launch_draft<64, 32, 2, 1, 64, 4>(a, L, ws, s); break;
+    case DraftTile::kRows64: launch_draft<64, 64, 2, 2, 64, 4>(a, L, ws, s); break;
+    case DraftTile::kRows128: launch_draft<128, 128, 2, 2, 64, 3>(a, L, ws, s); break;
+  }
+  if (int rc = launch_status("k_draft_partial")) return rc;
+  if (int rc = record_event(a->k_end_event, s, "hipEventRecord(k_end_event)")) return rc;
+  DraftGrowArgs g;
+  g.B = a->B;
+  g.S = L.S;
+  g.step = a->step;
+  g.rec_v = reinterpret_cast<const float*>(ws + L.off_v);
+  g.rec_i = reinterpret_cast<const int32_t*>(ws + L.off_i);
+  g.rec_s = reinterpret_cast<const float*>(ws + L.off_s);
+  g.vocab_map = a->vocab_map;
+  g.state = a->state;
+  for (int k = 0; k < 3; ++k) g.shape[k] = a->shape[k];
+  g.tree = a->tree;
+  g.topk_id = a->topk_id;
+  g.topk_logp = a->topk_logp;
+  g.row_lse = a->row_lse;
+  g.front_tok = a->front_tok;
+  g.draft_conf = a->draft_conf;
+  k_draft_grow<<<a->B, kDraftThreads, 0, s>>>(g);
+  return launch_status("k_draft_grow");
+}
+
+extern "C" int asv_draft_prune(const asv_draft_tree* tree, int32_t B, const int32_t* root_tok,
+                               int32_t n_cap, int32_t* parent, int32_t* draft_tok,
+                               int32_t* req_offsets, int32_t* req_status, void* stream) {
+  if (B < 0 || n_cap < 0) return ASV_EINVAL;
+  if (B == 0) return ASV_OK;
+  if (!tree || !parent || !draft_tok || !req_offsets || !req_status) return ASV_EINVAL;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  k_draft_prune<<<B, kPruneThreads, 0, s>>>(tree, B, root_tok, n_cap, parent, draft_tok,
+                                            req_offsets, req_status);
+  return launch_status("k_draft_prune");
+}
+
+extern "C" int asv_tree_meta(const int32_t* parent, const int32_t* req_offsets, int32_t B,
+                             int32_t N, const int32_t* pos_base, int32_t mask_words,
+                             int32_t* pos, uint32_t* mask, int32_t* req_status, void* stream) {
+  if (B < 0 || N < B || (B == 0) != (N == 0)) return ASV_EINVAL;
+  if (B == 0) return ASV_OK;
+  if (!parent || !req_offsets || !req_status || (mask && mask_words < 1)) return ASV_EINVAL;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  k_tree_meta<<<B, kMetaThreads, 0, s>>>(parent, req_offsets, B, N, pos_base, mask_words, pos,
+                                         mask, req_status);
+  return launch_status("k_tree_meta");
+}
+
+extern "C" int asv_commit(const asv_commit_args* a, void* stream) {
+  if (!a || a->B < 0 || a->N < a->B || (a->B == 0) != (a->N == 0)) return ASV_EINVAL;
+  if (a->B == 0) return ASV_OK;
+  if (!a->req_offsets || !a->draft_tok || !a->accepted_len || !a->accepted_path ||
+      !a->bonus_token || !a->commit_off || !a->commit_tok || !a->commit_row || !a->req_status)
+    return ASV_EINVAL;
+  if (a->row_src) {
+    if (!a->row_dst || a->row_bytes <= 0 || a->row_bytes % 4 != 0) return ASV_EINVAL;
+    if ((reinterpret_cast<uintptr_t>(a->row_src) | reinterpret_cast<uintptr_t>(a->row_dst)) & 3)
+      return ASV_EINVAL;
+  }
+  CommitArgs c;
+  c.B = a->B;
+  c.N = a->N;
+  c.off = a->req_offsets;
+  c.tok = a->draft_tok;
+  c.acc_len = a->accepted_len;
+  c.path = a->accepted_path;
+  c.bonus = a->bonus_token;
+  c.c_off = a->commit_off;
+  c.c_tok = a->commit_tok;
+  c.c_row = a->commit_row;
+  c.src = static_cast<const char*>(a->row_src);
+  c.dst = static_cast<char*>(a->row_dst);
+  c.row_bytes = a->row_bytes;
+  c.status = a->req_status;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  k_commit<<<a->B, kCommitThreads, 0, s>>>(c);
+  return launch_status("k_commit");
 }

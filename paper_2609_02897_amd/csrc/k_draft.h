@@ -1,0 +1,464 @@
+// Draft side of a decoding step (Sec. 2, "Draft"): the draft LM head reduced to each row's top-4
+// and log-sum-exp, one growth step of every request's draft tree, and the final pruning to the
+// verification budget.
+//
+// K5 k_draft_partial: the LM-head tile of K1 (same staging, MFMA and accumulator layout) with a
+//   top-4 epilogue: per (draft row, 256-entry vocabulary slab) it writes the slab's four best
+//   (logit, id) pairs, best first, and the sum of exp(z - best). The logits never reach memory.
+// K6 k_draft_grow: one workgroup per request, one wave per draft row (4 rows per request):
+//   merge the slab records of the row, then wave 0 applies the growth step to the request's tree.
+// K7 k_draft_prune: one workgroup per request: rank the pool, keep the best ndt - 1 nodes in
+//   pool order and write the verification layout.
+//
+// Order of (logit, id) pairs everywhere: higher logit first, lower id on equal logits; a logit
+// that is not a number is taken as -inf before any comparison.
+#pragma once
+
+#include "asv.h"
+#include "k_common.h"
+#include "k_lmhead.h"
+
+namespace asv {
+
+constexpr int kTopK = ASV_TOPK_MAX;   // 4
+constexpr int kPoolMax = ASV_POOL_MAX;
+constexpr int kDraftThreads = kTopK * kWave;
+
+__device__ __forceinline__ bool pair_better(float va, int ia, float vb, int ib) {
+  return va > vb || (va == vb && ia < ib);
+}
+
+// Four (logit, id) pairs in the pair order, plus the sum of exp(z - v[0]) over the set they
+// were taken from (0 for an empty set).
+struct Top4 {
+  float v[kTopK];
+  int i[kTopK];
+  float s;
+};
+
+__device__ __forceinline__ Top4 top4_empty() {
+  Top4 t;
+#pragma unroll
+  for (int k = 0; k < kTopK; ++k) {
+    t.v[k] = kNegInf;
+    t.i[k] = kNoIndex;
+  }
+  t.s = 0.f;
+  return t;
+}
+
+// Slot a keeps the better pair.
+__device__ __forceinline__ void pair_order(float& va, int& ia, float& vb, int& ib) {
+  const bool sw = pair_better(vb, ib, va, ia);
+  const float tv = sw ? vb : va;
+  const int ti = sw ? ib : ia;
+  vb = sw ? va : vb;
+  ib = sw ? ia : ib;
+  va = tv;
+  ia = ti;
+}
+
+// The four best pairs of two sorted lists with disjoint ids: the better of a[k] and b[3-k] for
+// every k is a bitonic sequence holding them, which two compare-exchange stages sort. The sums
+// merge like online-softmax records.
+__device__ __forceinline__ Top4 top4_merge(const Top4& a, const Top4& b) {
+  Top4 c;
+#pragma unroll
+  for (int k = 0; k < kTopK; ++k) {
+    const bool ta = pair_better(a.v[k], a.i[k], b.v[3 - k], b.i[3 - k]);
+    c.v[k] = ta ? a.v[k] : b.v[3 - k];
+    c.i[k] = ta ? a.i[k] : b.i[3 - k];
+  }
+  pair_order(c.v[0], c.i[0], c.v[2], c.i[2]);
+  pair_order(c.v[1], c.i[1], c.v[3], c.i[3]);
+  pair_order(c.v[0], c.i[0], c.v[1], c.i[1]);
+  pair_order(c.v[2], c.i[2], c.v[3], c.i[3]);
+  const Rec r = rec_merge(Rec{a.v[0], a.s, 0}, Rec{b.v[0], b.s, 0});
+  c.s = r.s;
+  // Opaque to the optimiser: chains of these merges (a slab loop followed by a butterfly) are
+  // otherwise folded into select trees that grow exponentially with the chain length and
+  // stall the compiler. The empty asm costs no instruction.
+#pragma unroll
+  for (int k = 0; k < kTopK; ++k) asm volatile("" : "+v"(c.v[k]), "+v"(c.i[k]));
+  return c;
+}
+
+__device__ __forceinline__ Top4 top4_shfl_xor(const Top4& x, int mask) {
+  Top4 y;
+#pragma unroll
+  for (int k = 0; k < kTopK; ++k) {
+    y.v[k] = __shfl_xor(x.v[k], mask, kWave);
+    y.i[k] = __shfl_xor(x.i[k], mask, kWave);
+  }
+  y.s = __shfl_xor(x.s, mask, kWave);
+  return y;
+}
+
+// ------------------------------------------------------------------------------------------ K5
+
+template <int TV, int TR, int WV, int WR, int BK, int NST, int PF = 0>
+__global__ __launch_bounds__(WV * WR * kWave, 1)
+void k_draft_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int R,
+                     int H, int V, int S, int RT, float* __restrict__ rec_v,
+                     int32_t* __restrict__ rec_i, float* __restrict__ rec_s) {
+  using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
+  constexpr int T = C::kThreads;
+  __shared__ uint4 smem[(C::kLds + lmhead_sink_bytes<TV, TR, WV, WR, PF>()) / 16];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wv = wave % WV, wr = wave / WV;
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  const int slab = tile / RT, rt = tile % RT;
+  const int v0 = slab * TV, r0 = rt * TR;
+
+  f32x16 acc[C::MV][C::MR];
+  lmhead_tile<TV, TR, WV, WR, BK, NST, PF, false, -1>(X, W, R, H, V, v0, r0, smem, acc);
+
+  // Output block (i, j), register e of a lane holds vocabulary row
+  //   v0 + wv * kWaveV + 32 i + 8 (e / 4) + 4 (lane / 32) + e % 4   and
+  // tree row wr * kWaveR + 32 j + lane % 32. For a fixed lane the entry ordinal k = 16 i + e
+  // visits the lane's vocabulary ids in increasing order.
+  const bool full_slab = v0 + TV <= V;
+  const int vlane = v0 + wv * C::kWaveV + 4 * (lane >> 5);
+  auto entry_v = [&](int k) { return vlane + 32 * (k >> 4) + 8 * ((k & 15) >> 2) + (k & 3); };
+  // Lane-local top-4 of row block j: the first four entries sorted, then every later entry
+  // inserted where it beats a kept one strictly (it has the highest id so far, so it loses
+  // ties). MASK drops entries past V (last slab).
+  auto lane_top4 = [&](int j, auto mask_tag) -> Top4 {
+    constexpr bool MASK = decltype(mask_tag)::value;
+    auto entry = [&](int k) {
+      float z = fmaxf(acc[k >> 4][j][k & 15], kNegInf);    // a non-number becomes -inf
+      if constexpr (MASK) z = entry_v(k) < V ? z : kNegInf;
+      return z;
+    };
+    Top4 t;
+#pragma unroll
+    for (int k = 0; k < kTopK; ++k) {
+      t.v[k] = entry(k);
+      t.i[k] = entry_v(k);
+    }
+    pair_order(t.v[0], t.i[0], t.v[1], t.i[1]);
+    pair_order(t.v[2], t.i[2], t.v[3], t.i[3]);
+    pair_order(t.v[0], t.i[0], t.v[2], t.i[2]);
+    pair_order(t.v[1], t.i[1], t.v[3], t.i[3]);
+    pair_order(t.v[1], t.i[1], t.v[2], t.i[2]);
+#pragma unroll
+    for (int k = kTopK; k < C::MV * 16; ++k) {
+      const float z = entry(k);
+      const int id = entry_v(k);
+      const bool b0 = z > t.v[0], b1 = z > t.v[1], b2 = z > t.v[2], b3 = z > t.v[3];
+      t.v[3] = b2 ? t.v[2] : (b3 ? z : t.v[3]);
+      t.i[3] = b2 ? t.i[2] : (b3 ? id : t.i[3]);
+      t.v[2] = b1 ? t.v[1] : (b2 ? z : t.v[2]);
+      t.i[2] = b1 ? t.i[1] : (b2 ? id : t.i[2]);
+      t.v[1] = b0 ? t.v[0] : (b1 ? z : t.v[1]);
+      t.i[1] = b0 ? t.i[0] : (b1 ? id : t.i[1]);
+      t.v[0] = b0 ? z : t.v[0];
+      t.i[0] = b0 ? id : t.i[0];
+    }
+    const float mb = t.v[0] * kLog2e;
+    float sum = 0.f;
+#pragma unroll
+    for (int k = 0; k < C::MV * 16; ++k) sum += exp2_rel(fmaf(entry(k), kLog2e, -mb));
+    t.s = t.v[0] == kNegInf ? 0.f : sum;
+    return t;
+  };
+
+  // Per-row exchange area in the (now idle) LDS ring: WV records of 9 words per tree row.
+  float* const x_v = reinterpret_cast<float*>(smem);
+  int* const x_i = reinterpret_cast<int*>(x_v + WV * TR * kTopK);
+  float* const x_s = reinterpret_cast<float*>(x_i + WV * TR * kTopK);
+  static_assert(WV * TR * (2 * kTopK + 1) * 4 <= C::kLds, "exchange area exceeds the ring");
+#pragma unroll
+  for (int j = 0; j < C::MR; ++j) {
+    if (r0 + wr * C::kWaveR + 32 * j >= R) continue;        // row block past the last row
+    Top4 t = full_slab ? lane_top4(j, std::false_type{}) : lane_top4(j, std::true_type{});
+    t = top4_merge(t, top4_shfl_xor(t, 32));
+    if (lane < 32) {
+      const int at = wv * TR + wr * C::kWaveR + 32 * j + lane;
+#pragma unroll
+      for (int k = 0; k < kTopK; ++k) {
+        x_v[at * kTopK + k] = t.v[k];
+        x_i[at * kTopK + k] = t.i[k];
+      }
+      x_s[at] = t.s;
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  __syncthreads();
+  for (int row = tid; row < TR; row += T) {
+    const int n = r0 + row;
+    if (n >= R) break;
+    auto load = [&](int w) {
+      Top4 t;
+      const int at = w * TR + row;
+#pragma unroll
+      for (int k = 0; k < kTopK; ++k) {
+        t.v[k] = x_v[at * kTopK + k];
+        t.i[k] = x_i[at * kTopK + k];
+      }
+      t.s = x_s[at];
+      return t;
+    };
+    Top4 t = load(0);
+#pragma unroll
+    for (int w = 1; w < WV; ++w) t = top4_merge(t, load(w));
+    const size_t at = (size_t)n * S + slab;
+    *reinterpret_cast<float4*>(rec_v + at * kTopK) = make_float4(t.v[0], t.v[1], t.v[2], t.v[3]);
+    *reinterpret_cast<int4*>(rec_i + at * kTopK) = make_int4(t.i[0], t.i[1], t.i[2], t.i[3]);
+    rec_s[at] = t.s;
+  }
+}
+
+// ------------------------------------------------------------------------------------------ K6
+
+struct DraftGrowArgs {
+  int B, S, step;
+  const float* rec_v;
+  const int32_t* rec_i;
+  const float* rec_s;
+  const int32_t* vocab_map;
+  const asv_req_state* state;
+  int shape[3];
+  asv_draft_tree* tree;
+  int32_t* topk_id;
+  float* topk_logp;
+  float* row_lse;
+  int32_t* front_tok;
+  float* draft_conf;
+};
+
+__device__ __forceinline__ bool draft_shape_ok(int nsteps, int topk, int ndt) {
+  return nsteps >= 1 && topk >= 1 && topk <= kTopK && ndt >= 1 &&
+         nsteps <= kPoolMax && topk + (nsteps - 1) * topk * topk <= kPoolMax;
+}
+
+__global__ __launch_bounds__(kDraftThreads)
+void k_draft_grow(DraftGrowArgs a) {
+  __shared__ int s_id[kTopK][kTopK];
+  __shared__ float s_lp[kTopK][kTopK];
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
+  const int slot = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int row = b * kTopK + slot;
+
+  // ---- merge the S slab records of this wave's row (lane l takes slabs l, l + 64, ...)
+  Top4 t = top4_empty();
+  for (int sl = lane; sl < a.S; sl += kWave) {
+    const size_t at = (size_t)row * a.S + sl;
+    const float4 v = *reinterpret_cast<const float4*>(a.rec_v + at * kTopK);
+    const int4 i = *reinterpret_cast<const int4*>(a.rec_i + at * kTopK);
+    Top4 r;
+    r.v[0] = v.x; r.v[1] = v.y; r.v[2] = v.z; r.v[3] = v.w;
+    r.i[0] = i.x; r.i[1] = i.y; r.i[2] = i.z; r.i[3] = i.w;
+    r.s = a.rec_s[at];
+    t = top4_merge(t, r);
+  }
+#pragma unroll
+  for (int mask = 32; mask >= 1; mask >>= 1) t = top4_merge(t, top4_shfl_xor(t, mask));
+  // every lane holds the same four pairs; lane 0's sum is the one used, for determinism
+  const float s0 = lane_value(t.s, 0);
+  const float lse = t.v[0] == kNegInf ? kNegInf : t.v[0] + logf(s0);
+  if (lane < kTopK) {
+    float v = t.v[0];
+    int id = t.i[0];
+#pragma unroll
+    for (int k = 1; k < kTopK; ++k)
+      if (lane == k) {
+        v = t.v[k];
+        id = t.i[k];
+      }
+    float lp = v - lse;
+    lp = lp != lp ? kNegInf : lp;
+    const int tok = a.vocab_map ? a.vocab_map[id] : id;
+    a.topk_id[row * kTopK + lane] = tok;
+    a.topk_logp[row * kTopK + lane] = lp;
+    s_id[slot][lane] = tok;
+    s_lp[slot][lane] = lp;
+  }
+  if (lane == 0) a.row_lse[row] = lse;
+  __syncthreads();
+  if (slot != 0) return;
+
+  // ---- wave 0: one growth step of request b's tree
+  asv_draft_tree* tr = a.tree + b;
+  int nsteps, topk, ndt, steps, n_pool, n_front, status;
+  int front[kTopK];
+  float fscore[kTopK];
+  if (a.step == 0) {
+    if (a.state) {
+      nsteps = a.state[b].shape[0];
+      topk = a.state[b].shape[1];
+      ndt = a.state[b].shape[2];
+    } else {
+      nsteps = a.shape[0];
+      topk = a.shape[1];
+      ndt = a.shape[2];
+    }
+    steps = 0;
+    n_pool = 0;
+    n_front = 1;
+    status = draft_shape_ok(nsteps, topk, ndt) ? 0 : ASV_DS_BAD_SHAPE;
+#pragma unroll
+    for (int k = 0; k < kTopK; ++k) {
+      front[k] = -1;
+      fscore[k] = 0.f;
+    }
+    if (a.draft_conf && lane == 0) a.draft_conf[b] = expf(s_lp[0][0]);
+  } else {
+    nsteps = tr->nsteps;
+    topk = tr->topk;
+    ndt = tr->ndt;
+    steps = tr->steps;
+    n_pool = tr->n_pool;
+    n_front = tr->n_front;
+    status = tr->status;
+    if (status == 0 && !draft_shape_ok(nsteps, topk, ndt)) status = ASV_DS_BAD_SHAPE;
+#pragma unroll
+    for (int k = 0; k < kTopK; ++k) {
+      front[k] = tr->front[k];
+      fscore[k] = tr->front_score[k];
+    }
+  }
+  // the header bounds are checked again so that a tree that was never initialised (step > 0
+  // first) cannot send a write outside its pool
+  const bool grow = status == 0 && steps >= 0 && steps < nsteps && n_front >= 1 &&
+                    n_front <= kTopK && n_pool >= 0 && n_pool + n_front * topk <= kPoolMax;
+  int new_front_tok = -1;
+  if (grow) {
+    // candidate q = j * topk + c: child c of frontier slot j
+    const int ncand = n_front * topk;
+    float sc = kNegInf;
+    int tok = -1, par = -1;
+    if (lane < ncand) {
+      const int j = lane / topk, c = lane % topk;
+      float fs = fscore[0];
+      int fp = front[0];
+#pragma unroll
+      for (int k = 1; k < kTopK; ++k)
+        if (j == k) {
+          fs = fscore[k];
+          fp = front[k];
+        }
+      sc = __fadd_rn(fs, s_lp[j][c]);
+      tok = s_id[j][c];
+      par = fp;
+    }
+    int rank = 0;
+    for (int q = 0; q < ncand; ++q) {
+      const float sq = lane_value(sc, q);
+      rank += (sq > sc || (sq == sc && q < lane)) ? 1 : 0;
+    }
+    if (lane < ncand) {
+      tr->tok[n_pool + lane] = tok;
+      tr->par[n_pool + lane] = par;
+      tr->score[n_pool + lane] = sc;
+    }
+      if (lane < ncand && rank < topk) {
+      tr->front[rank] = n_pool + lane;
+      tr->front_score[rank] = sc;
+    }
+    // the token of frontier slot r goes to lane r (the next forward's input order)
+    for (int q = 0; q < ncand; ++q) {
+      const int rq = lane_value(rank, q), tq = lane_value(tok, q);
+      if (rq < topk && lane == rq) new_front_tok = tq;
+    }
+    if (lane == 0) {
+      tr->n_pool = n_pool + ncand;
+      tr->n_front = topk;
+      tr->steps = steps + 1;
+    }
+  }
+  if (a.step == 0 && lane == 0) {
+    tr->nsteps = nsteps;
+    tr->topk = topk;
+    tr->ndt = ndt;
+    tr->status = status;
+    tr->reserved = 0;
+    if (!grow) {
+      tr->steps = 0;
+      tr->n_pool = 0;
+      tr->n_front = 1;
+      tr->front[0] = -1;
+      tr->front_score[0] = 0.f;
+    }
+  }
+  if (lane < kTopK) a.front_tok[b * kTopK + lane] = new_front_tok;
+}
+
+// ------------------------------------------------------------------------------------------ K7
+
+constexpr int kPruneThreads = kPoolMax;
+
+__device__ __forceinline__ int draft_tree_rows(const asv_draft_tree* t) {
+  const int n_pool = t->n_pool, ndt = t->ndt;
+  if (t->status != 0 || n_pool < 0 || n_pool > kPoolMax || ndt < 1) return 1;
+  return 1 + min(ndt - 1, n_pool);
+}
+
+__global__ __launch_bounds__(kPruneThreads)
+void k_draft_prune(const asv_draft_tree* __restrict__ trees, int B,
+                   const int32_t* __restrict__ root_tok, int n_cap, int32_t* __restrict__ parent,
+                   int32_t* __restrict__ draft_tok, int32_t* __restrict__ req_offsets,
+                   int32_t* __restrict__ req_status) {
+  __shared__ float s_score[kPoolMax];
+  __shared__ int s_map[kPoolMax];
+  __shared__ int s_part[kPruneThreads / kWave];
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const asv_draft_tree* t = trees + b;
+
+  // ---- offset of this request: rows of all earlier trees
+  __shared__ int s_lo;
+  if (tid == 0) s_lo = 0;
+  __syncthreads();
+  int part = 0;
+  for (int q = tid; q < b; q += kPruneThreads) part += draft_tree_rows(trees + q);
+  if (part) atomicAdd(&s_lo, part);
+  __syncthreads();
+  const int lo = s_lo;
+  const int n = draft_tree_rows(t);
+  const int hi = lo + n;
+  if (tid == 0) {
+    req_offsets[b + 1] = hi;
+    if (b == 0) req_offsets[0] = 0;
+    req_status[b] = t->status | (hi > n_cap ? ASV_DS_OVERFLOW : 0);
+  }
+  if (hi > n_cap) return;
+  if (tid == 0) {
+    parent[lo] = -1;
+    draft_tok[lo] = root_tok ? root_tok[b] : -1;
+  }
+  if (n == 1) return;
+
+  // ---- rank the pool: the n - 1 best (higher score, earlier entry on ties) are kept
+  const int P = t->n_pool, m = n - 1;
+  const float sq = tid < P ? t->score[tid] : kNegInf;
+  if (tid < P) s_score[tid] = sq;
+  __syncthreads();
+  int rank = 0;
+  for (int q = 0; q < P; ++q) {
+    const float s = s_score[q];
+    rank += (s > sq || (s == sq && q < tid)) ? 1 : 0;
+  }
+  const bool keep = tid < P && rank < m;
+  // ---- position of each kept entry in pool order: exclusive prefix count of `keep`
+  const uint64_t bal = __ballot(keep);
+  const int before = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32),
+                                               __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+  if (lane == 0) s_part[wave] = __popcll(bal);
+  __syncthreads();
+  int base = 0;
+  for (int w = 0; w < wave; ++w) base += s_part[w];
+  if (tid < P) s_map[tid] = keep ? 1 + base + before : -1;
+  __syncthreads();
+  if (keep) {
+    const int node = lo + 1 + base + before;
+    const int p = t->par[tid];
+    // parents score at least as high and come earlier, so a kept node's parent is kept
+    const int pl = p < 0 ? 0 : (p < P && s_map[p] > 0 ? s_map[p] : 0);
+    parent[node] = lo + pl;
+    draft_tok[node] = t->tok[tid];
+  }
+}
+
+}  // namespace asv

@@ -127,53 +127,49 @@ __device__ __forceinline__ int xcd_tile(int bid, int G) {
   return xcd * q + min(xcd, rem) + loc;
 }
 
+// LDS bytes of the L2-prefetch sink (PF > 0): one 1 KB region per wave, never read.
+template <int TV, int TR, int WV, int WR, int PF>
+constexpr int lmhead_sink_bytes() { return PF > 0 ? WV * WR * 1024 : 0; }
+
+// The logits of one tile, left in the MFMA accumulators: acc[i][j] holds the 32x32 block of
+// vocabulary rows v0 + wv * kWaveV + 32 i .. and tree rows r0 + wr * kWaveR + 32 j .. of this
+// wave, summed over all of H. Rows past V or past N read as zeros. On return every stage copy
+// has landed and the workgroup has passed a barrier, so the caller may reuse the LDS ring.
+//
 // PF > 0: every stage also pulls the W lines of stage k + PF into L2 (one 4-byte LDS-sink
 // load per W row), so the stage copies that follow hit L2 instead of waiting on HBM.
-// IGLP >= 0: the compiler's MFMA / LDS-read interleaving strategy of that number is applied to
-// each K16 step that reads the next step's fragments (-1: the default schedule).
-template <int TV, int TR, int WV, int WR, int BK, int NST, int OCC = 1, int ORDER = 0,
-          int PF = 0, bool PFX = false, int IGLP = -1>
-__global__ __launch_bounds__(WV * WR * kWave, OCC)
-void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
-                      const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
-                      const int32_t* __restrict__ req_offsets, int B, int N, int H, int V,
-                      int S, int RT, float* __restrict__ rec_m, float* __restrict__ rec_s,
-                      int32_t* __restrict__ rec_a, float* __restrict__ drafted_logit,
-                      int32_t* __restrict__ done_cnt, int n_cnt) {
+// PFX: the same for the X rows. IGLP >= 0: the compiler's MFMA / LDS-read interleaving
+// strategy of that number is applied to each K16 step that reads the next step's fragments
+// (-1: the default schedule).
+template <int TV, int TR, int WV, int WR, int BK, int NST, int PF, bool PFX, int IGLP>
+__device__ __forceinline__ void lmhead_tile(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int N, int H, int V,
+    int v0, int r0, uint4* smem,
+    f32x16 (&acc)[LmheadCfg<TV, TR, WV, WR, BK, NST>::MV][LmheadCfg<TV, TR, WV, WR, BK, NST>::MR]) {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
   constexpr int CPR = C::CPR;
-  constexpr int T = C::kThreads;
   constexpr int kPfRows = TV / C::kWaves;             // W rows each wave prefetches
   constexpr int kPfRowsX = TR / C::kWaves;            // X rows each wave prefetches (PFX)
   constexpr int kPfW = PF > 0 ? kPfRows / kWave : 0;
   constexpr int kPfX = PF > 0 && PFX ? kPfRowsX / kWave : 0;
   constexpr int kPf = kPfW + kPfX;                    // prefetch loads per wave per stage
-  constexpr int kSink = PF > 0 ? C::kWaves * 1024 : 0;
   constexpr int kGroup = C::kLoads + kPf;             // vector-memory ops per wave per stage
   static_assert(PF == 0 || (kPfRows % kWave == 0 && (!PFX || kPfRowsX % kWave == 0)),
                 "whole prefetch rows per lane");
   static_assert((NST - 2) * kGroup + kPf <= 63, "vmcnt range");
-  static_assert(C::kLds + kSink <= 160 * 1024, "LDS per workgroup");
-  __shared__ uint4 smem[(C::kLds + kSink) / 16];
+  static_assert(C::kLds + lmhead_sink_bytes<TV, TR, WV, WR, PF>() <= 160 * 1024,
+                "LDS per workgroup");
 
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wv = wave % WV, wr = wave / WV;
-  // clear the per-request completion counters of the finishing kernel that follows
-  for (int i = blockIdx.x * T + tid; i < n_cnt; i += gridDim.x * T) done_cnt[i] = 0;
-  const int tile = xcd_tile(blockIdx.x, gridDim.x);
-  // ORDER 0: consecutive tiles are the row tiles of one slab (W slab shared in L2);
-  // ORDER 1: consecutive tiles are the slabs of one row tile (X tile resident in L2).
-  const int slab = ORDER == 0 ? tile / RT : tile % S;
-  const int rt = ORDER == 0 ? tile % RT : tile / S;
-  const int v0 = slab * TV, r0 = rt * TR;
   const int v_end = min(v0 + TV, V);
   const int r_last = min(r0 + TR, N) - 1;
   const int lds0 = __builtin_amdgcn_readfirstlane((int)(size_t)smem);
 
   // ---- one buffer resource per operand covering only this tile's valid rows: rows past V
   // (last slab) or past N (last row tile) read as zeros and never touch memory outside the
-  // arrays; their results are discarded below.
+  // arrays; their results are discarded by the caller.
   const __amdgpu_buffer_rsrc_t w_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(W + (size_t)v0 * H), (short)0, (v_end - v0) * H * 2, kRsrcWord3);
   const __amdgpu_buffer_rsrc_t x_rsrc = __builtin_amdgcn_make_buffer_rsrc(
@@ -215,28 +211,6 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
     }
   };
 
-  // ---- prefetch what the drafted-logit gather needs: the request offsets (to find the end
-  // of the segment holding the tile's last row; children of the tile's rows lie before it)
-  // and the parent / token of the first candidate nodes after r0.
-  int off_lo = 0, off_hi = 0;
-  if (tid < B) {
-    off_lo = req_offsets[tid];
-    off_hi = req_offsets[tid + 1];
-  }
-  int cc[C::kCand], cp[C::kCand], cd[C::kCand];
-#pragma unroll
-  for (int k = 0; k < C::kCand; ++k) {
-    cc[k] = r0 + 1 + k * T + tid;
-    cp[k] = -1;
-    cd[k] = -1;
-    if (cc[k] < N) {
-      cp[k] = parent[cc[k]];
-      cd[k] = draft_tok[cc[k]];
-    }
-  }
-
-  // ---- main loop over K
-  f32x16 acc[C::MV][C::MR];
 #pragma unroll
   for (int i = 0; i < C::MV; ++i)
 #pragma unroll
@@ -300,10 +274,63 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
     }
   }
   static_assert(NS16 % 2 == 0, "fragment double buffer alternates within a stage");
-  // the last L2 prefetches may still be in flight: every LDS copy lands before the epilogue
-  // and before the workgroup can exit
+  // the last L2 prefetches may still be in flight: every LDS copy lands before the caller
+  // reuses the ring and before the workgroup can exit
   if constexpr (PF > 0) asm volatile("s_waitcnt vmcnt(0)" : : : "memory");
   __syncthreads();
+}
+
+template <int TV, int TR, int WV, int WR, int BK, int NST, int OCC = 1, int ORDER = 0,
+          int PF = 0, bool PFX = false, int IGLP = -1>
+__global__ __launch_bounds__(WV * WR * kWave, OCC)
+void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
+                      const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
+                      const int32_t* __restrict__ req_offsets, int B, int N, int H, int V,
+                      int S, int RT, float* __restrict__ rec_m, float* __restrict__ rec_s,
+                      int32_t* __restrict__ rec_a, float* __restrict__ drafted_logit,
+                      int32_t* __restrict__ done_cnt, int n_cnt) {
+  using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
+  constexpr int T = C::kThreads;
+  __shared__ uint4 smem[(C::kLds + lmhead_sink_bytes<TV, TR, WV, WR, PF>()) / 16];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wv = wave % WV, wr = wave / WV;
+  // clear the per-request completion counters of the finishing kernel that follows
+  for (int i = blockIdx.x * T + tid; i < n_cnt; i += gridDim.x * T) done_cnt[i] = 0;
+  const int tile = xcd_tile(blockIdx.x, gridDim.x);
+  // ORDER 0: consecutive tiles are the row tiles of one slab (W slab shared in L2);
+  // ORDER 1: consecutive tiles are the slabs of one row tile (X tile resident in L2).
+  const int slab = ORDER == 0 ? tile / RT : tile % S;
+  const int rt = ORDER == 0 ? tile % RT : tile / S;
+  const int v0 = slab * TV, r0 = rt * TR;
+  const int v_end = min(v0 + TV, V);
+  const int r_last = min(r0 + TR, N) - 1;
+
+  // ---- prefetch what the drafted-logit gather needs: the request offsets (to find the end
+  // of the segment holding the tile's last row; children of the tile's rows lie before it)
+  // and the parent / token of the first candidate nodes after r0.
+  int off_lo = 0, off_hi = 0;
+  if (tid < B) {
+    off_lo = req_offsets[tid];
+    off_hi = req_offsets[tid + 1];
+  }
+  int cc[C::kCand], cp[C::kCand], cd[C::kCand];
+#pragma unroll
+  for (int k = 0; k < C::kCand; ++k) {
+    cc[k] = r0 + 1 + k * T + tid;
+    cp[k] = -1;
+    cd[k] = -1;
+    if (cc[k] < N) {
+      cp[k] = parent[cc[k]];
+      cd[k] = draft_tok[cc[k]];
+    }
+  }
+
+  // ---- the tile's logits
+  f32x16 acc[C::MV][C::MR];
+  lmhead_tile<TV, TR, WV, WR, BK, NST, PF, PFX, IGLP>(X, W, N, H, V, v0, r0, smem, acc);
+  const int frag_half = lane >> 5;
 
   // Output block (i, j), register e of a lane holds vocab row
   //   32*i + 8*(e/4) + 4*(lane/32) + e%4   (of the wave's vocab range) and

@@ -36,7 +36,7 @@ def test_exports(lib):
 
 
 def test_version_and_status(lib):
-    assert lib.asv_version() == 110
+    assert lib.asv_version() == 120
     for code in (0, -1, -2, -3, 7):
         assert lib.asv_status_string(code)
 
@@ -46,6 +46,11 @@ def test_struct_layouts():
     assert ctypes.sizeof(_abi.AsvParams) == 60
     # 4 ints, 18 pointers, params (60 B, padded to 64), 2 event pointers
     assert ctypes.sizeof(_abi.AsvVerifyArgs) == 16 + 18 * 8 + 64 + 2 * 8
+    assert ctypes.sizeof(_abi.AsvDraftTree) == 64 + 3 * 4 * 256
+    # 4 ints, 4 pointers, 3 ints (+4 padding), 8 pointers
+    assert ctypes.sizeof(_abi.AsvDraftArgs) == 16 + 4 * 8 + 16 + 8 * 8
+    # 2 ints, 10 pointers, an int64, a pointer
+    assert ctypes.sizeof(_abi.AsvCommitArgs) == 8 + 10 * 8 + 8 + 8
 
 
 def test_param_and_policy_checks_on_host(lib):
@@ -144,3 +149,55 @@ def test_microbench_library_exports_and_checks():
     assert mb.asvb_stream_read(p, 64, p, 0, None) == -1
     assert mb.asvb_mfma_loop(None, 4, 4, None) == -1
     assert mb.asvb_mfma_loop(p, 0, 4, None) == -1
+
+
+def test_draft_and_tree_entry_points_reject_on_host(lib):
+    """asv_draft_*, asv_tree_meta and asv_commit reject bad arguments before any HIP call."""
+    out = ctypes.c_uint64(0)
+    assert lib.asv_draft_workspace_bytes(2, 4096, 32000, ctypes.byref(out)) == 0
+    S = (32000 + 63) // 64                         # 8 draft rows use 64-wide vocabulary slabs
+    assert out.value >= 8 * S * (4 + 4 + 1) * 4 and out.value % 256 == 0
+    for bad in [(-1, 64, 10), (1, 100, 10), (1, 64, 3), (1, 0, 10)]:
+        assert lib.asv_draft_workspace_bytes(*bad, ctypes.byref(out)) == asv.ASV_EINVAL, bad
+    a = _abi.AsvDraftArgs()
+    a.B, a.H, a.V, a.step = 0, 64, 10, 0
+    assert lib.asv_draft_step(ctypes.byref(a), None, 0, None) == asv.ASV_OK       # empty batch
+    a.B = 1
+    assert lib.asv_draft_step(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL   # null pointers
+    fake = 0x100000
+    for f in ("hidden", "w_draft", "tree", "topk_id", "topk_logp", "row_lse", "front_tok"):
+        setattr(a, f, fake)
+    for shape in [(0, 1, 1), (1, 5, 4), (1, 1, 0), (17, 4, 8)]:   # the last overflows the pool
+        a.shape = (ctypes.c_int32 * 3)(*shape)
+        assert lib.asv_draft_step(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL, shape
+    a.shape = (ctypes.c_int32 * 3)(3, 4, 4)
+    assert lib.asv_draft_step(ctypes.byref(a), None, 0, None) == asv.ASV_EWORKSPACE
+    a.hidden = fake + 2
+    assert lib.asv_draft_step(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL   # misaligned
+    a.hidden, a.step = fake, -1
+    assert lib.asv_draft_step(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
+
+    p = ctypes.c_void_p(fake)
+    assert lib.asv_draft_prune(None, 0, None, 0, None, None, None, None, None) == asv.ASV_OK
+    assert lib.asv_draft_prune(p, -1, None, 0, p, p, p, p, None) == asv.ASV_EINVAL
+    assert lib.asv_draft_prune(p, 1, None, -1, p, p, p, p, None) == asv.ASV_EINVAL
+    assert lib.asv_draft_prune(p, 1, None, 4, None, p, p, p, None) == asv.ASV_EINVAL
+
+    assert lib.asv_tree_meta(None, None, 0, 0, None, 0, None, None, None, None) == asv.ASV_OK
+    assert lib.asv_tree_meta(p, p, 2, 1, None, 0, p, None, p, None) == asv.ASV_EINVAL  # N < B
+    assert lib.asv_tree_meta(p, p, 1, 4, None, 0, p, p, p, None) == asv.ASV_EINVAL  # 0 words
+    assert lib.asv_tree_meta(None, p, 1, 4, None, 1, p, p, p, None) == asv.ASV_EINVAL
+
+    c = _abi.AsvCommitArgs()
+    assert lib.asv_commit(ctypes.byref(c), None) == asv.ASV_OK                      # B = N = 0
+    c.B, c.N = 1, 4
+    assert lib.asv_commit(ctypes.byref(c), None) == asv.ASV_EINVAL                  # nulls
+    for f in ("req_offsets", "draft_tok", "accepted_len", "accepted_path", "bonus_token",
+              "commit_off", "commit_tok", "commit_row", "req_status"):
+        setattr(c, f, fake)
+    c.row_src, c.row_dst, c.row_bytes = fake, fake, 6                               # not % 4
+    assert lib.asv_commit(ctypes.byref(c), None) == asv.ASV_EINVAL
+    c.row_bytes, c.row_dst = 8, None
+    assert lib.asv_commit(ctypes.byref(c), None) == asv.ASV_EINVAL
+    c.row_dst, c.row_src = fake, fake + 2                                           # misaligned
+    assert lib.asv_commit(ctypes.byref(c), None) == asv.ASV_EINVAL

@@ -1,0 +1,408 @@
+"""GPU parity of the draft side (asv_draft_step, asv_draft_prune) and of the steps around the
+target forward (asv_tree_meta, asv_commit) with the CPU oracle, through the C ABI.
+
+Draft top-4: ids bit-exact outside 1e-3 bands around the logit gaps that decide them (banded
+rows must hold a valid top-4 within the band), log-probabilities and log-sum-exp within 2e-3.
+Tree growth and pruning: bit-exact against the oracle fed with the GPU's own float32 top-4
+(both sides take the integer decisions in float32, as the method states them). Tree metadata
+and commit: bit-exact.
+"""
+
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle
+from harness import BAND, TOL_F
+from workloads import (bf16_weights, build_tree, draft_hidden, draft_shapes, draft_vocab_map,
+                       root_tokens)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module")
+def asv():
+    import paper_2609_02897_amd as m
+    m.load()
+    return m
+
+
+def _t(x, dev):
+    import torch
+    return torch.from_numpy(np.array(x, copy=True, order="C")).to(dev)
+
+
+def _bf16(bits, dev):
+    import torch
+    return _t(np.asarray(bits, dtype=np.uint16).view(np.int16), dev).view(torch.bfloat16)
+
+
+def _state_with_shapes(asv, shapes, dev):
+    raw = b""
+    for s in shapes:
+        st = asv.AsvReqState()
+        st.shape = (ctypes.c_int32 * 3)(*[int(v) for v in s])
+        raw += bytes(st)
+    return _t(np.frombuffer(raw, dtype=np.uint8).reshape(len(shapes), -1), dev)
+
+
+def _check_topk(tag, x_bits, w64, vmap, ids, logp, lse):
+    """GPU top-4 of every row against the oracle, banded where logits are within 1e-3."""
+    x64 = oracle.widen_bf16(x_bits)
+    ref = oracle.draft_topk(x64, w64, 4, vmap)
+    z = oracle.logits(x64, w64)
+    z = np.where(np.isnan(z), -np.inf, z)
+    inv = None if vmap is None else {int(t): i for i, t in enumerate(vmap)}
+    banded = 0
+    for r in range(x64.shape[0]):
+        assert abs(lse[r] - ref["lse"][r]) <= TOL_F or lse[r] == ref["lse"][r], (tag, r)
+        d_ids = [int(i) if inv is None else inv[int(i)] for i in ids[r]]
+        assert len(set(d_ids)) == 4, (tag, r, d_ids)
+        zs = ref["zs"][r]
+        with np.errstate(invalid="ignore"):
+            gaps = zs[:4] - zs[1:5]
+        if np.all(gaps > BAND):
+            assert list(ids[r]) == list(ref["ids"][r]), (tag, r, list(ids[r]),
+                                                        list(ref["ids"][r]))
+        else:
+            banded += 1
+            for j in range(4):
+                assert abs(z[r, d_ids[j]] - zs[j]) <= BAND or z[r, d_ids[j]] == zs[j], (tag, r)
+        for j in range(4):
+            want = z[r, d_ids[j]] - ref["lse"][r]
+            if np.isfinite(want):
+                assert abs(logp[r, j] - want) <= TOL_F, (tag, r, j, logp[r, j], want)
+            else:
+                assert logp[r, j] == -np.inf, (tag, r, j)
+    print(f"[{tag}] draft top-4: {x64.shape[0]} rows, {banded} banded")
+    return ref
+
+
+def _draft_host(out):
+    return (out.topk_id.cpu().numpy(), out.topk_logp.cpu().numpy(), out.row_lse.cpu().numpy(),
+            out.front_tok.cpu().numpy(),
+            None if out.draft_conf is None else out.draft_conf.cpu().numpy())
+
+
+# ----------------------------------------------------------------------------- draft top-4
+
+@pytest.mark.parametrize("B,V,H,mapped", [(1, 1000, 256, False), (3, 1000, 256, True),
+                                          (9, 1000, 256, False), (17, 1000, 256, True),
+                                          (40, 777, 128, False), (2, 4, 64, False)])
+def test_draft_topk(asv, dev, B, V, H, mapped):
+    """Every draft tile family (4, 12 rows: 32-row tile; 36: 64-row; 68: 128-row; 160: two
+    128-row tiles, the last ragged), ragged last vocabulary slabs, the id map, and a vocabulary
+    of exactly four ids."""
+    print(f"case B={B} V={V} H={H} mapped={mapped}", flush=True)
+    W = bf16_weights(V, H, 0.5, 11)
+    x = draft_hidden(B, H, 0, seed=V)
+    vmap = draft_vocab_map(V, 5 * V) if mapped else None
+    trees = asv.alloc_draft_trees(B, dev)
+    out = asv.draft_step(_bf16(x, dev), _bf16(W, dev), trees, 0, shape=(3, 4, 4),
+                         vocab_map=None if vmap is None else _t(vmap, dev))
+    ids, logp, lse, _, _ = _draft_host(out)
+    _check_topk(f"B{B}V{V}", x, oracle.widen_weights(W), vmap, ids, logp, lse)
+
+
+def test_draft_topk_exact_ties_and_nan(asv, dev):
+    """Bit-identical logits (duplicated W rows in different slabs, one in the ragged last slab)
+    come out lowest id first without bands; a row holding a non-number ranks every id as -inf."""
+    V, H, B = 1000, 128, 2
+    W = bf16_weights(V, H, 0.02, 12).copy()
+    half = np.uint16(0x3F00)                         # 0.5
+    for v in (3, 700, 999):
+        W[v] = half
+    x = np.full((4 * B, H), np.uint16(0x3F80))      # 1.0: the tied logits are 64 exactly
+    x[5, 7] = np.uint16(0x7FC0)                      # NaN in row 5
+    trees = asv.alloc_draft_trees(B, dev)
+    out = asv.draft_step(_bf16(x, dev), _bf16(W, dev), trees, 0, shape=(2, 3, 8))
+    ids, logp, lse, _, _ = _draft_host(out)
+    for r in range(4 * B):
+        if r == 5:
+            assert list(ids[r]) == [0, 1, 2, 3]
+            assert np.all(logp[r] == -np.inf) and lse[r] == -np.inf
+            continue
+        assert list(ids[r][:3]) == [3, 700, 999], (r, list(ids[r]))
+        assert logp[r, 0] == logp[r, 1] == logp[r, 2]
+        assert abs(logp[r, 0] - (64.0 - lse[r])) < 1e-5
+
+
+# ----------------------------------------------------------------------------- tree growth
+
+def _oracle_step(trees_ref, ids, logp):
+    """Advance the oracle trees with the GPU's own float32 top-4 of the frontier rows."""
+    out = []
+    for b, t in enumerate(trees_ref):
+        rows = slice(4 * b, 4 * b + len(t.front))
+        out.append(oracle.draft_tree_step(t, ids[rows], logp[rows].astype(np.float32)))
+    return out
+
+
+def _compare_trees(asv, trees, trees_ref, front_tok, grew, tag):
+    got = asv.draft_tree_fields(trees)
+    for b, (g, t) in enumerate(zip(got, trees_ref)):
+        P = len(t.tok)
+        assert (g.nsteps, g.topk, g.ndt) == (t.nsteps, t.topk, t.ndt), (tag, b)
+        assert g.status == 0 and g.steps == t.steps and g.n_pool == P, (tag, b, g.n_pool, P)
+        assert list(g.tok[:P]) == t.tok, (tag, b)
+        assert list(g.par[:P]) == t.par, (tag, b)
+        assert np.array_equal(np.array(g.score[:P], np.float32), np.array(t.score, np.float32))
+        nf = len(t.front)
+        assert g.n_front == nf and list(g.front[:nf]) == t.front, (tag, b)
+        assert np.array_equal(np.array(g.front_score[:nf], np.float32),
+                              np.array(t.front_score, np.float32))
+        # a tree that grew this step reports its new frontier's tokens, any other -1s
+        want_tok = [t.tok[q] for q in t.front] if grew[b] else []
+        exp = (want_tok + [-1] * 4)[:4]
+        assert list(front_tok[b]) == exp, (tag, b, list(front_tok[b]), exp)
+
+
+def _grow_and_prune(asv, dev, B, V, H, shapes=None, shape=None, steps=None, vmap=None,
+                    W=None, hidden=None, tag=""):
+    import torch
+    W = bf16_weights(V, H, 0.5, 13) if W is None else W
+    w64 = oracle.widen_weights(W)
+    trees = asv.alloc_draft_trees(B, dev)
+    state = None if shapes is None else _state_with_shapes(asv, shapes, dev)
+    all_shapes = shapes if shapes is not None else [shape] * B
+    trees_ref = [oracle.draft_tree_init(s) for s in all_shapes]
+    steps = steps or max(int(s[0]) for s in all_shapes) + 1
+    wd = _bf16(W, dev)
+    vm = None if vmap is None else _t(vmap, dev)
+    for s in range(steps):
+        x = draft_hidden(B, H, s, seed=7) if hidden is None else hidden(s)
+        out = asv.draft_step(_bf16(x, dev), wd, trees, s, state=state, shape=shape,
+                             vocab_map=vm, with_conf=True)
+        ids, logp, lse, ftok, conf = _draft_host(out)
+        _check_topk(f"{tag}s{s}", x, w64, vmap, ids, logp, lse)
+        if s == 0:
+            for b in range(B):
+                assert conf[b] == np.exp(np.float32(logp[4 * b, 0])) or \
+                    abs(conf[b] - np.exp(np.float64(logp[4 * b, 0]))) < 1e-6
+        before = [t.steps for t in trees_ref]
+        trees_ref = _oracle_step(trees_ref, ids, logp)
+        grew = [t.steps > n for t, n in zip(trees_ref, before)]
+        _compare_trees(asv, trees, trees_ref, ftok, grew, f"{tag}s{s}")
+    roots = root_tokens(B, 1000)
+    n_cap = sum(t.ndt for t in trees_ref)
+    parent, tok, off, status = asv.draft_prune(trees, n_cap, _t(roots, dev))
+    torch.cuda.synchronize()
+    pruned = [oracle.draft_tree_prune(t, int(r)) for t, r in zip(trees_ref, roots)]
+    par_ref, tok_ref, off_ref = oracle.draft_trees_to_batch(pruned)
+    off = off.cpu().numpy()
+    assert list(off) == list(off_ref), (tag, list(off), list(off_ref))
+    n = int(off[-1])
+    assert list(parent.cpu().numpy()[:n]) == list(par_ref), tag
+    assert list(tok.cpu().numpy()[:n]) == list(tok_ref), tag
+    assert not status.cpu().numpy().any()
+    return trees, trees_ref
+
+
+@pytest.mark.parametrize("B", [1, 6, 20])
+def test_draft_tree_growth_per_request_shapes(asv, dev, B):
+    """Per-request shapes from the policy state (the paper's range), one extra step after the
+    deepest tree is done, then pruning to the verification layout."""
+    print(f"case growth B={B}", flush=True)
+    shapes = draft_shapes(B, seed=B)
+    _grow_and_prune(asv, dev, B, 1000, 256, shapes=shapes, tag=f"grow{B}")
+
+
+def test_draft_tree_growth_uniform_shape_with_map(asv, dev):
+    vmap = draft_vocab_map(1000, 128256)
+    _grow_and_prune(asv, dev, 3, 1000, 256, shape=(4, 4, 12), vmap=vmap, tag="uniform")
+
+
+def test_draft_tree_growth_with_tied_scores(asv, dev):
+    """Every row has three exactly tied best logits and all rows are equal, so candidates tie
+    within and across frontier slots: the earlier candidate wins at every step and in pruning."""
+    V, H, B = 1000, 128, 2
+    W = bf16_weights(V, H, 0.02, 12).copy()
+    for v in (3, 700, 999):
+        W[v] = np.uint16(0x3F00)
+    ones = np.full((4 * B, H), np.uint16(0x3F80))
+    _grow_and_prune(asv, dev, B, V, H, shape=(3, 3, 9), W=W, hidden=lambda s: ones,
+                    tag="ties")
+
+
+def test_draft_bad_shape_and_prune_overflow(asv, dev):
+    """A bad shape in the state leaves that tree root-only with ASV_DS_BAD_SHAPE; pruning into
+    too small an output flags the requests that do not fit and writes none of their rows."""
+    import torch
+    V, H, B = 600, 128, 3
+    W = bf16_weights(V, H, 0.5, 14)
+    shapes = [(3, 4, 4), (2, 5, 4), (3, 2, 6)]       # topk 5 is out of range
+    state = _state_with_shapes(asv, shapes, dev)
+    trees = asv.alloc_draft_trees(B, dev)
+    for s in range(3):
+        out = asv.draft_step(_bf16(draft_hidden(B, H, s, 3), dev), _bf16(W, dev), trees, s,
+                             state=state)
+        ftok = out.front_tok.cpu().numpy()
+        assert list(ftok[1]) == [-1] * 4
+    f = asv.draft_tree_fields(trees)
+    assert f[1].status == asv.DS_BAD_SHAPE and f[1].n_pool == 0
+    parent, tok, off, status = asv.draft_prune(trees, 100)
+    off, status = off.cpu().numpy(), status.cpu().numpy()
+    n0 = 1 + min(3, f[0].n_pool)
+    assert list(off) == [0, n0, n0 + 1, n0 + 1 + 1 + min(5, f[2].n_pool)]
+    assert status[1] == asv.DS_BAD_SHAPE and status[0] == 0 and status[2] == 0
+    assert parent.cpu().numpy()[n0] == -1          # the bad tree's root
+    cap = n0 + 1                                    # the third tree does not fit
+    p2, t2, off2, st2 = asv.draft_prune(trees, cap)
+    torch.cuda.synchronize()
+    assert list(off2.cpu().numpy()) == list(off)
+    st2 = st2.cpu().numpy()
+    assert st2[2] == asv.DS_OVERFLOW and st2[0] == 0 and st2[1] == asv.DS_BAD_SHAPE
+
+
+# ----------------------------------------------------------------------------- tree metadata
+
+def _pack_vis(vis, words):
+    n = vis.shape[0]
+    out = np.zeros((n, words), dtype=np.uint32)
+    for c in range(n):
+        for j in np.nonzero(vis[c])[0]:
+            out[c, j >> 5] |= np.uint32(1) << np.uint32(j & 31)
+    return out
+
+
+def _random_batch(kinds, seed):
+    rng = np.random.default_rng(seed)
+    trees = [build_tree(k, rng, b) for b, k in enumerate(kinds)]
+    off = np.cumsum([0] + [len(t) for t in trees])
+    parent = np.concatenate([[p + off[b] if p >= 0 else -1 for p in t]
+                             for b, t in enumerate(trees)]).astype(np.int32)
+    return parent, off.astype(np.int32)
+
+
+@pytest.mark.parametrize("kinds", [["eagle60"], ["tiny", "level8x8", "adaptive", "tiny"],
+                                   ["chain_or_wide"] * 6])
+def test_tree_meta(asv, dev, kinds):
+    import torch
+    parent, off = _random_batch(kinds, len(kinds))
+    B = len(off) - 1
+    n_max = int(np.diff(off).max())
+    words = (n_max + 31) // 32 + 1                   # one spare word must come out zero
+    base = np.arange(B, dtype=np.int32) * 1000 + 17
+    pos, mask, status = asv.tree_meta(_t(parent, dev), _t(off, dev), _t(base, dev), words)
+    torch.cuda.synchronize()
+    depth, pos_ref, vis = oracle.tree_meta(parent, off, base)
+    assert list(pos.cpu().numpy()) == list(pos_ref)
+    m = mask.cpu().numpy().view(np.uint32)
+    for b in range(B):
+        assert np.array_equal(m[off[b]:off[b + 1]], _pack_vis(vis[b], words)), b
+    assert not status.cpu().numpy().any()
+    pos2, _, _ = asv.tree_meta(_t(parent, dev), _t(off, dev))          # positions only
+    assert list(pos2.cpu().numpy()) == list(depth)
+
+
+def test_tree_meta_large_request_and_status(asv, dev):
+    """A 9000-node request (walked from global memory, past the LDS stage), a mask too narrow
+    for it, a bad parent, a bad root, and malformed offsets."""
+    import torch
+    rng = np.random.default_rng(5)
+    n = 9000
+    big = np.array([-1] + [int(rng.integers(max(0, c - 40), c)) for c in range(1, n)])
+    small = np.array([-1, 0, 0, 1])
+    parent = np.concatenate([big, small + n]).astype(np.int32)
+    parent[n] = -1
+    off = np.array([0, n, n + 4], dtype=np.int32)
+    words = (n + 31) // 32
+    pos, mask, status = asv.tree_meta(_t(parent, dev), _t(off, dev), None, words)
+    torch.cuda.synchronize()
+    depth, _, vis = oracle.tree_meta(parent, off, np.zeros(2, np.int64))
+    assert list(pos.cpu().numpy()) == list(depth)
+    m = mask.cpu().numpy().view(np.uint32)
+    packed = np.packbits(vis[0], axis=1, bitorder="little")
+    packed = np.pad(packed, ((0, 0), (0, 4 * words - packed.shape[1])))
+    assert np.array_equal(m[:n], packed.view(np.uint32)[:, :words])
+    # a mask too small for the big request: positions only, status set
+    _, _, st = asv.tree_meta(_t(parent, dev), _t(off, dev), None, 4)
+    assert list(st.cpu().numpy()) == [asv.RS_MASK_SMALL, 0]
+    bad = parent.copy()
+    bad[n + 3] = n + 3                               # a node that is its own parent
+    _, _, st = asv.tree_meta(_t(bad, dev), _t(off, dev), None, 1)
+    assert list(st.cpu().numpy()) == [asv.RS_MASK_SMALL, asv.RS_BAD_PARENT]
+    bad = parent.copy()
+    bad[n] = 3
+    _, _, st = asv.tree_meta(_t(bad, dev), _t(off, dev), None, 0)
+    assert list(st.cpu().numpy()) == [0, asv.RS_BAD_ROOT]
+    _, _, st = asv.tree_meta(_t(parent, dev), _t(np.array([0, n + 4, n], np.int32), dev))
+    assert list(st.cpu().numpy()) == [asv.RS_BAD_OFFSETS] * 2
+
+
+# ----------------------------------------------------------------------------- commit
+
+def _accepted_paths(parent, off, rng):
+    N, B = len(parent), len(off) - 1
+    path = np.full(N, -1, dtype=np.int32)
+    acc = np.zeros(B, dtype=np.int32)
+    for b in range(B):
+        cur, k = int(off[b]), 0
+        while True:
+            kids = [c for c in range(off[b] + 1, off[b + 1]) if parent[c] == cur]
+            if not kids or rng.random() < 0.25:
+                break
+            cur = kids[int(rng.integers(len(kids)))]
+            path[off[b] + k] = cur
+            k += 1
+        acc[b] = k
+    return path, acc
+
+
+def test_commit(asv, dev):
+    import torch
+    rng = np.random.default_rng(21)
+    parent, off = _random_batch(["tiny", "eagle60", "level8x8", "tiny", "adaptive"], 3)
+    N, B = len(parent), len(off) - 1
+    tok = rng.integers(0, 128256, N).astype(np.int32)
+    path, acc = _accepted_paths(parent, off, rng)
+    bonus = rng.integers(0, 128256, B).astype(np.int32)
+    rows16 = rng.integers(-2**31, 2**31, (N, 8)).astype(np.int32)     # 32-byte rows
+    rows4 = rng.integers(-2**31, 2**31, (N, 3)).astype(np.int32)      # 12-byte rows
+    ref = oracle.commit(path, acc, bonus, tok, off)
+    total = int(ref["off"][-1])
+    for rows in (rows16, rows4, None):
+        c_off, c_tok, c_row, dst, status = asv.commit(
+            _t(off, dev), _t(tok, dev), _t(acc, dev), _t(path, dev), _t(bonus, dev),
+            None if rows is None else _t(rows, dev))
+        torch.cuda.synchronize()
+        assert list(c_off.cpu().numpy()) == list(ref["off"])
+        assert list(c_tok.cpu().numpy()[:total]) == list(ref["tok"])
+        assert list(c_row.cpu().numpy()[:total]) == list(ref["row"])
+        assert not status.cpu().numpy().any()
+        if rows is not None:
+            assert np.array_equal(dst.cpu().numpy()[:total], rows[ref["row"]])
+
+
+def test_commit_bad_path_and_offsets(asv, dev):
+    import torch
+    parent, off = _random_batch(["tiny", "tiny", "tiny"], 4)
+    N, B = len(parent), len(off) - 1
+    rng = np.random.default_rng(8)
+    tok = rng.integers(0, 1000, N).astype(np.int32)
+    path, acc = _accepted_paths(parent, off, rng)
+    acc[0] = int(off[1] - off[0])                     # longer than the request allows
+    path[off[2]] = off[0] + 1                         # a node of another request
+    acc[2] = max(acc[2], 1)
+    bonus = np.array([5, 6, 7], dtype=np.int32)
+    c_off, c_tok, c_row, _, status = asv.commit(_t(off, dev), _t(tok, dev), _t(acc, dev),
+                                                 _t(path, dev), _t(bonus, dev))
+    torch.cuda.synchronize()
+    st = status.cpu().numpy()
+    assert st[0] == asv.RS_BAD_PATH and st[1] == 0 and st[2] == asv.RS_BAD_PATH
+    c_off = c_off.cpu().numpy()
+    assert c_off[1] == 1 and c_off[3] - c_off[2] == 1
+    assert c_tok.cpu().numpy()[0] == 5 and c_row.cpu().numpy()[0] == off[0]
+    assert c_tok.cpu().numpy()[c_off[2]] == 7 and c_row.cpu().numpy()[c_off[2]] == off[2]
+    _, _, _, _, st = asv.commit(_t(np.array([0, 3, 2, N], np.int32), dev), _t(tok, dev),
+                                _t(acc, dev), _t(path, dev), _t(bonus, dev))
+    assert list(st.cpu().numpy()) == [asv.RS_BAD_OFFSETS] * 3

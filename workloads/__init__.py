@@ -20,3 +20,14 @@ from .synth import (  # noqa: F401
     round_to_bf16_bits,
     tree_depths,
 )
+from .draft import (  # noqa: F401
+    DRAFT_CONFIGS,
+    DRAFT_SHAPES,
+    DraftWorkload,
+    draft_hidden,
+    draft_shapes,
+    draft_vocab_map,
+    draft_weights,
+    make_draft_workload,
+    root_tokens,
+)
