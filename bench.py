@@ -1,7 +1,7 @@
 """Throughput of the AdaptiveSpec verification hot path on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 1|3] [--no-cpu] \
-                    [--secondary 3|none] | --reference | --copy-calibration MIB
+                    [--secondary 3|none] [--no-draft] | --reference | --copy-calibration MIB
 
 A step is one asv_verify call (LM-head kernel over every tree row with the per-slab
 reductions and drafted-logit gather, then the fused slab merge + margin rule + tree walk +
@@ -11,7 +11,9 @@ shaped batch-1 verify (H=4096, V=128256, one 60-node EAGLE-style tree, kappa=0.3
 32x64-node batch (2048 rows) is measured after it as the MFMA-bound point. Prints one JSON
 line: verified tree nodes per second, the LM-head kernel's roofline fraction (its duration
 from HIP events recorded around it in every timed step) and the CPU oracle's throughput on a
-bounded sample of the same workload.
+bounded sample of the same workload. The JSON line also carries the draft step that precedes
+verification (``draft``: the draft LM head reduced to each row's top-4, and one tree-growth
+step) on the EAGLE-3-shaped draft head at batch 1 and 32, with its kernel's roofline.
 """
 
 from __future__ import annotations
@@ -35,13 +37,23 @@ TABLES = os.path.join(ROOT, "tests", "golden")
 TRAFFIC = os.path.join(ROOT, "profiles", "k1_traffic.json")
 K1_SOURCES = [os.path.join(ROOT, "paper_2609_02897_amd", "csrc", f)
               for f in ("k_lmhead.h", "k_common.h")]
+K5_SOURCES = [os.path.join(ROOT, "paper_2609_02897_amd", "csrc", f)
+              for f in ("k_draft.h", "k_lmhead.h", "k_common.h")]
+
+
+def _sha(paths) -> str:
+    h = hashlib.sha256()
+    for p in paths:
+        h.update(open(p, "rb").read())
+    return h.hexdigest()[:16]
 
 
 def k1_source_sha() -> str:
-    h = hashlib.sha256()
-    for p in K1_SOURCES:
-        h.update(open(p, "rb").read())
-    return h.hexdigest()[:16]
+    return _sha(K1_SOURCES)
+
+
+def k5_source_sha() -> str:
+    return _sha(K5_SOURCES)
 
 
 class HipEvents:
@@ -147,6 +159,99 @@ def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents):
     return res, w, W
 
 
+def _microbench_lib():
+    lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_02897_amd", "libasv_microbench.so"))
+    lib.asvb_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p,
+                                     ctypes.c_int32, ctypes.c_void_p]
+    return lib
+
+
+def measure_draft(name: str, steps: int, warmup: int, dev, hip: HipEvents, cpu: bool) -> dict:
+    """One draft step (asv_draft_step: the draft LM head with its top-4 epilogue, then the slab
+    merge and one tree-growth step) on the EAGLE-3-shaped draft head (H=4096, 32000 draft ids),
+    trees of the wide end of the paper's range (3,4,4): four draft rows per request.
+
+    Throughput: back-to-back steps. The draft LM head (262 MB) fits the 256 MB last-level cache
+    about whole, which back-to-back launches would read from; in a decode loop the draft
+    model's other weights evict it between steps, so the kernel's roofline uses launches that
+    each follow a clean 1 GiB read, timed with HIP events around the kernel on its stream."""
+    import torch
+    import paper_2609_02897_amd as asv
+    from workloads import make_draft_workload
+    dw = make_draft_workload(name)
+    W, x, vmap = dw.weights(), dw.hidden(0), dw.vocab_map()
+
+    def t(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+
+    wd = t(W.view(np.int16)).view(torch.bfloat16)
+    xd = t(x.view(np.int16)).view(torch.bfloat16)
+    vm = t(vmap)
+    B, R = dw.B, 4 * dw.B
+    shape = (3, 4, 4)
+    trees = asv.alloc_draft_trees(B, dev)
+    ws = torch.empty(max(asv.draft_workspace_bytes(B, dw.H, dw.V), 256), dtype=torch.uint8,
+                     device=dev)
+    out = asv.draft_step(xd, wd, trees, 0, shape=shape, vocab_map=vm, workspace=ws,
+                         with_conf=True)
+
+    def step(i, ev=None):
+        asv.draft_step(xd, wd, trees, i % shape[0], shape=shape, vocab_map=vm, out=out,
+                       workspace=ws, events=ev)
+
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(i)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    # cold launches: a clean read of 1 GiB before each, outside the event window
+    mb = _microbench_lib()
+    flush = torch.ones((1 << 30) // 4, dtype=torch.int32, device=dev)
+    sink = torch.zeros(1 << 16, dtype=torch.int32, device=dev)
+    handle = torch.cuda.current_stream(dev).cuda_stream
+    reps = 50
+    evs = [(hip.create(), hip.create()) for _ in range(reps)]
+    for i in range(reps):
+        assert mb.asvb_stream_read(flush.data_ptr(), 1 << 30, sink.data_ptr(), 1024,
+                                   handle) == 0
+        step(i, evs[i])
+    torch.cuda.synchronize()
+    k_ms = [hip.elapsed_ms(a, b) for a, b in evs]
+    for a, b in evs:
+        hip.destroy(a)
+        hip.destroy(b)
+    del flush
+    k_avg = float(np.mean(k_ms))
+    S = (dw.V + (64 if R <= 64 else 128) - 1) // (64 if R <= 64 else 128)
+    bytes_alg = 2 * dw.V * dw.H + 2 * R * dw.H + R * S * 36
+    flops_alg = 2 * R * dw.V * dw.H
+    res = dict(workload=name, requests=B, rows=R, H=dw.H, V=dw.V, tree_shape=list(shape),
+               us_per_step=round(1e6 * dt / steps, 2),
+               draft_steps_per_s=round(steps / dt, 1),
+               roofline=dict(bound="hbm", kernel="k_draft_partial",
+                             k_avg_us_cold=round(1e3 * k_avg, 2),
+                             achieved=round(bytes_alg / (k_avg * 1e-3) / 1e9, 1),
+                             peak=HBM_PEAK_GBS, unit="GB/s",
+                             frac=round(bytes_alg / (k_avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                             bytes_alg=bytes_alg, flops_alg=flops_alg,
+                             traffic=measured_draft_traffic(name)))
+    if cpu:
+        import oracle
+        w64 = oracle.widen_weights(W)
+        x64 = oracle.widen_bf16(x)
+        n, t0 = 0, time.perf_counter()
+        while n < 3 or time.perf_counter() - t0 < 3.0:
+            oracle.draft_topk(x64, w64, 4, vmap)
+            n += 1
+        res["cpu_oracle_us_per_step"] = round(1e6 * (time.perf_counter() - t0) / n, 1)
+    del wd, xd, ws, out, trees
+    torch.cuda.empty_cache()
+    return res
+
+
 def roofline(r: dict, ceilings: dict = None) -> dict:
     """Roofline of K1 against the published peak; with ``ceilings`` (measured_ceilings) also
     against the peak a microbenchmark reaches on this GPU."""
@@ -177,6 +282,18 @@ def measured_traffic(cfg: int):
         t = json.load(f)
     e = t.get(f"cfg{cfg}")
     if not e or t.get("k1_source_sha") != k1_source_sha():
+        return None
+    return e.get("bytes_per_launch")
+
+
+def measured_draft_traffic(name: str):
+    """The same for the draft LM-head kernel, keyed by draft workload."""
+    if not os.path.exists(TRAFFIC):
+        return None
+    with open(TRAFFIC) as f:
+        t = json.load(f)
+    e = t.get(name)
+    if not e or t.get("k5_source_sha") != k5_source_sha():
         return None
     return e.get("bytes_per_launch")
 
@@ -287,6 +404,8 @@ def main():
     ap.add_argument("--config", type=int, default=1)
     ap.add_argument("--secondary", default="3")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-draft", action="store_true",
+                    help="skip the draft-step measurement (the step before verification)")
     ap.add_argument("--reference", action="store_true",
                     help="only time the vendor references on the bench shapes and exit: "
                          "torch.matmul (hipBLASLt) of the logits alone, and a 1 GiB "
@@ -358,6 +477,14 @@ def main():
         line["secondary"]["roofline"] = roofline(r2, ceilings)
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(w, W)
+    if not args.no_draft:
+        del w, W
+        line["draft"] = [measure_draft(n, args.steps, args.warmup, dev, hip, not args.no_cpu)
+                         for n in ("llama31_8b_draft_b1", "llama31_8b_draft_b32")]
+        for d in line["draft"]:
+            print(f"# draft {d['workload']}: {d['us_per_step']} us/step, K5 cold "
+                  f"{d['roofline']['k_avg_us_cold']} us, {d['roofline']['achieved']} GB/s",
+                  file=sys.stderr, flush=True)
     print(json.dumps(line), flush=True)
 
 
