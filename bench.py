@@ -104,6 +104,17 @@ def to_device(w, W, dev):
                 draft_logits=None if w.draft_logits is None else t(w.draft_logits))
 
 
+def _per_call_us(fn, reps: int) -> float:
+    import torch
+    fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        fn()
+    torch.cuda.synchronize()
+    return 1e6 * (time.perf_counter() - t0) / reps
+
+
 def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents):
     import torch
     import paper_2609_02897_amd as asv
@@ -142,6 +153,18 @@ def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents):
         hip.destroy(b)
     status = out.req_status.cpu().numpy()
     assert np.all(status == 0), status
+    # The steps on either side of the target forward on the same trees: tree-attention metadata
+    # (positions and ancestor masks) and the commit of this step's accepted paths with a gather
+    # of their hidden rows. Both are latency-bound; host-inclusive wall clock per call.
+    words = (int(np.diff(w.req_offsets).max()) + 31) // 32
+    base = torch.zeros(w.B, dtype=torch.int32, device=dev)
+    around = dict(
+        tree_meta_us_per_call=round(_per_call_us(
+            lambda: asv.tree_meta(d["parent"], d["req_offsets"], base, words), steps), 2),
+        commit_us_per_call=round(_per_call_us(
+            lambda: asv.commit(d["req_offsets"], d["draft_tok"], out.accepted_len,
+                               out.accepted_path, out.bonus_token, d["hidden"]), steps), 2),
+        note="host-inclusive wall clock per call; kernel durations in profiles/")
     k1_avg = float(np.mean(k1_ms))
     nodes = w.N * steps
     bytes_alg = 2 * w.V * w.H + 2 * w.N * w.H
@@ -153,7 +176,7 @@ def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents):
                hbm_gbs=bytes_alg / (k1_avg * 1e-3) / 1e9,
                mfma_tflops=flops_alg / (k1_avg * 1e-3) / 1e12,
                bytes_alg=bytes_alg, flops_alg=flops_alg,
-               accepted_len=out.accepted_len.cpu().numpy().tolist()[:4])
+               accepted_len=out.accepted_len.cpu().numpy().tolist()[:4], around=around)
     del d, out, ws
     torch.cuda.empty_cache()
     return res, w, W
@@ -224,6 +247,10 @@ def measure_draft(name: str, steps: int, warmup: int, dev, hip: HipEvents, cpu: 
         hip.destroy(a)
         hip.destroy(b)
     del flush
+    # pruning the grown trees into the verification layout (host-inclusive, per call)
+    for i in range(shape[0]):
+        step(i)
+    prune_us = _per_call_us(lambda: asv.draft_prune(trees, B * shape[2]), steps)
     k_avg = float(np.mean(k_ms))
     S = (dw.V + (64 if R <= 64 else 128) - 1) // (64 if R <= 64 else 128)
     bytes_alg = 2 * dw.V * dw.H + 2 * R * dw.H + R * S * 36
@@ -231,6 +258,7 @@ def measure_draft(name: str, steps: int, warmup: int, dev, hip: HipEvents, cpu: 
     res = dict(workload=name, requests=B, rows=R, H=dw.H, V=dw.V, tree_shape=list(shape),
                us_per_step=round(1e6 * dt / steps, 2),
                draft_steps_per_s=round(steps / dt, 1),
+               prune_us_per_call=round(prune_us, 2),
                roofline=dict(bound="hbm", kernel="k_draft_partial",
                              k_avg_us_cold=round(1e3 * k_avg, 2),
                              achieved=round(bytes_alg / (k_avg * 1e-3) / 1e9, 1),
@@ -454,6 +482,7 @@ def main():
         "config": {"workload": r["name"], "H": r["H"], "V": r["V"], "rows": r["N"],
                    "requests": r["B"], "tau": r["tau"], "parallelism": "single GPU"},
         "roofline": None,
+        "around_target_forward": r["around"],
     }
     if args.secondary != "none" and int(args.secondary) != args.config:
         del w, W
@@ -463,7 +492,8 @@ def main():
               file=sys.stderr, flush=True)
         line["secondary"] = {"workload": r2["name"], "rows": r2["N"], "requests": r2["B"],
                              "value": round(r2["value"], 1), "unit": "nodes/s",
-                             "ms_per_step": round(r2["ms_per_step"], 4)}
+                             "ms_per_step": round(r2["ms_per_step"], 4),
+                             "around_target_forward": r2["around"]}
         w, _ = load_workload(args.config)
         W = w.weights()
     try:

@@ -23,6 +23,7 @@ namespace asv {
 constexpr int kTopK = ASV_TOPK_MAX;   // 4
 constexpr int kPoolMax = ASV_POOL_MAX;
 constexpr int kDraftThreads = kTopK * kWave;
+constexpr int kGrowBatch = 8;         // slab records a lane loads before merging them
 
 __device__ __forceinline__ bool pair_better(float va, int ia, float vb, int ib) {
   return va > vb || (va == vb && ia < ib);
@@ -92,6 +93,41 @@ __device__ __forceinline__ Top4 top4_shfl_xor(const Top4& x, int mask) {
   }
   y.s = __shfl_xor(x.s, mask, kWave);
   return y;
+}
+
+template <int N>
+__device__ __forceinline__ Top4 top4_row_ror(const Top4& x) {
+  Top4 y;
+#pragma unroll
+  for (int k = 0; k < kTopK; ++k) {
+    y.v[k] = row_ror<N>(x.v[k]);
+    y.i[k] = row_ror<N>(x.i[k]);
+  }
+  y.s = row_ror<N>(x.s);
+  return y;
+}
+
+__device__ __forceinline__ Top4 top4_lane(const Top4& x, int l) {
+  Top4 y;
+#pragma unroll
+  for (int k = 0; k < kTopK; ++k) {
+    y.v[k] = lane_value(x.v[k], l);
+    y.i[k] = lane_value(x.i[k], l);
+  }
+  y.s = lane_value(x.s, l);
+  return y;
+}
+
+// Wave-wide merge without LDS round trips: rotations within each 16-lane row (every lane ends
+// with its row's merge; the merged sets are disjoint at each step), then the four rows read as
+// scalars and merged in a fixed order. Every lane returns the same record.
+__device__ __forceinline__ Top4 top4_wave_reduce(Top4 t) {
+  t = top4_merge(t, top4_row_ror<8>(t));
+  t = top4_merge(t, top4_row_ror<4>(t));
+  t = top4_merge(t, top4_row_ror<2>(t));
+  t = top4_merge(t, top4_row_ror<1>(t));
+  return top4_merge(top4_merge(top4_lane(t, 0), top4_lane(t, 16)),
+                    top4_merge(top4_lane(t, 32), top4_lane(t, 48)));
 }
 
 // ------------------------------------------------------------------------------------------ K5
@@ -242,45 +278,7 @@ void k_draft_grow(DraftGrowArgs a) {
   const int slot = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int row = b * kTopK + slot;
 
-  // ---- merge the S slab records of this wave's row (lane l takes slabs l, l + 64, ...)
-  Top4 t = top4_empty();
-  for (int sl = lane; sl < a.S; sl += kWave) {
-    const size_t at = (size_t)row * a.S + sl;
-    const float4 v = *reinterpret_cast<const float4*>(a.rec_v + at * kTopK);
-    const int4 i = *reinterpret_cast<const int4*>(a.rec_i + at * kTopK);
-    Top4 r;
-    r.v[0] = v.x; r.v[1] = v.y; r.v[2] = v.z; r.v[3] = v.w;
-    r.i[0] = i.x; r.i[1] = i.y; r.i[2] = i.z; r.i[3] = i.w;
-    r.s = a.rec_s[at];
-    t = top4_merge(t, r);
-  }
-#pragma unroll
-  for (int mask = 32; mask >= 1; mask >>= 1) t = top4_merge(t, top4_shfl_xor(t, mask));
-  // every lane holds the same four pairs; lane 0's sum is the one used, for determinism
-  const float s0 = lane_value(t.s, 0);
-  const float lse = t.v[0] == kNegInf ? kNegInf : t.v[0] + logf(s0);
-  if (lane < kTopK) {
-    float v = t.v[0];
-    int id = t.i[0];
-#pragma unroll
-    for (int k = 1; k < kTopK; ++k)
-      if (lane == k) {
-        v = t.v[k];
-        id = t.i[k];
-      }
-    float lp = v - lse;
-    lp = lp != lp ? kNegInf : lp;
-    const int tok = a.vocab_map ? a.vocab_map[id] : id;
-    a.topk_id[row * kTopK + lane] = tok;
-    a.topk_logp[row * kTopK + lane] = lp;
-    s_id[slot][lane] = tok;
-    s_lp[slot][lane] = lp;
-  }
-  if (lane == 0) a.row_lse[row] = lse;
-  __syncthreads();
-  if (slot != 0) return;
-
-  // ---- wave 0: one growth step of request b's tree
+  // ---- the tree's header, read first so that its latency overlaps the merge below
   asv_draft_tree* tr = a.tree + b;
   int nsteps, topk, ndt, steps, n_pool, n_front, status;
   int front[kTopK];
@@ -304,7 +302,6 @@ void k_draft_grow(DraftGrowArgs a) {
       front[k] = -1;
       fscore[k] = 0.f;
     }
-    if (a.draft_conf && lane == 0) a.draft_conf[b] = expf(s_lp[0][0]);
   } else {
     nsteps = tr->nsteps;
     topk = tr->topk;
@@ -320,6 +317,57 @@ void k_draft_grow(DraftGrowArgs a) {
       fscore[k] = tr->front_score[k];
     }
   }
+
+  // ---- merge the S slab records of this wave's row: lane l takes slabs l, l + 64, ...,
+  // kGrowBatch at a time, all loads of a batch issued before any merge (addresses clamped into
+  // the row, slots past S masked afterwards), merged as a pairwise tree
+  Top4 t = top4_empty();
+  for (int base = 0; base < a.S; base += kWave * kGrowBatch) {
+    Top4 r[kGrowBatch];
+#pragma unroll
+    for (int q = 0; q < kGrowBatch; ++q) {
+      const int sl = base + q * kWave + lane;
+      const size_t at = (size_t)row * a.S + min(sl, a.S - 1);
+      const float4 v = *reinterpret_cast<const float4*>(a.rec_v + at * kTopK);
+      const int4 i = *reinterpret_cast<const int4*>(a.rec_i + at * kTopK);
+      r[q].v[0] = v.x; r[q].v[1] = v.y; r[q].v[2] = v.z; r[q].v[3] = v.w;
+      r[q].i[0] = i.x; r[q].i[1] = i.y; r[q].i[2] = i.z; r[q].i[3] = i.w;
+      r[q].s = a.rec_s[at];
+    }
+#pragma unroll
+    for (int q = 0; q < kGrowBatch; ++q)
+      if (base + q * kWave + lane >= a.S) r[q] = top4_empty();
+#pragma unroll
+    for (int w = 1; w < kGrowBatch; w *= 2)
+#pragma unroll
+      for (int q = 0; q + w < kGrowBatch; q += 2 * w) r[q] = top4_merge(r[q], r[q + w]);
+    t = top4_merge(t, r[0]);
+  }
+  t = top4_wave_reduce(t);
+  const float lse = t.v[0] == kNegInf ? kNegInf : t.v[0] + logf(t.s);
+  if (lane < kTopK) {
+    float v = t.v[0];
+    int id = t.i[0];
+#pragma unroll
+    for (int k = 1; k < kTopK; ++k)
+      if (lane == k) {
+        v = t.v[k];
+        id = t.i[k];
+      }
+    float lp = v - lse;
+    lp = lp != lp ? kNegInf : lp;
+    const int tok = a.vocab_map ? a.vocab_map[id] : id;
+    a.topk_id[row * kTopK + lane] = tok;
+    a.topk_logp[row * kTopK + lane] = lp;
+    s_id[slot][lane] = tok;
+    s_lp[slot][lane] = lp;
+  }
+  if (lane == 0) a.row_lse[row] = lse;
+  __syncthreads();
+  if (slot != 0) return;
+
+  // ---- wave 0: one growth step of request b's tree
+  if (a.step == 0 && a.draft_conf && lane == 0) a.draft_conf[b] = expf(s_lp[0][0]);
   // the header bounds are checked again so that a tree that was never initialised (step > 0
   // first) cannot send a write outside its pool
   const bool grow = status == 0 && steps >= 0 && steps < nsteps && n_front >= 1 &&

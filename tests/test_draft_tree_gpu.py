@@ -406,3 +406,18 @@ def test_commit_bad_path_and_offsets(asv, dev):
     _, _, _, _, st = asv.commit(_t(np.array([0, 3, 2, N], np.int32), dev), _t(tok, dev),
                                 _t(acc, dev), _t(path, dev), _t(bonus, dev))
     assert list(st.cpu().numpy()) == [asv.RS_BAD_OFFSETS] * 3
+
+
+# ----------------------------------------------------------------------------- full size
+
+@pytest.mark.parametrize("name", ["llama31_8b_draft_b1", "llama31_8b_draft_b32"])
+def test_draft_full_size(asv, dev, name):
+    """The bench workloads (H=4096, 32000 draft ids mapped into the 128256-id target vocabulary,
+    trees (3,4,4)) in bench.py's launch configuration: every row's top-4 against the oracle, then
+    three growth steps and pruning bit-exact against the oracle fed with the GPU's values."""
+    from workloads import make_draft_workload
+    dw = make_draft_workload(name)
+    print(f"case {name}", flush=True)
+    W = dw.weights()
+    _grow_and_prune(asv, dev, dw.B, dw.V, dw.H, shape=(3, 4, 4), vmap=dw.vocab_map(), W=W,
+                    hidden=lambda s: dw.hidden(s), tag=name)
