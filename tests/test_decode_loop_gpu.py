@@ -1,0 +1,150 @@
+"""The device-side decoding loop end to end, through the C ABI, against the CPU oracle.
+
+Three decoding steps for a batch of four requests:
+  draft steps (asv_draft_step; each tree takes its shape from the policy state) -> the fresh
+  p_draft(top1) enters the state (asv_tree_policy) -> pruning (asv_draft_prune) -> tree metadata
+  (asv_tree_meta) -> the target LM head and margin rule (asv_verify, which updates RAR, the
+  history and the next shape) -> commit (asv_commit; the bonus becomes the next root).
+Every stage is compared with the oracle on the GPU's own inputs to that stage: floats within
+2e-3, integer decisions bit-exact (float32 tree decisions taken on the GPU's float32 values;
+verification outside its 1e-3 bands).
+"""
+
+from types import SimpleNamespace
+
+import numpy as np
+import pytest
+
+import oracle
+from harness import compare, compare_state, to_host
+from workloads import bf16_normal, bf16_weights, draft_hidden, draft_vocab_map, root_tokens
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module")
+def asv():
+    import paper_2609_02897_amd as m
+    m.load()
+    return m
+
+
+def _t(x, dev):
+    import torch
+    return torch.from_numpy(np.array(x, copy=True, order="C")).to(dev)
+
+
+def _bf16(bits, dev):
+    import torch
+    return _t(np.asarray(bits, dtype=np.uint16).view(np.int16), dev).view(torch.bfloat16)
+
+
+def test_decode_loop(asv, dev):
+    import torch
+    B, H, Vd, Vt = 4, 256, 1000, 3000
+    # kappa 0 accepts every drafted node (full-depth commits); 1 is strict token match
+    tau = np.array([0.0, 0.05, 0.3, 1.0], dtype=np.float32)
+    Wd, Wt = bf16_weights(Vd, H, 0.5, 21), bf16_weights(Vt, H, 0.5, 22)
+    wd64, wt64 = oracle.widen_weights(Wd), oracle.widen_weights(Wt)
+    vmap = draft_vocab_map(Vd, Vt)
+    params = asv.make_params()
+    p_ref = oracle.Params()
+    state = asv.state_init(B, params, dev)
+    st_ref = [oracle.state_init(p_ref) for _ in range(B)]
+    trees = asv.alloc_draft_trees(B, dev)
+    wdd, wtd, vmd = _bf16(Wd, dev), _bf16(Wt, dev), _t(vmap, dev)
+    roots = root_tokens(B, Vt)
+    committed = np.zeros(B, dtype=np.int32)                 # tokens committed so far
+    for step in range(3):
+        print(f"decode step {step}", flush=True)
+        # ---- draft: shapes come from the state the previous verify wrote
+        shapes = [tuple(s.shape) for s in asv.state_fields(state)]
+        assert shapes == [tuple(s.shape) for s in st_ref], (step, shapes)
+        trees_ref = [oracle.draft_tree_init(sh) for sh in shapes]
+        conf = None
+        for s in range(max(sh[0] for sh in shapes)):
+            x = draft_hidden(B, H, s, seed=100 + step)
+            out = asv.draft_step(_bf16(x, dev), wdd, trees, s, state=state, vocab_map=vmd,
+                                 with_conf=(s == 0))
+            ids, logp = out.topk_id.cpu().numpy(), out.topk_logp.cpu().numpy()
+            if s == 0:
+                conf = out.draft_conf.cpu().numpy()
+                ref0 = oracle.draft_topk(oracle.widen_bf16(x), wd64, 4, vmap)
+                for b in range(B):
+                    assert abs(conf[b] - np.exp(ref0["logp"][4 * b, 0])) < 2e-3 * max(
+                        conf[b], 1e-3), (step, b)
+            trees_ref = [oracle.draft_tree_step(t, ids[4 * b:4 * b + len(t.front)],
+                                                logp[4 * b:4 * b + len(t.front)])
+                         for b, t in enumerate(trees_ref)]
+        # the step's fresh draft confidence enters the policy state (Eq. (2) at step t)
+        asv.tree_policy(state, _t(conf, dev), params)
+        for b in range(B):
+            st_ref[b].draft_conf = float(conf[b])
+        # ---- prune to the verification layout
+        n_cap = sum(sh[2] for sh in shapes)
+        parent, tok, off, pst = asv.draft_prune(trees, n_cap, _t(roots, dev))
+        pruned = [oracle.draft_tree_prune(t, int(r)) for t, r in zip(trees_ref, roots)]
+        par_ref, tok_ref, off_ref = oracle.draft_trees_to_batch(pruned)
+        off_h = off.cpu().numpy()
+        N = int(off_h[-1])
+        assert list(off_h) == list(off_ref) and not pst.cpu().numpy().any()
+        assert list(parent.cpu().numpy()[:N]) == list(par_ref)
+        assert list(tok.cpu().numpy()[:N]) == list(tok_ref)
+        parent_d, tok_d = parent[:N].contiguous(), tok[:N].contiguous()
+        # ---- tree metadata for the target forward
+        words = (int(np.diff(off_h).max()) + 31) // 32
+        pos, mask, mst = asv.tree_meta(parent_d, off, _t(committed, dev), words)
+        torch.cuda.synchronize()
+        depth, pos_ref, vis = oracle.tree_meta(par_ref, off_ref, committed)
+        assert list(pos.cpu().numpy()) == list(pos_ref) and not mst.cpu().numpy().any()
+        m = mask.cpu().numpy().view(np.uint32)
+        for b in range(B):
+            lo, hi = int(off_h[b]), int(off_h[b + 1])
+            for c in range(hi - lo):
+                bits = sum(1 << j for j in np.nonzero(vis[b][c])[0])
+                got = sum(int(m[lo + c, w]) << (32 * w) for w in range(words))
+                assert got == bits, (step, b, c)
+        # ---- target forward stand-in: seeded final hidden states of the N tree rows
+        hid = bf16_normal(np.random.default_rng([7, step, N]), (N, H), 1.0)
+        vout = asv.verify(_bf16(hid, dev), wtd, tok_d, parent_d, off, _t(tau, dev),
+                          state=state, params=params)
+        torch.cuda.synchronize()
+        got = to_host(vout)
+        ref = oracle.verify(wt64, hid, tok_ref, par_ref, off_ref, tau, None, st_ref, p_ref)
+        w = SimpleNamespace(N=N, B=B, parent=par_ref, draft_tok=tok_ref, req_offsets=off_ref)
+        rep = compare(w, ref, got)
+        print(f"  N={N} accepted={list(got['accepted_len'])} banded requests "
+              f"{rep.banded_requests}")
+        banded = {b for b in range(B) if int(ref["band_at"][b]) >= 0}
+        # the oracle's history follows the GPU's accepted lengths (equal outside the bands)
+        for b in range(B):
+            lo, hi = int(off_ref[b]), int(off_ref[b + 1])
+            st_ref[b] = oracle.state_update(st_ref[b], int(got["accepted_len"][b]), hi - lo,
+                                            None, p_ref)
+        compare_state(asv.state_fields(state), st_ref, params=p_ref)
+        # ---- commit
+        c_off, c_tok, c_row, dst, cst = asv.commit(off, tok_d, vout.accepted_len,
+                                                   vout.accepted_path, vout.bonus_token,
+                                                   _bf16(hid, dev))
+        torch.cuda.synchronize()
+        cref = oracle.commit(got["accepted_path"], got["accepted_len"], got["bonus_token"],
+                             tok_ref, off_ref)
+        total = int(cref["off"][-1])
+        assert list(c_off.cpu().numpy()) == list(cref["off"]) and not cst.cpu().numpy().any()
+        assert list(c_tok.cpu().numpy()[:total]) == list(cref["tok"])
+        assert list(c_row.cpu().numpy()[:total]) == list(cref["row"])
+        kept = dst.view(torch.int16).cpu().numpy().view(np.uint16)[:total]
+        assert np.array_equal(kept, hid[cref["row"]])
+        # the next step: the bonus is the new root; positions advance by what was committed
+        roots = got["bonus_token"].astype(np.int32)
+        committed = committed + np.diff(cref["off"]).astype(np.int32)
+        assert not banded or rep.banded_requests == len(banded)
+        assert got["accepted_len"][0] >= 1                  # kappa 0 walks to a leaf
