@@ -65,6 +65,7 @@ class HipEvents:
         self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float),
                                                  ctypes.c_void_p, ctypes.c_void_p]
         self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
 
     def create(self) -> int:
         ev = ctypes.c_void_p()
@@ -78,6 +79,9 @@ class HipEvents:
 
     def destroy(self, ev: int):
         self.hip.hipEventDestroy(ev)
+
+    def record(self, ev: int, stream: int):
+        assert self.hip.hipEventRecord(ctypes.c_void_p(ev), ctypes.c_void_p(stream)) == 0
 
 
 def load_workload(cfg: int, step: int = 0):
@@ -243,6 +247,25 @@ def measure_draft(name: str, steps: int, warmup: int, dev, hip: HipEvents, cpu: 
         step(i, evs[i])
     torch.cuda.synchronize()
     k_ms = [hip.elapsed_ms(a, b) for a, b in evs]
+    # the achievable ceiling for this launch: a plain streaming read of the same number of
+    # bytes after the same flush, best of two grid sizes
+    n_rd = (2 * dw.V * dw.H) // 16 * 16
+    rd = torch.ones(n_rd // 4, dtype=torch.int32, device=dev)
+    rd_ms = []
+    for grid in (1024, 2048):
+        t_ms = []
+        for i in range(20):
+            assert mb.asvb_stream_read(flush.data_ptr(), 1 << 30, sink.data_ptr(), 1024,
+                                       handle) == 0
+            a, b = evs[i]
+            hip.record(a, handle)
+            assert mb.asvb_stream_read(rd.data_ptr(), n_rd, sink.data_ptr(), grid, handle) == 0
+            hip.record(b, handle)
+            torch.cuda.synchronize()
+            t_ms.append(hip.elapsed_ms(a, b))
+        rd_ms.append(float(np.mean(t_ms)))
+    read_gbs = n_rd / (min(rd_ms) * 1e-3) / 1e9
+    del rd
     for a, b in evs:
         hip.destroy(a)
         hip.destroy(b)
@@ -264,6 +287,9 @@ def measure_draft(name: str, steps: int, warmup: int, dev, hip: HipEvents, cpu: 
                              achieved=round(bytes_alg / (k_avg * 1e-3) / 1e9, 1),
                              peak=HBM_PEAK_GBS, unit="GB/s",
                              frac=round(bytes_alg / (k_avg * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                             measured_peak=round(read_gbs, 1),
+                             frac_of_measured=round(bytes_alg / (k_avg * 1e-3) / 1e9 / read_gbs,
+                                                    4),
                              bytes_alg=bytes_alg, flops_alg=flops_alg,
                              traffic=measured_draft_traffic(name)))
     if cpu:

@@ -152,7 +152,7 @@ int draft_slab(DraftTile t) { return t == DraftTile::kRows128 ? 128 : 64; }
 
 struct DraftLayout {
   int S = 0;  // vocabulary slabs of the chosen tile
-  size_t off_v = 0, off_i = 0, off_s = 0, bytes = 0;
+  size_t off_k = 0, off_s = 0, bytes = 0;
 };
 
 DraftLayout draft_layout(int B, int V) {
@@ -161,8 +161,7 @@ DraftLayout draft_layout(int B, int V) {
   L.S = (V + draft_slab(pick_draft_tile(R)) - 1) / draft_slab(pick_draft_tile(R));
   const size_t rec = (size_t)R * L.S;
   size_t at = 0;
-  L.off_v = at; at += align_up(rec * kTopK * 4);
-  L.off_i = at; at += align_up(rec * kTopK * 4);
+  L.off_k = at; at += align_up(rec * kTopK * 8);
   L.off_s = at; at += align_up(rec * 4);
   L.bytes = at;
   return L;
@@ -181,8 +180,8 @@ void launch_draft(const asv_draft_args* a, const DraftLayout& L, char* ws, hipSt
   const int R = a->B * kTopK;
   const int RT = (R + TR - 1) / TR;
   k_draft_partial<TV, TR, WV, WR, BK, NST, PF><<<L.S * RT, WV * WR * kWave, 0, s>>>(
-      a->hidden, a->w_draft, R, a->H, a->V, L.S, RT, reinterpret_cast<float*>(ws + L.off_v),
-      reinterpret_cast<int32_t*>(ws + L.off_i), reinterpret_cast<float*>(ws + L.off_s));
+      a->hidden, a->w_draft, R, a->H, a->V, L.S, RT, reinterpret_cast<uint64_t*>(ws + L.off_k),
+      reinterpret_cast<float*>(ws + L.off_s));
 }
 
 int record_event(void* ev, hipStream_t s, const char* what) {
@@ -352,8 +351,7 @@ extern "C" int asv_draft_step(const asv_draft_args* a, void* workspace, uint64_t
   g.B = a->B;
   g.S = L.S;
   g.step = a->step;
-  g.rec_v = reinterpret_cast<const float*>(ws + L.off_v);
-  g.rec_i = reinterpret_cast<const int32_t*>(ws + L.off_i);
+  g.rec_k = reinterpret_cast<const uint64_t*>(ws + L.off_k);
   g.rec_s = reinterpret_cast<const float*>(ws + L.off_s);
   g.vocab_map = a->vocab_map;
   g.state = a->state;

@@ -25,16 +25,6 @@ namespace asv {
 
 static_assert(ASV_HIST_WINDOW == 16, "the ring arithmetic below assumes 16 slots");
 
-// LDS writes of every lane of this wave are visible to its later LDS reads: the LDS executes a
-// wave's instructions in order, so a compiler fence plus the drain of this wave's LDS queue
-// suffice (no workgroup barrier, which would need every wave of the workgroup).
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
 __device__ __forceinline__ bool wave_any(bool x) { return __ballot(x) != 0; }
 
 // ---- per-row merge of the slab records (the first half of the finishing step)

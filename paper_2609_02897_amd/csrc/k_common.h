@@ -116,6 +116,16 @@ __device__ __forceinline__ int32_t ld_device(const int32_t* p) {
   return __hip_atomic_load(const_cast<int32_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// LDS writes of every lane of this wave are visible to its later LDS reads: the LDS executes a
+// wave's instructions in order, so a compiler fence plus the drain of this wave's LDS queue
+// suffice (no workgroup barrier, which would need every wave of the workgroup).
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Wait until every global store this wave issued has completed (vmcnt(0)).
 __device__ __forceinline__ void wait_stores() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 

@@ -3,8 +3,9 @@
 // verification budget.
 //
 // K5 k_draft_partial: the LM-head tile of K1 (same staging, MFMA and accumulator layout) with a
-//   top-4 epilogue: per (draft row, 256-entry vocabulary slab) it writes the slab's four best
-//   (logit, id) pairs, best first, and the sum of exp(z - best). The logits never reach memory.
+//   top-4 epilogue: per (draft row, vocabulary slab) it writes the slab's four best (logit, id)
+//   pairs, best first, as 64-bit order keys, and the sum of exp(z - best). The logits never
+//   reach memory.
 // K6 k_draft_grow: one workgroup per request, one wave per draft row (4 rows per request):
 //   merge the slab records of the row, then wave 0 applies the growth step to the request's tree.
 // K7 k_draft_prune: one workgroup per request: rank the pool, keep the best ndt - 1 nodes in
@@ -29,25 +30,6 @@ __device__ __forceinline__ bool pair_better(float va, int ia, float vb, int ib) 
   return va > vb || (va == vb && ia < ib);
 }
 
-// Four (logit, id) pairs in the pair order, plus the sum of exp(z - v[0]) over the set they
-// were taken from (0 for an empty set).
-struct Top4 {
-  float v[kTopK];
-  int i[kTopK];
-  float s;
-};
-
-__device__ __forceinline__ Top4 top4_empty() {
-  Top4 t;
-#pragma unroll
-  for (int k = 0; k < kTopK; ++k) {
-    t.v[k] = kNegInf;
-    t.i[k] = kNoIndex;
-  }
-  t.s = 0.f;
-  return t;
-}
-
 // Slot a keeps the better pair.
 __device__ __forceinline__ void pair_order(float& va, int& ia, float& vb, int& ib) {
   const bool sw = pair_better(vb, ib, va, ia);
@@ -59,50 +41,94 @@ __device__ __forceinline__ void pair_order(float& va, int& ia, float& vb, int& i
   ia = ti;
 }
 
-// The four best pairs of two sorted lists with disjoint ids: the better of a[k] and b[3-k] for
-// every k is a bitonic sequence holding them, which two compare-exchange stages sort. The sums
+// A (logit, id) pair as one 64-bit key whose unsigned order is the pair order: the high word is
+// the logit's bits mapped to an order-preserving unsigned integer, the low word the complement
+// of the id (a lower id gives a larger key). Logits are never a non-number here; -0 is folded
+// into +0 first, so that equal logits compare equal as floats do. Key 0 lies below every pair.
+__device__ __forceinline__ uint64_t pair_key(float v, int id) {
+  const uint32_t u = __float_as_uint(v + 0.f);
+  const uint32_t o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return ((uint64_t)o << 32) | (uint32_t)~id;
+}
+__device__ __forceinline__ float key_value(uint64_t k) {
+  const uint32_t o = (uint32_t)(k >> 32);
+  return __uint_as_float((o & 0x80000000u) ? (o & 0x7fffffffu) : ~o);
+}
+__device__ __forceinline__ int key_id(uint64_t k) { return (int)~(uint32_t)k; }
+
+// Four pairs as keys in descending order, the best logit m (the value of k[0]) and the sum of
+// exp(z - m) over the set they were taken from (an empty set: keys 0, m = -inf, s = 0).
+struct Top4 {
+  uint64_t k[kTopK];
+  float m;
+  float s;
+};
+
+__device__ __forceinline__ Top4 top4_empty() {
+  Top4 t;
+#pragma unroll
+  for (int q = 0; q < kTopK; ++q) t.k[q] = 0;
+  t.m = kNegInf;
+  t.s = 0.f;
+  return t;
+}
+
+__device__ __forceinline__ void key_order(uint64_t& a, uint64_t& b) {
+  const uint64_t hi = a > b ? a : b, lo = a > b ? b : a;
+  a = hi;
+  b = lo;
+}
+
+// The four best pairs of two sorted lists with disjoint ids: the larger of a[q] and b[3-q] for
+// every q is a bitonic sequence holding them, which two compare-exchange stages sort. The sums
 // merge like online-softmax records.
 __device__ __forceinline__ Top4 top4_merge(const Top4& a, const Top4& b) {
   Top4 c;
 #pragma unroll
-  for (int k = 0; k < kTopK; ++k) {
-    const bool ta = pair_better(a.v[k], a.i[k], b.v[3 - k], b.i[3 - k]);
-    c.v[k] = ta ? a.v[k] : b.v[3 - k];
-    c.i[k] = ta ? a.i[k] : b.i[3 - k];
-  }
-  pair_order(c.v[0], c.i[0], c.v[2], c.i[2]);
-  pair_order(c.v[1], c.i[1], c.v[3], c.i[3]);
-  pair_order(c.v[0], c.i[0], c.v[1], c.i[1]);
-  pair_order(c.v[2], c.i[2], c.v[3], c.i[3]);
-  const Rec r = rec_merge(Rec{a.v[0], a.s, 0}, Rec{b.v[0], b.s, 0});
+  for (int q = 0; q < kTopK; ++q) c.k[q] = a.k[q] > b.k[3 - q] ? a.k[q] : b.k[3 - q];
+  key_order(c.k[0], c.k[2]);
+  key_order(c.k[1], c.k[3]);
+  key_order(c.k[0], c.k[1]);
+  key_order(c.k[2], c.k[3]);
+  const Rec r = rec_merge(Rec{a.m, a.s, 0}, Rec{b.m, b.s, 0});
+  c.m = r.m;
   c.s = r.s;
-  // Opaque to the optimiser: chains of these merges (a slab loop followed by a butterfly) are
-  // otherwise folded into select trees that grow exponentially with the chain length and
-  // stall the compiler. The empty asm costs no instruction.
+  // Opaque to the optimiser: chains of these merges (a slab loop followed by a wave
+  // reduction) are otherwise folded into select trees that grow exponentially with the chain
+  // length and stall the compiler. The empty asm costs no instruction.
 #pragma unroll
-  for (int k = 0; k < kTopK; ++k) asm volatile("" : "+v"(c.v[k]), "+v"(c.i[k]));
+  for (int q = 0; q < kTopK; ++q) asm volatile("" : "+v"(c.k[q]));
   return c;
+}
+
+__device__ __forceinline__ uint64_t shfl_xor64(uint64_t x, int mask) {
+  const uint32_t lo = __shfl_xor((uint32_t)x, mask, kWave);
+  const uint32_t hi = __shfl_xor((uint32_t)(x >> 32), mask, kWave);
+  return ((uint64_t)hi << 32) | lo;
 }
 
 __device__ __forceinline__ Top4 top4_shfl_xor(const Top4& x, int mask) {
   Top4 y;
 #pragma unroll
-  for (int k = 0; k < kTopK; ++k) {
-    y.v[k] = __shfl_xor(x.v[k], mask, kWave);
-    y.i[k] = __shfl_xor(x.i[k], mask, kWave);
-  }
+  for (int q = 0; q < kTopK; ++q) y.k[q] = shfl_xor64(x.k[q], mask);
+  y.m = __shfl_xor(x.m, mask, kWave);
   y.s = __shfl_xor(x.s, mask, kWave);
   return y;
+}
+
+template <int N>
+__device__ __forceinline__ uint64_t row_ror64(uint64_t x) {
+  const uint32_t lo = (uint32_t)row_ror<N>((int)(uint32_t)x);
+  const uint32_t hi = (uint32_t)row_ror<N>((int)(uint32_t)(x >> 32));
+  return ((uint64_t)hi << 32) | lo;
 }
 
 template <int N>
 __device__ __forceinline__ Top4 top4_row_ror(const Top4& x) {
   Top4 y;
 #pragma unroll
-  for (int k = 0; k < kTopK; ++k) {
-    y.v[k] = row_ror<N>(x.v[k]);
-    y.i[k] = row_ror<N>(x.i[k]);
-  }
+  for (int q = 0; q < kTopK; ++q) y.k[q] = row_ror64<N>(x.k[q]);
+  y.m = row_ror<N>(x.m);
   y.s = row_ror<N>(x.s);
   return y;
 }
@@ -110,10 +136,12 @@ __device__ __forceinline__ Top4 top4_row_ror(const Top4& x) {
 __device__ __forceinline__ Top4 top4_lane(const Top4& x, int l) {
   Top4 y;
 #pragma unroll
-  for (int k = 0; k < kTopK; ++k) {
-    y.v[k] = lane_value(x.v[k], l);
-    y.i[k] = lane_value(x.i[k], l);
+  for (int q = 0; q < kTopK; ++q) {
+    const uint32_t lo = (uint32_t)lane_value((int)(uint32_t)x.k[q], l);
+    const uint32_t hi = (uint32_t)lane_value((int)(uint32_t)(x.k[q] >> 32), l);
+    y.k[q] = ((uint64_t)hi << 32) | lo;
   }
+  y.m = lane_value(x.m, l);
   y.s = lane_value(x.s, l);
   return y;
 }
@@ -135,8 +163,8 @@ __device__ __forceinline__ Top4 top4_wave_reduce(Top4 t) {
 template <int TV, int TR, int WV, int WR, int BK, int NST, int PF = 0>
 __global__ __launch_bounds__(WV * WR * kWave, 1)
 void k_draft_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int R,
-                     int H, int V, int S, int RT, float* __restrict__ rec_v,
-                     int32_t* __restrict__ rec_i, float* __restrict__ rec_s) {
+                     int H, int V, int S, int RT, uint64_t* __restrict__ rec_k,
+                     float* __restrict__ rec_s) {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
   constexpr int T = C::kThreads;
   __shared__ uint4 smem[(C::kLds + lmhead_sink_bytes<TV, TR, WV, WR, PF>()) / 16];
@@ -168,44 +196,49 @@ void k_draft_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict_
       if constexpr (MASK) z = entry_v(k) < V ? z : kNegInf;
       return z;
     };
-    Top4 t;
+    float v[kTopK];
+    int id[kTopK];
 #pragma unroll
     for (int k = 0; k < kTopK; ++k) {
-      t.v[k] = entry(k);
-      t.i[k] = entry_v(k);
+      v[k] = entry(k);
+      id[k] = entry_v(k);
     }
-    pair_order(t.v[0], t.i[0], t.v[1], t.i[1]);
-    pair_order(t.v[2], t.i[2], t.v[3], t.i[3]);
-    pair_order(t.v[0], t.i[0], t.v[2], t.i[2]);
-    pair_order(t.v[1], t.i[1], t.v[3], t.i[3]);
-    pair_order(t.v[1], t.i[1], t.v[2], t.i[2]);
+    pair_order(v[0], id[0], v[1], id[1]);
+    pair_order(v[2], id[2], v[3], id[3]);
+    pair_order(v[0], id[0], v[2], id[2]);
+    pair_order(v[1], id[1], v[3], id[3]);
+    pair_order(v[1], id[1], v[2], id[2]);
 #pragma unroll
     for (int k = kTopK; k < C::MV * 16; ++k) {
       const float z = entry(k);
-      const int id = entry_v(k);
-      const bool b0 = z > t.v[0], b1 = z > t.v[1], b2 = z > t.v[2], b3 = z > t.v[3];
-      t.v[3] = b2 ? t.v[2] : (b3 ? z : t.v[3]);
-      t.i[3] = b2 ? t.i[2] : (b3 ? id : t.i[3]);
-      t.v[2] = b1 ? t.v[1] : (b2 ? z : t.v[2]);
-      t.i[2] = b1 ? t.i[1] : (b2 ? id : t.i[2]);
-      t.v[1] = b0 ? t.v[0] : (b1 ? z : t.v[1]);
-      t.i[1] = b0 ? t.i[0] : (b1 ? id : t.i[1]);
-      t.v[0] = b0 ? z : t.v[0];
-      t.i[0] = b0 ? id : t.i[0];
+      const int e = entry_v(k);
+      const bool b0 = z > v[0], b1 = z > v[1], b2 = z > v[2], b3 = z > v[3];
+      v[3] = b2 ? v[2] : (b3 ? z : v[3]);
+      id[3] = b2 ? id[2] : (b3 ? e : id[3]);
+      v[2] = b1 ? v[1] : (b2 ? z : v[2]);
+      id[2] = b1 ? id[1] : (b2 ? e : id[2]);
+      v[1] = b0 ? v[0] : (b1 ? z : v[1]);
+      id[1] = b0 ? id[0] : (b1 ? e : id[1]);
+      v[0] = b0 ? z : v[0];
+      id[0] = b0 ? e : id[0];
     }
-    const float mb = t.v[0] * kLog2e;
+    const float mb = v[0] * kLog2e;
     float sum = 0.f;
 #pragma unroll
     for (int k = 0; k < C::MV * 16; ++k) sum += exp2_rel(fmaf(entry(k), kLog2e, -mb));
-    t.s = t.v[0] == kNegInf ? 0.f : sum;
+    Top4 t;
+#pragma unroll
+    for (int k = 0; k < kTopK; ++k) t.k[k] = pair_key(v[k], id[k]);
+    t.m = v[0];
+    t.s = v[0] == kNegInf ? 0.f : sum;
     return t;
   };
 
-  // Per-row exchange area in the (now idle) LDS ring: WV records of 9 words per tree row.
-  float* const x_v = reinterpret_cast<float*>(smem);
-  int* const x_i = reinterpret_cast<int*>(x_v + WV * TR * kTopK);
-  float* const x_s = reinterpret_cast<float*>(x_i + WV * TR * kTopK);
-  static_assert(WV * TR * (2 * kTopK + 1) * 4 <= C::kLds, "exchange area exceeds the ring");
+  // Per-row exchange area in the (now idle) LDS ring: WV records of four keys and a sum per
+  // tree row.
+  uint64_t* const x_k = reinterpret_cast<uint64_t*>(smem);
+  float* const x_s = reinterpret_cast<float*>(x_k + WV * TR * kTopK);
+  static_assert(WV * TR * (8 * kTopK + 4) <= C::kLds, "exchange area exceeds the ring");
 #pragma unroll
   for (int j = 0; j < C::MR; ++j) {
     if (r0 + wr * C::kWaveR + 32 * j >= R) continue;        // row block past the last row
@@ -214,10 +247,7 @@ void k_draft_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict_
     if (lane < 32) {
       const int at = wv * TR + wr * C::kWaveR + 32 * j + lane;
 #pragma unroll
-      for (int k = 0; k < kTopK; ++k) {
-        x_v[at * kTopK + k] = t.v[k];
-        x_i[at * kTopK + k] = t.i[k];
-      }
+      for (int k = 0; k < kTopK; ++k) x_k[at * kTopK + k] = t.k[k];
       x_s[at] = t.s;
     }
     __builtin_amdgcn_sched_barrier(0);
@@ -230,10 +260,8 @@ void k_draft_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict_
       Top4 t;
       const int at = w * TR + row;
 #pragma unroll
-      for (int k = 0; k < kTopK; ++k) {
-        t.v[k] = x_v[at * kTopK + k];
-        t.i[k] = x_i[at * kTopK + k];
-      }
+      for (int k = 0; k < kTopK; ++k) t.k[k] = x_k[at * kTopK + k];
+      t.m = key_value(t.k[0]);
       t.s = x_s[at];
       return t;
     };
@@ -241,8 +269,11 @@ void k_draft_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict_
 #pragma unroll
     for (int w = 1; w < WV; ++w) t = top4_merge(t, load(w));
     const size_t at = (size_t)n * S + slab;
-    *reinterpret_cast<float4*>(rec_v + at * kTopK) = make_float4(t.v[0], t.v[1], t.v[2], t.v[3]);
-    *reinterpret_cast<int4*>(rec_i + at * kTopK) = make_int4(t.i[0], t.i[1], t.i[2], t.i[3]);
+    uint4* const dst = reinterpret_cast<uint4*>(rec_k + at * kTopK);
+    dst[0] = make_uint4((uint32_t)t.k[0], (uint32_t)(t.k[0] >> 32), (uint32_t)t.k[1],
+                        (uint32_t)(t.k[1] >> 32));
+    dst[1] = make_uint4((uint32_t)t.k[2], (uint32_t)(t.k[2] >> 32), (uint32_t)t.k[3],
+                        (uint32_t)(t.k[3] >> 32));
     rec_s[at] = t.s;
   }
 }
@@ -251,8 +282,7 @@ void k_draft_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict_
 
 struct DraftGrowArgs {
   int B, S, step;
-  const float* rec_v;
-  const int32_t* rec_i;
+  const uint64_t* rec_k;
   const float* rec_s;
   const int32_t* vocab_map;
   const asv_req_state* state;
@@ -274,6 +304,8 @@ __global__ __launch_bounds__(kDraftThreads)
 void k_draft_grow(DraftGrowArgs a) {
   __shared__ int s_id[kTopK][kTopK];
   __shared__ float s_lp[kTopK][kTopK];
+  __shared__ float s_sc[kTopK * kTopK];
+  __shared__ int s_ft[kTopK];
   const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
   const int slot = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int row = b * kTopK + slot;
@@ -328,10 +360,13 @@ void k_draft_grow(DraftGrowArgs a) {
     for (int q = 0; q < kGrowBatch; ++q) {
       const int sl = base + q * kWave + lane;
       const size_t at = (size_t)row * a.S + min(sl, a.S - 1);
-      const float4 v = *reinterpret_cast<const float4*>(a.rec_v + at * kTopK);
-      const int4 i = *reinterpret_cast<const int4*>(a.rec_i + at * kTopK);
-      r[q].v[0] = v.x; r[q].v[1] = v.y; r[q].v[2] = v.z; r[q].v[3] = v.w;
-      r[q].i[0] = i.x; r[q].i[1] = i.y; r[q].i[2] = i.z; r[q].i[3] = i.w;
+      const uint4* const src = reinterpret_cast<const uint4*>(a.rec_k + at * kTopK);
+      const uint4 k01 = src[0], k23 = src[1];
+      r[q].k[0] = ((uint64_t)k01.y << 32) | k01.x;
+      r[q].k[1] = ((uint64_t)k01.w << 32) | k01.z;
+      r[q].k[2] = ((uint64_t)k23.y << 32) | k23.x;
+      r[q].k[3] = ((uint64_t)k23.w << 32) | k23.z;
+      r[q].m = key_value(r[q].k[0]);
       r[q].s = a.rec_s[at];
     }
 #pragma unroll
@@ -344,16 +379,14 @@ void k_draft_grow(DraftGrowArgs a) {
     t = top4_merge(t, r[0]);
   }
   t = top4_wave_reduce(t);
-  const float lse = t.v[0] == kNegInf ? kNegInf : t.v[0] + logf(t.s);
+  const float lse = t.m == kNegInf ? kNegInf : t.m + logf(t.s);
   if (lane < kTopK) {
-    float v = t.v[0];
-    int id = t.i[0];
+    uint64_t key = t.k[0];
 #pragma unroll
     for (int k = 1; k < kTopK; ++k)
-      if (lane == k) {
-        v = t.v[k];
-        id = t.i[k];
-      }
+      if (lane == k) key = t.k[k];
+    const float v = key_value(key);
+    const int id = key_id(key);
     float lp = v - lse;
     lp = lp != lp ? kNegInf : lp;
     const int tok = a.vocab_map ? a.vocab_map[id] : id;
@@ -392,25 +425,29 @@ void k_draft_grow(DraftGrowArgs a) {
       tok = s_id[j][c];
       par = fp;
     }
+    // rank of each candidate: the candidates with a higher score, or an equal score and an
+    // earlier position, read back from LDS by every lane
+    if (lane < ncand) s_sc[lane] = sc;
+    wave_lds_sync();
     int rank = 0;
-    for (int q = 0; q < ncand; ++q) {
-      const float sq = lane_value(sc, q);
-      rank += (sq > sc || (sq == sc && q < lane)) ? 1 : 0;
+#pragma unroll
+    for (int q = 0; q < kTopK * kTopK; ++q) {
+      const float sq = s_sc[q];
+      rank += (q < ncand && (sq > sc || (sq == sc && q < lane))) ? 1 : 0;
     }
     if (lane < ncand) {
       tr->tok[n_pool + lane] = tok;
       tr->par[n_pool + lane] = par;
       tr->score[n_pool + lane] = sc;
     }
-      if (lane < ncand && rank < topk) {
+    if (lane < ncand && rank < topk) {
       tr->front[rank] = n_pool + lane;
       tr->front_score[rank] = sc;
+      s_ft[rank] = tok;
     }
     // the token of frontier slot r goes to lane r (the next forward's input order)
-    for (int q = 0; q < ncand; ++q) {
-      const int rq = lane_value(rank, q), tq = lane_value(tok, q);
-      if (rq < topk && lane == rq) new_front_tok = tq;
-    }
+    wave_lds_sync();
+    if (lane < topk) new_front_tok = s_ft[lane];
     if (lane == 0) {
       tr->n_pool = n_pool + ncand;
       tr->n_front = topk;
