@@ -421,3 +421,40 @@ def test_draft_full_size(asv, dev, name):
     W = dw.weights()
     _grow_and_prune(asv, dev, dw.B, dw.V, dw.H, shape=(3, 4, 4), vmap=dw.vocab_map(), W=W,
                     hidden=lambda s: dw.hidden(s), tag=name)
+
+
+def test_many_requests(asv, dev):
+    """600 requests: the offset sums of pruning, tree metadata and commit run over several
+    rounds of their workgroup; a 150-request draft batch spans five 128-row tiles."""
+    import torch
+    rng = np.random.default_rng(31)
+    # draft side: 150 requests, per-request shapes, small vocabulary
+    B, V, H = 150, 300, 64
+    shapes = draft_shapes(B, seed=3)
+    _grow_and_prune(asv, dev, B, V, H, shapes=shapes, tag="many")
+    # tree metadata and commit: 600 requests of 1..40 nodes
+    sizes = rng.integers(1, 41, 600)
+    off = np.concatenate([[0], np.cumsum(sizes)]).astype(np.int32)
+    parent = np.full(off[-1], -1, dtype=np.int32)
+    for b, n in enumerate(sizes):
+        for c in range(1, n):
+            parent[off[b] + c] = off[b] + int(rng.integers(c))
+    base = rng.integers(0, 5000, 600).astype(np.int32)
+    pos, mask, st = asv.tree_meta(_t(parent, dev), _t(off, dev), _t(base, dev), 2)
+    torch.cuda.synchronize()
+    depth, pos_ref, vis = oracle.tree_meta(parent, off, base)
+    assert list(pos.cpu().numpy()) == list(pos_ref) and not st.cpu().numpy().any()
+    m = mask.cpu().numpy().view(np.uint32)
+    for b in range(0, 600, 37):
+        assert np.array_equal(m[off[b]:off[b + 1]], _pack_vis(vis[b], 2)), b
+    tok = rng.integers(0, 1000, off[-1]).astype(np.int32)
+    path, acc = _accepted_paths(parent, off, rng)
+    bonus = rng.integers(0, 1000, 600).astype(np.int32)
+    c_off, c_tok, c_row, _, cst = asv.commit(_t(off, dev), _t(tok, dev), _t(acc, dev),
+                                             _t(path, dev), _t(bonus, dev))
+    torch.cuda.synchronize()
+    ref = oracle.commit(path, acc, bonus, tok, off)
+    total = int(ref["off"][-1])
+    assert list(c_off.cpu().numpy()) == list(ref["off"]) and not cst.cpu().numpy().any()
+    assert list(c_tok.cpu().numpy()[:total]) == list(ref["tok"])
+    assert list(c_row.cpu().numpy()[:total]) == list(ref["row"])
