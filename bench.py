@@ -119,10 +119,12 @@ def _per_call_us(fn, reps: int) -> float:
     return 1e6 * (time.perf_counter() - t0) / reps
 
 
-def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents):
+def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents, tau=None):
     import torch
     import paper_2609_02897_amd as asv
     w, c = load_workload(cfg)
+    if tau is not None:
+        w.tau[:] = np.float32(tau)
     W = w.weights()
     d = to_device(w, W, dev)
     out = asv.alloc_outputs(w.B, w.N, dev, d["draft_logits"] is not None)
@@ -180,7 +182,8 @@ def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents):
                hbm_gbs=bytes_alg / (k1_avg * 1e-3) / 1e9,
                mfma_tflops=flops_alg / (k1_avg * 1e-3) / 1e12,
                bytes_alg=bytes_alg, flops_alg=flops_alg,
-               accepted_len=out.accepted_len.cpu().numpy().tolist()[:4], around=around)
+               accepted_len=out.accepted_len.cpu().numpy().tolist()[:4],
+               mean_accepted_len=float(out.accepted_len.float().mean().cpu()), around=around)
     del d, out, ws
     torch.cuda.empty_cache()
     return res, w, W
@@ -327,6 +330,13 @@ def roofline(r: dict, ceilings: dict = None) -> dict:
     return ro
 
 
+def other_bound(r: dict) -> dict:
+    """K1 against the roofline that does not bind at this row count (both fractions are asked
+    for where the row count sits near the ridge)."""
+    return dict(hbm_frac=round(r["hbm_gbs"] / HBM_PEAK_GBS, 4),
+                mfma_frac=round(r["mfma_tflops"] / BF16_PEAK_TFLOPS, 4))
+
+
 def measured_traffic(cfg: int):
     """HBM bytes per K1 launch from the committed rocprofv3 counter summary, if it was taken
     on the current K1 source; otherwise None."""
@@ -460,6 +470,9 @@ def main():
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-draft", action="store_true",
                     help="skip the draft-step measurement (the step before verification)")
+    ap.add_argument("--others", default="2,4",
+                    help="further verify workloads reported under other_configs ('none' to "
+                         "skip); configuration 4 is timed at each of its thresholds")
     ap.add_argument("--reference", action="store_true",
                     help="only time the vendor references on the bench shapes and exit: "
                          "torch.matmul (hipBLASLt) of the logits alone, and a 1 GiB "
@@ -533,8 +546,24 @@ def main():
         line["secondary"]["roofline"] = roofline(r2, ceilings)
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(w, W)
+    del w, W
+    if args.others != "none":
+        from workloads import CONFIGS
+        line["other_configs"] = []
+        for cfg in (int(x) for x in args.others.split(",")):
+            for tau in (CONFIGS[cfg]["taus"] if cfg == 4 else (None,)):
+                ro, _, _ = measure(cfg, args.steps, args.warmup, dev, hip, tau)
+                print(f"# cfg{cfg} {ro['name']} tau={ro['tau']:.2f}: "
+                      f"{ro['ms_per_step']*1e3:.1f} us/step, K1 {ro['k1_avg_ms']*1e3:.1f} us",
+                      file=sys.stderr, flush=True)
+                line["other_configs"].append({
+                    "workload": ro["name"], "rows": ro["N"], "requests": ro["B"],
+                    "tau": round(ro["tau"], 4), "value": round(ro["value"], 1),
+                    "unit": "nodes/s", "ms_per_step": round(ro["ms_per_step"], 4),
+                    "mean_accepted_len": round(ro["mean_accepted_len"], 3),
+                    "roofline": roofline(ro, ceilings),
+                    "roofline_other_bound": other_bound(ro)})
     if not args.no_draft:
-        del w, W
         line["draft"] = [measure_draft(n, args.steps, args.warmup, dev, hip, not args.no_cpu)
                          for n in ("llama31_8b_draft_b1", "llama31_8b_draft_b32")]
         for d in line["draft"]:
