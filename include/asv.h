@@ -10,6 +10,11 @@
  * adaptive tree policy reads (Sec. 3.3: draft top-1 confidence of Eq. (2) and the rolling
  * acceptance rate with its circuit breaker).
  *
+ * Around it: asv_draft_step / asv_draft_prune build the next draft tree from the draft model's
+ * LM head (Sec. 2, "Draft": topk-way branching, pruning to ndt tokens) in the shape the policy
+ * state selects; asv_tree_meta gives the target forward its positions and tree-attention mask;
+ * asv_commit gathers what a verification step commits.
+ *
  * Conventions shared by every entry point:
  *   - Every array argument is DEVICE memory owned by the caller (e.g. a torch tensor's
  *     data_ptr()). The library never allocates, frees or keeps a pointer after a call returns.

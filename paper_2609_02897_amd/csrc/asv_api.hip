@@ -1,5 +1,6 @@
-// Host side of libasv: argument checks, workspace layout, tile selection and the launch
-// sequence of one verification step. Every entry point is declared in include/asv.h.
+// Host side of libasv: argument checks, workspace layouts, tile selection and the launch
+// sequences of one verification step, one draft step, the pruning of the draft trees, the
+// tree-attention metadata and the commit. Every entry point is declared in include/asv.h.
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
