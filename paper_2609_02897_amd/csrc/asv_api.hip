@@ -279,7 +279,8 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
     // <vocab rows, tree rows, waves along vocab, waves along rows, K per stage, ring depth,
     // W L2-prefetch distance in stages, interleaving strategy>, each the fastest of a sweep on
     // MI355X for its row range. The weight-streaming 64-row tile keeps two workgroups per CU
-    // (80 KB of LDS each), which leaves no room for the prefetch sink.
+    // (80 KB of LDS each), which leaves no room for the prefetch sink; a 3-deep ring with one
+    // workgroup per CU was 0.7% slower in an interleaved comparison over ten placements of W.
     case Tile::kRows64: launch_lmhead<256, 64, 4, 1, 64, 2>(a, L, ws, s); break;
     case Tile::kRows128: launch_lmhead<256, 128, 2, 2, 64, 3>(a, L, ws, s); break;
     case Tile::kRows256: launch_lmhead<256, 256, 2, 2, 64, 2, 3, 0>(a, L, ws, s); break;
