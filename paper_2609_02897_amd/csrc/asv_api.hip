@@ -97,12 +97,13 @@ bool params_ok(const asv_params& p) {
   return true;
 }
 
-template <int TV, int TR, int WV, int WR, int BK, int NST, int PF = 0, int IGLP = -1>
+template <int TV, int TR, int WV, int WR, int BK, int NST, int PF = 0, int IGLP = -1,
+          bool SPREAD = false>
 void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStream_t s) {
   static_assert(TV == kSlab, "tiles span exactly one record slab");
   const int RT = (a->N + TR - 1) / TR;
   const int grid = L.S * RT;
-  k_lmhead_partial<TV, TR, WV, WR, BK, NST, 1, 0, PF, false, IGLP>
+  k_lmhead_partial<TV, TR, WV, WR, BK, NST, 1, 0, PF, false, IGLP, SPREAD>
       <<<grid, WV * WR * kWave, 0, s>>>(
       a->hidden, a->w_lm, a->parent, a->draft_tok, a->req_offsets, a->B, a->N, a->H, a->V,
       L.S, RT, reinterpret_cast<float*>(ws + L.off_rec_m),
@@ -277,13 +278,15 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
   }
   switch (pick_tile(a->N)) {
     // <vocab rows, tree rows, waves along vocab, waves along rows, K per stage, ring depth,
-    // W L2-prefetch distance in stages, interleaving strategy>, each the fastest of a sweep on
-    // MI355X for its row range. The weight-streaming 64-row tile keeps two workgroups per CU
-    // (80 KB of LDS each), which leaves no room for the prefetch sink; a 3-deep ring with one
-    // workgroup per CU was 0.7% slower in an interleaved comparison over ten placements of W.
+    // W L2-prefetch distance in stages, interleaving strategy, spread K loop>, each the
+    // fastest of a sweep on MI355X for its row range. The weight-streaming 64-row tile keeps
+    // two workgroups per CU (80 KB of LDS each), which leaves no room for the prefetch sink; a
+    // 3-deep ring with one workgroup per CU was 0.7% slower in an interleaved comparison over
+    // ten placements of W. The 256-row tile runs the spread K loop (copies spaced between the
+    // MFMAs, no prefetch): 20% faster than the burst ring at 2048 and 3048 rows.
     case Tile::kRows64: launch_lmhead<256, 64, 4, 1, 64, 2>(a, L, ws, s); break;
     case Tile::kRows128: launch_lmhead<256, 128, 2, 2, 64, 3>(a, L, ws, s); break;
-    case Tile::kRows256: launch_lmhead<256, 256, 2, 2, 64, 2, 3, 0>(a, L, ws, s); break;
+    case Tile::kRows256: launch_lmhead<256, 256, 2, 2, 64, 2, 0, -1, true>(a, L, ws, s); break;
   }
   if (int rc = launch_status("k_lmhead_partial")) return rc;
   if (a->k1_end_event) {

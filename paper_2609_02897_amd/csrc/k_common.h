@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace asv {
 
 constexpr int kWave = 64;
@@ -124,6 +126,16 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0)
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// f(std::integral_constant<int, i>{}) for i = 0 .. M-1, each i a compile-time constant (a
+// fully unrolled loop whose body may select code with if constexpr).
+template <int M, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  if constexpr (M > 0) {
+    static_for<M - 1>(f);
+    f(std::integral_constant<int, M - 1>{});
+  }
 }
 
 // Wait until every global store this wave issued has completed (vmcnt(0)).

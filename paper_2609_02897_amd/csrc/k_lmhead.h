@@ -280,8 +280,145 @@ __device__ __forceinline__ void lmhead_tile(
   __syncthreads();
 }
 
+// LDS reads complete, then the workgroup barrier.
+__device__ __forceinline__ void wait_lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" : : : "memory");
+}
+
+// The same logits as lmhead_tile for 64-deep stages in a two-slot ring, with a fixed
+// instruction schedule that spreads each stage's copies over the MFMAs. A stage has four K16
+// steps F0..F3 of NF = MV + MR fragments and MV * MR MFMAs each (NM MFMAs in all). Per stage
+// k, in issue order (one MFMA per position m, the other work attached after it):
+//   m < 2 NF        read F2 and F3 of slot k, one fragment per MFMA;
+//   m = Q1 - 1      LDS reads done + barrier: no wave reads slot k any more;
+//   Q1 <= m < NM    the copies of stage k + 2 into slot k, evenly spaced;
+//   m = Q2 - 1      wait until stage k + 1 has landed (only copies of stage k + 2 may be
+//                   outstanding) + barrier;
+//   m >= Q2         read F0 and F1 of stage k + 1, one fragment per MFMA.
+// Each wave's vector-memory queue thus never holds a whole stage of copies (issued in one
+// burst, they block the wave's in-order instruction stream, and with it its MFMAs, until the
+// CU's address unit has taken them); the stage copy has about 1.5 stages to land. MFMAs
+// accumulate in the same K order as lmhead_tile, so the logits are bit-identical. The
+// schedule is branch-free: past the last stage the copies repeat the last stage into the slot
+// just freed (never read again) and the reads of the stage after the last are discarded.
+template <int TV, int TR, int WV, int WR>
+__device__ __forceinline__ void lmhead_tile_spread(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int N, int H, int V,
+    int v0, int r0, uint4* smem,
+    f32x16 (&acc)[LmheadCfg<TV, TR, WV, WR, 64, 2>::MV][LmheadCfg<TV, TR, WV, WR, 64, 2>::MR]) {
+  constexpr int BK = 64, NST = 2;
+  using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
+  constexpr int CPR = C::CPR;
+  constexpr int MV = C::MV, MR = C::MR;
+  constexpr int NF = MV + MR;                 // fragments per K16 step
+  constexpr int NM = 4 * MV * MR;             // MFMAs per stage
+  constexpr int kCopies = C::kLoads;          // copies per wave per stage
+  constexpr int Q1 = 2 * NF + 2;              // slot-free barrier after MFMA Q1 - 1
+  constexpr int Q2 = NM - 2 * NF - 4;         // next-stage barrier after MFMA Q2 - 1
+  static_assert(2 * NF <= 2 * MV * MR, "F2 and F3 are read within steps 0 and 1");
+  static_assert(Q1 < Q2 && Q2 + 2 * NF <= NM, "schedule points inside the stage");
+  static_assert(Q2 >= 2 * MV * MR, "F0 and F1 of the next stage overwrite registers steps 0 "
+                "and 1 of this stage have finished with");
+  // position of copy c, and how many copies precede the next-stage barrier
+  constexpr auto copy_pos = [](int c) { return Q1 + c * (NM - Q1) / kCopies; };
+  constexpr int kBeforeQ2 = [&] {
+    int n = 0;
+    for (int c = 0; c < kCopies; ++c) n += copy_pos(c) <= Q2 - 1 ? 1 : 0;
+    return n;
+  }();
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wv = wave % WV, wr = wave / WV;
+  const int v_end = min(v0 + TV, V);
+  const int r_last = min(r0 + TR, N) - 1;
+  const int lds0 = __builtin_amdgcn_readfirstlane((int)(size_t)smem);
+  const __amdgpu_buffer_rsrc_t w_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(W + (size_t)v0 * H), (short)0, (v_end - v0) * H * 2, kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t x_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(X + (size_t)r0 * H), (short)0, (r_last + 1 - r0) * H * 2,
+      kRsrcWord3);
+  auto copy_voff = [&](int j) {
+    const int row = j * C::kRowsPerCopy + lane / CPR;
+    return row * H * 2 + ((lane % CPR) ^ swz_phase<CPR>(row)) * 16;
+  };
+  int w_voff[C::DW], x_voff[C::DX];
+#pragma unroll
+  for (int i = 0; i < C::DW; ++i) w_voff[i] = copy_voff(i * C::kWaves + wave);
+#pragma unroll
+  for (int i = 0; i < C::DX; ++i) x_voff[i] = copy_voff(i * C::kWaves + wave);
+  const int KT = H / BK;
+  // copy c (W copies first, then X) of K stage ks into ring slot `slot`
+  auto issue_copy = [&](int slot, int ks, auto cc) {
+    constexpr int c = decltype(cc)::value;
+    const int k2 = ks * BK * 2;
+    const int base = lds0 + slot * C::kStage;
+    if constexpr (c < C::DW)
+      dma16(base + (c * C::kWaves + wave) * 1024, w_voff[c] + k2, w_rsrc);
+    else
+      dma16(base + C::kStageW + ((c - C::DW) * C::kWaves + wave) * 1024, x_voff[c - C::DW] + k2,
+            x_rsrc);
+  };
+
+#pragma unroll
+  for (int i = 0; i < MV; ++i)
+#pragma unroll
+    for (int j = 0; j < MR; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int frag_row = lane & 31, frag_half = lane >> 5;
+  bf16x8 fa[4][MV], fb[4][MR];
+  // fragment f (W for f < MV, else X) of K16 step s of ring slot `slot`
+  auto read_frag = [&](int slot, int s, int f) {
+    const uint4* w = smem + slot * (C::kStage / 16);
+    const uint4* x = w + C::kStageW / 16;
+    if (f < MV)
+      fa[s][f] = __builtin_bit_cast(
+          bf16x8, w[swz<CPR>(wv * C::kWaveV + 32 * f + frag_row, 2 * s + frag_half)]);
+    else
+      fb[s][f - MV] = __builtin_bit_cast(
+          bf16x8, x[swz<CPR>(wr * C::kWaveR + 32 * (f - MV) + frag_row, 2 * s + frag_half)]);
+  };
+
+  // Prologue: stages 0 and 1, wait for stage 0, read its F0 and F1.
+  static_for<kCopies>([&](auto cc) { issue_copy(0, 0, cc); });
+  if (KT > 1) {
+    static_for<kCopies>([&](auto cc) { issue_copy(1, 1, cc); });
+    wait_vm_barrier<kCopies>();
+  } else {
+    wait_vm_barrier<0>();
+  }
+#pragma unroll
+  for (int f = 0; f < NF; ++f) read_frag(0, 0, f);
+#pragma unroll
+  for (int f = 0; f < NF; ++f) read_frag(0, 1, f);
+
+  for (int k = 0; k < KT; ++k) {
+    const int slot = k & 1;
+    const int ks_copy = min(k + 2, KT - 1);
+    static_for<NM>([&](auto mc) {
+      constexpr int m = decltype(mc)::value;
+      constexpr int s = m / (MV * MR), q = m % (MV * MR), i = q / MR, j = q % MR;
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
+      if constexpr (m < 2 * NF) read_frag(slot, 2 + m / NF, m % NF);
+      if constexpr (m == Q1 - 1) wait_lds_barrier();
+      static_for<kCopies>([&](auto cc) {
+        if constexpr (copy_pos(decltype(cc)::value) == m) issue_copy(slot, ks_copy, cc);
+      });
+      if constexpr (m == Q2 - 1) wait_vm_barrier<kBeforeQ2>();
+      if constexpr (m >= Q2 && m < Q2 + 2 * NF)
+        read_frag(slot ^ 1, (m - Q2) / NF, (m - Q2) % NF);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  }
+  // every copy lands before the caller reuses the ring and before the workgroup can exit
+  asm volatile("s_waitcnt vmcnt(0)" : : : "memory");
+  __syncthreads();
+}
+
 template <int TV, int TR, int WV, int WR, int BK, int NST, int OCC = 1, int ORDER = 0,
-          int PF = 0, bool PFX = false, int IGLP = -1>
+          int PF = 0, bool PFX = false, int IGLP = -1, bool SPREAD = false>
 __global__ __launch_bounds__(WV * WR * kWave, OCC)
 void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                       const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
@@ -329,7 +466,12 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
 
   // ---- the tile's logits
   f32x16 acc[C::MV][C::MR];
-  lmhead_tile<TV, TR, WV, WR, BK, NST, PF, PFX, IGLP>(X, W, N, H, V, v0, r0, smem, acc);
+  if constexpr (SPREAD) {
+    static_assert(BK == 64 && NST == 2 && PF == 0, "the spread K loop: 64-deep stages, 2 slots");
+    lmhead_tile_spread<TV, TR, WV, WR>(X, W, N, H, V, v0, r0, smem, acc);
+  } else {
+    lmhead_tile<TV, TR, WV, WR, BK, NST, PF, PFX, IGLP>(X, W, N, H, V, v0, r0, smem, acc);
+  }
   const int frag_half = lane >> 5;
 
   // Output block (i, j), register e of a lane holds vocab row
