@@ -98,7 +98,7 @@ bool params_ok(const asv_params& p) {
 }
 
 template <int TV, int TR, int WV, int WR, int BK, int NST, int PF = 0, int IGLP = -1,
-          bool SPREAD = false>
+          int SPREAD = 0>
 void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStream_t s) {
   static_assert(TV == kSlab, "tiles span exactly one record slab");
   const int RT = (a->N + TR - 1) / TR;
@@ -282,11 +282,12 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
     // fastest of a sweep on MI355X for its row range. The weight-streaming 64-row tile keeps
     // two workgroups per CU (80 KB of LDS each), which leaves no room for the prefetch sink; a
     // 3-deep ring with one workgroup per CU was 0.7% slower in an interleaved comparison over
-    // ten placements of W. The 256-row tile runs the spread K loop (copies spaced between the
-    // MFMAs, no prefetch): 20% faster than the burst ring at 2048 and 3048 rows.
+    // ten placements of W. The 128- and 256-row tiles run the spread K loop (copies spaced
+    // between the MFMAs, no prefetch), in interleaved comparisons 28% faster than the burst
+    // ring at 378 rows and 20% at 2048 and 3048 rows.
     case Tile::kRows64: launch_lmhead<256, 64, 4, 1, 64, 2>(a, L, ws, s); break;
-    case Tile::kRows128: launch_lmhead<256, 128, 2, 2, 64, 3>(a, L, ws, s); break;
-    case Tile::kRows256: launch_lmhead<256, 256, 2, 2, 64, 2, 0, -1, true>(a, L, ws, s); break;
+    case Tile::kRows128: launch_lmhead<256, 128, 2, 2, 64, 3, 0, -1, 3>(a, L, ws, s); break;
+    case Tile::kRows256: launch_lmhead<256, 256, 2, 2, 64, 2, 0, -1, 2>(a, L, ws, s); break;
   }
   if (int rc = launch_status("k_lmhead_partial")) return rc;
   if (a->k1_end_event) {

@@ -417,8 +417,135 @@ __device__ __forceinline__ void lmhead_tile_spread(
   __syncthreads();
 }
 
+// The spread K loop for a three-slot ring: one barrier per stage. Stage j's copies go to slot
+// j % 3 and are spread evenly over the window from the barrier of stage j - 3 (after which no
+// wave reads that slot) to the barrier of stage j - 2 (which waits for stage j - 1); each copy
+// thus has at least one stage to land. Per stage k, one MFMA per position m:
+//   m < 2 NF        read F2 and F3 of slot k, one fragment per MFMA;
+//   m < Q2          the remaining copies of stage k + 2;
+//   m = Q2 - 1      wait until stage k + 1 has landed (only copies of stage k + 2 may be
+//                   outstanding) + barrier;
+//   m >= Q2         read F0 and F1 of stage k + 1; the first copies of stage k + 3.
+// Past the last stage the copies repeat the last stage into slots no later stage reads.
+template <int TV, int TR, int WV, int WR>
+__device__ __forceinline__ void lmhead_tile_spread3(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int N, int H, int V,
+    int v0, int r0, uint4* smem,
+    f32x16 (&acc)[LmheadCfg<TV, TR, WV, WR, 64, 3>::MV][LmheadCfg<TV, TR, WV, WR, 64, 3>::MR]) {
+  constexpr int BK = 64, NST = 3;
+  using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
+  constexpr int CPR = C::CPR;
+  constexpr int MV = C::MV, MR = C::MR;
+  constexpr int NF = MV + MR;                 // fragments per K16 step
+  constexpr int NM = 4 * MV * MR;             // MFMAs per stage
+  constexpr int G = C::kLoads;                // copies per wave per stage
+  constexpr int Q2 = NM - 2 * NF;             // the barrier after MFMA Q2 - 1
+  static_assert(Q2 >= 2 * NF + 2, "F2 and F3 reads land before the barrier");
+  static_assert(Q2 >= 2 * MV * MR, "F0 and F1 of the next stage overwrite registers steps 0 "
+                "and 1 of this stage have finished with");
+  static_assert(2 * G <= 63, "vmcnt range");
+  // copy c of a group sits c * NM / G MFMAs after the barrier that opens its window; the
+  // first n1 of them fall in the same stage as that barrier
+  constexpr auto rel = [](int c) { return c * NM / G; };
+  constexpr int n1 = [&] {
+    int n = 0;
+    for (int c = 0; c < G; ++c) n += Q2 + rel(c) < NM ? 1 : 0;
+    return n;
+  }();
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wv = wave % WV, wr = wave / WV;
+  const int v_end = min(v0 + TV, V);
+  const int r_last = min(r0 + TR, N) - 1;
+  const int lds0 = __builtin_amdgcn_readfirstlane((int)(size_t)smem);
+  const __amdgpu_buffer_rsrc_t w_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(W + (size_t)v0 * H), (short)0, (v_end - v0) * H * 2, kRsrcWord3);
+  const __amdgpu_buffer_rsrc_t x_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(X + (size_t)r0 * H), (short)0, (r_last + 1 - r0) * H * 2,
+      kRsrcWord3);
+  auto copy_voff = [&](int j) {
+    const int row = j * C::kRowsPerCopy + lane / CPR;
+    return row * H * 2 + ((lane % CPR) ^ swz_phase<CPR>(row)) * 16;
+  };
+  int w_voff[C::DW], x_voff[C::DX];
+#pragma unroll
+  for (int i = 0; i < C::DW; ++i) w_voff[i] = copy_voff(i * C::kWaves + wave);
+#pragma unroll
+  for (int i = 0; i < C::DX; ++i) x_voff[i] = copy_voff(i * C::kWaves + wave);
+  const int KT = H / BK;
+  // copy c (W copies first, then X) of stage j into slot j % 3, from K stage min(j, KT - 1)
+  auto issue_copy = [&](int j, auto cc) {
+    constexpr int c = decltype(cc)::value;
+    const int k2 = min(j, KT - 1) * BK * 2;
+    const int base = lds0 + (j % NST) * C::kStage;
+    if constexpr (c < C::DW)
+      dma16(base + (c * C::kWaves + wave) * 1024, w_voff[c] + k2, w_rsrc);
+    else
+      dma16(base + C::kStageW + ((c - C::DW) * C::kWaves + wave) * 1024, x_voff[c - C::DW] + k2,
+            x_rsrc);
+  };
+
+#pragma unroll
+  for (int i = 0; i < MV; ++i)
+#pragma unroll
+    for (int j = 0; j < MR; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+
+  const int frag_row = lane & 31, frag_half = lane >> 5;
+  bf16x8 fa[4][MV], fb[4][MR];
+  auto read_frag = [&](int slot, int s, int f) {
+    const uint4* w = smem + slot * (C::kStage / 16);
+    const uint4* x = w + C::kStageW / 16;
+    if (f < MV)
+      fa[s][f] = __builtin_bit_cast(
+          bf16x8, w[swz<CPR>(wv * C::kWaveV + 32 * f + frag_row, 2 * s + frag_half)]);
+    else
+      fb[s][f - MV] = __builtin_bit_cast(
+          bf16x8, x[swz<CPR>(wr * C::kWaveR + 32 * (f - MV) + frag_row, 2 * s + frag_half)]);
+  };
+
+  // Prologue: stages 0 and 1 and the first n1 copies of stage 2 (what the window of a stage
+  // -1 would have issued); wait for stage 0; read its F0 and F1.
+  static_for<G>([&](auto cc) { issue_copy(0, cc); });
+  static_for<G>([&](auto cc) { issue_copy(1, cc); });
+  static_for<G>([&](auto cc) {
+    if constexpr (decltype(cc)::value < n1) issue_copy(2, cc);
+  });
+  wait_vm_barrier<G + n1>();
+#pragma unroll
+  for (int f = 0; f < NF; ++f) read_frag(0, 0, f);
+#pragma unroll
+  for (int f = 0; f < NF; ++f) read_frag(0, 1, f);
+
+  int slot = 0;
+  for (int k = 0; k < KT; ++k) {
+    const int nslot = slot == NST - 1 ? 0 : slot + 1;
+    static_for<NM>([&](auto mc) {
+      constexpr int m = decltype(mc)::value;
+      constexpr int s = m / (MV * MR), q = m % (MV * MR), i = q / MR, j = q % MR;
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
+      if constexpr (m < 2 * NF) read_frag(slot, 2 + m / NF, m % NF);
+      static_for<G>([&](auto cc) {
+        constexpr int c = decltype(cc)::value;
+        if constexpr (c >= n1 && Q2 + rel(c) - NM == m) issue_copy(k + 2, cc);
+        if constexpr (c < n1 && Q2 + rel(c) == m) issue_copy(k + 3, cc);
+      });
+      if constexpr (m == Q2 - 1) wait_vm_barrier<G>();
+      if constexpr (m >= Q2 && m < Q2 + 2 * NF)
+        read_frag(nslot, (m - Q2) / NF, (m - Q2) % NF);
+      __builtin_amdgcn_sched_barrier(0);
+    });
+    slot = nslot;
+  }
+  // every copy lands before the caller reuses the ring and before the workgroup can exit
+  asm volatile("s_waitcnt vmcnt(0)" : : : "memory");
+  __syncthreads();
+}
+
 template <int TV, int TR, int WV, int WR, int BK, int NST, int OCC = 1, int ORDER = 0,
-          int PF = 0, bool PFX = false, int IGLP = -1, bool SPREAD = false>
+          int PF = 0, bool PFX = false, int IGLP = -1, int SPREAD = 0>
 __global__ __launch_bounds__(WV * WR * kWave, OCC)
 void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                       const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
@@ -466,9 +593,13 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
 
   // ---- the tile's logits
   f32x16 acc[C::MV][C::MR];
-  if constexpr (SPREAD) {
-    static_assert(BK == 64 && NST == 2 && PF == 0, "the spread K loop: 64-deep stages, 2 slots");
+  // SPREAD = ring depth of the spread K loop (2 or 3); 0: the burst ring of lmhead_tile
+  if constexpr (SPREAD == 2) {
+    static_assert(BK == 64 && NST == 2 && PF == 0, "two-slot spread loop: 64-deep stages");
     lmhead_tile_spread<TV, TR, WV, WR>(X, W, N, H, V, v0, r0, smem, acc);
+  } else if constexpr (SPREAD == 3) {
+    static_assert(BK == 64 && NST == 3 && PF == 0, "three-slot spread loop: 64-deep stages");
+    lmhead_tile_spread3<TV, TR, WV, WR>(X, W, N, H, V, v0, r0, smem, acc);
   } else {
     lmhead_tile<TV, TR, WV, WR, BK, NST, PF, PFX, IGLP>(X, W, N, H, V, v0, r0, smem, acc);
   }
