@@ -110,10 +110,22 @@ def _case(name):
         trees = [_rand_tree(rng, 20, 5, 3), _rand_tree(rng, 11, 4, 3)]
         return custom_workload(name, 64, 170000, trees, 0.2, seed=11, w_std=0.16,
                                draft_logits=True)
+    if name == "rows128_five_stages":
+        # 128-row tiles (three-slot spread loop) over H = 320, five K stages: both ring wraps
+        # and the tail copies past the last stage; two row tiles, the second ragged
+        trees = [_rand_tree(rng, int(rng.integers(20, 60)), 7, 4) for _ in range(5)]
+        return custom_workload(name, 320, 2000, trees, 0.2, seed=12, w_std=0.07)
+    if name == "rows256_five_stages":
+        # 256-row tiles (two-slot spread loop) over H = 320, five K stages; ragged last row tile
+        # and ragged last slab
+        trees = [_rand_tree(rng, int(rng.integers(40, 120)), 8, 4) for _ in range(9)]
+        return custom_workload(name, 320, 1500, trees, 0.2, seed=13, w_std=0.07,
+                               draft_logits=True)
     raise KeyError(name)
 
 
 CASES = ["tiny_config", "rows64_eagle60_ragged_vocab", "rows128_mixed", "rows256_three_tiles",
+         "rows128_five_stages", "rows256_five_stages",
          "deep_chain_and_wide", "root_only_requests", "many_tiny_requests",
          "unfused_large_batch", "request_over_lds_stage", "unfused_with_large_request",
          "single_row_single_slab", "vocab_over_one_merge_round"]
