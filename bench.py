@@ -21,6 +21,7 @@ from __future__ import annotations
 import argparse
 import ctypes
 import hashlib
+import re
 import json
 import os
 import sys
@@ -41,10 +42,19 @@ K5_SOURCES = [os.path.join(ROOT, "paper_2609_02897_amd", "csrc", f)
               for f in ("k_draft.h", "k_lmhead.h", "k_common.h")]
 
 
+def _code_text(path) -> str:
+    """The C++ source with comments removed and whitespace collapsed: what the kernel is made
+    of, so that a comment edit does not disown the counters taken on the same code."""
+    src = open(path, encoding="utf-8").read()
+    src = re.sub(r"/\*.*?\*/", " ", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", " ", src)
+    return " ".join(src.split())
+
+
 def _sha(paths) -> str:
     h = hashlib.sha256()
     for p in paths:
-        h.update(open(p, "rb").read())
+        h.update(_code_text(p).encode())
     return h.hexdigest()[:16]
 
 

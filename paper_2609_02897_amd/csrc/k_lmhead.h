@@ -9,14 +9,18 @@
 // margin rule of Sec. 3.2, Eq. (1) needs; the [N][V] logits never reach memory.
 //
 // Data flow: a ring of NST LDS stages, each holding BK K-elements of every W and X row of the
-// tile. Stages are filled by direct global->LDS buffer loads (no staging registers), issued
-// NST-1 stages ahead of their use; their completion is awaited by hand (s_waitcnt vmcnt) just
-// before the one workgroup barrier per stage. 16-byte chunks are XOR-swizzled so that
+// tile. Stages are filled by direct global->LDS buffer loads (no staging registers) and their
+// completion is awaited by hand (s_waitcnt vmcnt) before a workgroup barrier. Two K loops
+// share this layout: lmhead_tile issues each stage's copies in one burst, NST-1 stages ahead,
+// with one barrier per stage; lmhead_tile_spread / lmhead_tile_spread3 place every copy
+// between two MFMAs on a fixed schedule, so the copies never stall a wave's MFMAs (the 128-
+// and 256-row tiles, which are MFMA-bound). 16-byte chunks are XOR-swizzled so that
 // ds_read_b128 in the MFMA operand layout is free of bank conflicts. The MFMA is
 // v_mfma_f32_32x32x16_bf16 with A = W (32 vocabulary rows) and B = X (32 tree rows): each lane
 // then owns one tree row and 16 vocabulary entries of every 32x32 output block, so the
-// per-row reduction is mostly lane-local. Fragments of the next K16 step are read while the
-// current MFMAs run.
+// per-row reduction is mostly lane-local. Fragments of a later K16 step are read while the
+// current MFMAs run. Every loop accumulates K in increasing order, so all tiles give the same
+// logits bit for bit.
 #pragma once
 
 #include <type_traits>
