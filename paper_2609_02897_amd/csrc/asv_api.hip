@@ -97,14 +97,12 @@ bool params_ok(const asv_params& p) {
   return true;
 }
 
-template <int TV, int TR, int WV, int WR, int BK, int NST, int PF = 0, int IGLP = -1,
-          int SPREAD = 0>
+template <int TV, int TR, int WV, int WR, int BK, int NST, int LOOP = 0>
 void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStream_t s) {
   static_assert(TV == kSlab, "tiles span exactly one record slab");
   const int RT = (a->N + TR - 1) / TR;
   const int grid = L.S * RT;
-  k_lmhead_partial<TV, TR, WV, WR, BK, NST, 1, 0, PF, false, IGLP, SPREAD>
-      <<<grid, WV * WR * kWave, 0, s>>>(
+  k_lmhead_partial<TV, TR, WV, WR, BK, NST, LOOP><<<grid, WV * WR * kWave, 0, s>>>(
       a->hidden, a->w_lm, a->parent, a->draft_tok, a->req_offsets, a->B, a->N, a->H, a->V,
       L.S, RT, reinterpret_cast<float*>(ws + L.off_rec_m),
       reinterpret_cast<float*>(ws + L.off_rec_s), reinterpret_cast<int32_t*>(ws + L.off_rec_a),
@@ -178,11 +176,11 @@ bool draft_sizes_ok(int B, int H, int V) {
   return true;
 }
 
-template <int TV, int TR, int WV, int WR, int BK, int NST, int PF = 0>
+template <int TV, int TR, int WV, int WR, int BK, int NST>
 void launch_draft(const asv_draft_args* a, const DraftLayout& L, char* ws, hipStream_t s) {
   const int R = a->B * kTopK;
   const int RT = (R + TR - 1) / TR;
-  k_draft_partial<TV, TR, WV, WR, BK, NST, PF><<<L.S * RT, WV * WR * kWave, 0, s>>>(
+  k_draft_partial<TV, TR, WV, WR, BK, NST><<<L.S * RT, WV * WR * kWave, 0, s>>>(
       a->hidden, a->w_draft, R, a->H, a->V, L.S, RT, reinterpret_cast<uint64_t*>(ws + L.off_k),
       reinterpret_cast<float*>(ws + L.off_s));
 }
@@ -278,16 +276,15 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
   }
   switch (pick_tile(a->N)) {
     // <vocab rows, tree rows, waves along vocab, waves along rows, K per stage, ring depth,
-    // W L2-prefetch distance in stages, interleaving strategy, spread K loop>, each the
-    // fastest of a sweep on MI355X for its row range. The weight-streaming 64-row tile keeps
-    // two workgroups per CU (80 KB of LDS each), which leaves no room for the prefetch sink; a
-    // 3-deep ring with one workgroup per CU was 0.7% slower in an interleaved comparison over
-    // ten placements of W. The 128- and 256-row tiles run the spread K loop (copies spaced
-    // between the MFMAs, no prefetch), in interleaved comparisons 28% faster than the burst
-    // ring at 378 rows and 20% at 2048 and 3048 rows.
+    // K loop>, each the fastest of a sweep on MI355X for its row range. The weight-streaming
+    // 64-row tile keeps two workgroups per CU (80 KB of LDS each) with the burst ring; a 3-deep
+    // ring with one workgroup per CU was 0.7% slower in an interleaved comparison over ten
+    // placements of W. The 128- and 256-row tiles run the spread K loops (copies spaced
+    // between the MFMAs), in interleaved comparisons 28% faster than the burst ring at 378
+    // rows and 20% at 2048 and 3048 rows.
     case Tile::kRows64: launch_lmhead<256, 64, 4, 1, 64, 2>(a, L, ws, s); break;
-    case Tile::kRows128: launch_lmhead<256, 128, 2, 2, 64, 3, 0, -1, 3>(a, L, ws, s); break;
-    case Tile::kRows256: launch_lmhead<256, 256, 2, 2, 64, 2, 0, -1, 2>(a, L, ws, s); break;
+    case Tile::kRows128: launch_lmhead<256, 128, 2, 2, 64, 3, 3>(a, L, ws, s); break;
+    case Tile::kRows256: launch_lmhead<256, 256, 2, 2, 64, 2, 2>(a, L, ws, s); break;
   }
   if (int rc = launch_status("k_lmhead_partial")) return rc;
   if (a->k1_end_event) {
@@ -346,8 +343,7 @@ extern "C" int asv_draft_step(const asv_draft_args* a, void* workspace, uint64_t
   (void)hipGetLastError();
   if (int rc = record_event(a->k_begin_event, s, "hipEventRecord(k_begin_event)")) return rc;
   switch (pick_draft_tile(a->B * kTopK)) {
-    // <vocab rows, draft rows, waves along vocab, waves along rows, K per stage, ring depth,
-    // W L2-prefetch distance>
+    // <vocab rows, draft rows, waves along vocab, waves along rows, K per stage, ring depth>
     case DraftTile::kRows32: launch_draft<64, 32, 2, 1, 64, 4>(a, L, ws, s); break;
     case DraftTile::kRows64: launch_draft<64, 64, 2, 2, 64, 4>(a, L, ws, s); break;
     case DraftTile::kRows128: launch_draft<128, 128, 2, 2, 64, 3>(a, L, ws, s); break;

@@ -66,15 +66,6 @@ __device__ __forceinline__ void dma16(int lds, int voff, __amdgpu_buffer_rsrc_t 
                : "s"(lds), "v"(voff), "s"(r)
                : "memory", "m0");
 }
-// The same with 4 bytes per lane. Used to pull cache lines into L2 ahead of their stage: the
-// destination is a sink region of LDS that is never read (no register is left to be
-// overwritten by a late load).
-__device__ __forceinline__ void dma4(int lds, int voff, __amdgpu_buffer_rsrc_t r) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds"
-               :
-               : "s"(lds), "v"(voff), "s"(r)
-               : "memory", "m0");
-}
 #pragma clang diagnostic pop
 
 // Wait until at most N vector-memory operations of this wave are outstanding and its LDS
@@ -85,14 +76,14 @@ __device__ __forceinline__ void wait_vm_barrier() {
   asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" : : "n"(N) : "memory");
 }
 
-// wait_vm_barrier<T + newer * L>() for a run-time newer in [0, 3]: each stage issues L
-// operations, the last T of which (the L2 prefetches) need not have completed.
-template <int L, int T = 0>
+// wait_vm_barrier<newer * L>() for a run-time newer in [0, 3]: each stage issues L operations,
+// and the newer stages' operations may stay in flight.
+template <int L>
 __device__ __forceinline__ void wait_stage_barrier(int newer) {
-  if (newer >= 3) wait_vm_barrier<T + 3 * L>();
-  else if (newer == 2) wait_vm_barrier<T + 2 * L>();
-  else if (newer == 1) wait_vm_barrier<T + L>();
-  else wait_vm_barrier<T>();
+  if (newer >= 3) wait_vm_barrier<3 * L>();
+  else if (newer == 2) wait_vm_barrier<2 * L>();
+  else if (newer == 1) wait_vm_barrier<L>();
+  else wait_vm_barrier<0>();
 }
 
 template <int TV, int TR, int WV, int WR, int BK, int NST>
@@ -131,38 +122,17 @@ __device__ __forceinline__ int xcd_tile(int bid, int G) {
   return xcd * q + min(xcd, rem) + loc;
 }
 
-// LDS bytes of the L2-prefetch sink (PF > 0): one 1 KB region per wave, never read.
-template <int TV, int TR, int WV, int WR, int PF>
-constexpr int lmhead_sink_bytes() { return PF > 0 ? WV * WR * 1024 : 0; }
-
 // The logits of one tile, left in the MFMA accumulators: acc[i][j] holds the 32x32 block of
 // vocabulary rows v0 + wv * kWaveV + 32 i .. and tree rows r0 + wr * kWaveR + 32 j .. of this
 // wave, summed over all of H. Rows past V or past N read as zeros. On return every stage copy
 // has landed and the workgroup has passed a barrier, so the caller may reuse the LDS ring.
-//
-// PF > 0: every stage also pulls the W lines of stage k + PF into L2 (one 4-byte LDS-sink
-// load per W row), so the stage copies that follow hit L2 instead of waiting on HBM.
-// PFX: the same for the X rows. IGLP >= 0: the compiler's MFMA / LDS-read interleaving
-// strategy of that number is applied to each K16 step that reads the next step's fragments
-// (-1: the default schedule).
-template <int TV, int TR, int WV, int WR, int BK, int NST, int PF, bool PFX, int IGLP>
+template <int TV, int TR, int WV, int WR, int BK, int NST>
 __device__ __forceinline__ void lmhead_tile(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int N, int H, int V,
     int v0, int r0, uint4* smem,
     f32x16 (&acc)[LmheadCfg<TV, TR, WV, WR, BK, NST>::MV][LmheadCfg<TV, TR, WV, WR, BK, NST>::MR]) {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
   constexpr int CPR = C::CPR;
-  constexpr int kPfRows = TV / C::kWaves;             // W rows each wave prefetches
-  constexpr int kPfRowsX = TR / C::kWaves;            // X rows each wave prefetches (PFX)
-  constexpr int kPfW = PF > 0 ? kPfRows / kWave : 0;
-  constexpr int kPfX = PF > 0 && PFX ? kPfRowsX / kWave : 0;
-  constexpr int kPf = kPfW + kPfX;                    // prefetch loads per wave per stage
-  constexpr int kGroup = C::kLoads + kPf;             // vector-memory ops per wave per stage
-  static_assert(PF == 0 || (kPfRows % kWave == 0 && (!PFX || kPfRowsX % kWave == 0)),
-                "whole prefetch rows per lane");
-  static_assert((NST - 2) * kGroup + kPf <= 63, "vmcnt range");
-  static_assert(C::kLds + lmhead_sink_bytes<TV, TR, WV, WR, PF>() <= 160 * 1024,
-                "LDS per workgroup");
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -201,18 +171,6 @@ __device__ __forceinline__ void lmhead_tile(
 #pragma unroll
     for (int i = 0; i < C::DX; ++i)
       dma16(base + C::kStageW + (i * C::kWaves + wave) * 1024, x_voff[i] + k2, x_rsrc);
-    if constexpr (PF > 0) {
-      // always issued (clamped to the last stage) so every stage has kGroup operations
-      const int kp2 = min(ks + PF, KT - 1) * BK * 2;
-#pragma unroll
-      for (int i = 0; i < kPfW; ++i)
-        dma4(lds0 + C::kLds + wave * 1024,
-             ((wave * kPfW + i) * kWave + lane) * H * 2 + kp2, w_rsrc);
-#pragma unroll
-      for (int i = 0; i < kPfX; ++i)
-        dma4(lds0 + C::kLds + wave * 1024,
-             ((wave * kPfX + i) * kWave + lane) * H * 2 + kp2, x_rsrc);
-    }
   };
 
 #pragma unroll
@@ -249,7 +207,7 @@ __device__ __forceinline__ void lmhead_tile(
   // Prologue: fill the whole ring, then wait for stage 0.
   const int pro = min(NST, KT);
   for (int ks = 0; ks < pro; ++ks) issue_stage(ks);
-  wait_stage_barrier<kGroup, kPf>(pro - 1);
+  wait_stage_barrier<C::kLoads>(pro - 1);
   load_frags(0, 0, a0, b0);
 
   // Per stage k with K16 steps s = 0 .. BK/16 - 1: read the fragments of step s + 1 while the
@@ -267,10 +225,9 @@ __device__ __forceinline__ void lmhead_tile(
       bf16x8* nb = (s & 1) ? b0 : b1;
       if (s + 1 < NS16) {
         load_frags(slot, s + 1, na, nb);
-        if constexpr (IGLP >= 0) __builtin_amdgcn_iglp_opt(IGLP);
       } else if (k + 1 < KT) {
         // stage k+1 must have landed; the copies of the newer stages may stay in flight
-        wait_stage_barrier<kGroup, kPf>(min(NST - 2, KT - 2 - k));
+        wait_stage_barrier<C::kLoads>(min(NST - 2, KT - 2 - k));
         if (k + NST < KT) issue_stage(k + NST);
         load_frags((k + 1) % NST, 0, na, nb);
       }
@@ -278,9 +235,7 @@ __device__ __forceinline__ void lmhead_tile(
     }
   }
   static_assert(NS16 % 2 == 0, "fragment double buffer alternates within a stage");
-  // the last L2 prefetches may still be in flight: every LDS copy lands before the caller
-  // reuses the ring and before the workgroup can exit
-  if constexpr (PF > 0) asm volatile("s_waitcnt vmcnt(0)" : : : "memory");
+  // every copy was waited for by the last stage's predecessor
   __syncthreads();
 }
 
@@ -548,9 +503,10 @@ __device__ __forceinline__ void lmhead_tile_spread3(
   __syncthreads();
 }
 
-template <int TV, int TR, int WV, int WR, int BK, int NST, int OCC = 1, int ORDER = 0,
-          int PF = 0, bool PFX = false, int IGLP = -1, int SPREAD = 0>
-__global__ __launch_bounds__(WV * WR * kWave, OCC)
+// LOOP selects the K loop: 0 = the burst ring of lmhead_tile; 2 and 3 = the spread loop of
+// that ring depth (lmhead_tile_spread, lmhead_tile_spread3).
+template <int TV, int TR, int WV, int WR, int BK, int NST, int LOOP = 0>
+__global__ __launch_bounds__(WV * WR * kWave, 1)
 void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                       const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
                       const int32_t* __restrict__ req_offsets, int B, int N, int H, int V,
@@ -559,18 +515,17 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
                       int32_t* __restrict__ done_cnt, int n_cnt) {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
   constexpr int T = C::kThreads;
-  __shared__ uint4 smem[(C::kLds + lmhead_sink_bytes<TV, TR, WV, WR, PF>()) / 16];
+  __shared__ uint4 smem[C::kLds / 16];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wv = wave % WV, wr = wave / WV;
   // clear the per-request completion counters of the finishing kernel that follows
   for (int i = blockIdx.x * T + tid; i < n_cnt; i += gridDim.x * T) done_cnt[i] = 0;
+  // consecutive tiles are the row tiles of one slab, which share the W slab through L2
   const int tile = xcd_tile(blockIdx.x, gridDim.x);
-  // ORDER 0: consecutive tiles are the row tiles of one slab (W slab shared in L2);
-  // ORDER 1: consecutive tiles are the slabs of one row tile (X tile resident in L2).
-  const int slab = ORDER == 0 ? tile / RT : tile % S;
-  const int rt = ORDER == 0 ? tile % RT : tile / S;
+  const int slab = tile / RT;
+  const int rt = tile % RT;
   const int v0 = slab * TV, r0 = rt * TR;
   const int v_end = min(v0 + TV, V);
   const int r_last = min(r0 + TR, N) - 1;
@@ -597,15 +552,15 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
 
   // ---- the tile's logits
   f32x16 acc[C::MV][C::MR];
-  // SPREAD = ring depth of the spread K loop (2 or 3); 0: the burst ring of lmhead_tile
-  if constexpr (SPREAD == 2) {
-    static_assert(BK == 64 && NST == 2 && PF == 0, "two-slot spread loop: 64-deep stages");
+  if constexpr (LOOP == 2) {
+    static_assert(BK == 64 && NST == 2, "two-slot spread loop: 64-deep stages");
     lmhead_tile_spread<TV, TR, WV, WR>(X, W, N, H, V, v0, r0, smem, acc);
-  } else if constexpr (SPREAD == 3) {
-    static_assert(BK == 64 && NST == 3 && PF == 0, "three-slot spread loop: 64-deep stages");
+  } else if constexpr (LOOP == 3) {
+    static_assert(BK == 64 && NST == 3, "three-slot spread loop: 64-deep stages");
     lmhead_tile_spread3<TV, TR, WV, WR>(X, W, N, H, V, v0, r0, smem, acc);
   } else {
-    lmhead_tile<TV, TR, WV, WR, BK, NST, PF, PFX, IGLP>(X, W, N, H, V, v0, r0, smem, acc);
+    static_assert(LOOP == 0, "K loop");
+    lmhead_tile<TV, TR, WV, WR, BK, NST>(X, W, N, H, V, v0, r0, smem, acc);
   }
   const int frag_half = lane >> 5;
 
