@@ -56,9 +56,25 @@ def _same_trees(asv, a, b, tag):
         assert bytes(x.score)[:4 * P] == bytes(y.score)[:4 * P], tag
 
 
-def test_verify_graph_replays(asv, dev):
+def _chain_and_fans(n_req, size):
+    """n_req requests of `size` nodes: a chain of four, the rest fanned out under its tip."""
+    return [[-1, 0, 1, 2] + [3] * (size - 4) for _ in range(n_req)]
+
+
+# one tree set per K1 tile family: 20 rows (64-row tile, burst ring), 200 rows (128-row tile,
+# three-slot spread loop), 520 rows (256-row tile, two-slot spread loop)
+GRAPH_TREES = {
+    "rows64": [[-1, 0, 0, 1, 1, 2, 3], [-1, 0, 1], [-1] + [0] * 9],
+    "rows128": _chain_and_fans(5, 40),
+    "rows256": _chain_and_fans(8, 65),
+}
+
+
+@pytest.mark.parametrize("family", list(GRAPH_TREES))
+def test_verify_graph_replays(asv, dev, family):
     import torch
-    trees = [[-1, 0, 0, 1, 1, 2, 3], [-1, 0, 1], [-1] + [0] * 9]
+    print(f"[graph] verify {family}", flush=True)
+    trees = GRAPH_TREES[family]
     w = custom_workload("graph", 256, 3000, trees, 0.2, seed=41, w_std=0.1)
     rng = np.random.default_rng(5)
     w.draft_tok = rng.integers(0, 3000, w.N).astype(np.int32)
