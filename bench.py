@@ -36,10 +36,11 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2516.6      # MI355X dense bf16 MFMA (256 CU x 2.4 GHz x 4096 flop/clk)
 TABLES = os.path.join(ROOT, "tests", "golden")
 TRAFFIC = os.path.join(ROOT, "profiles", "k1_traffic.json")
+# the kernels and the host code that picks their tiles
 K1_SOURCES = [os.path.join(ROOT, "paper_2609_02897_amd", "csrc", f)
-              for f in ("k_lmhead.h", "k_common.h")]
+              for f in ("k_lmhead.h", "k_common.h", "asv_api.hip")]
 K5_SOURCES = [os.path.join(ROOT, "paper_2609_02897_amd", "csrc", f)
-              for f in ("k_draft.h", "k_lmhead.h", "k_common.h")]
+              for f in ("k_draft.h", "k_lmhead.h", "k_common.h", "asv_api.hip")]
 
 
 def _code_text(path) -> str:

@@ -40,18 +40,21 @@ int launch_status(const char* what) {
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Tile families of K1, chosen from the number of tree rows. Few rows (the weight-streaming
-// regime of small batches) use a 64-row tile so that all rows share one pass over W; up to 384
-// rows, 128-row tiles (twice the workgroups of 256-row tiles balance better over the CUs and
-// pad less: 5-10% faster on MI355X from 140 to 384 rows); beyond, 256x256 tiles.
-enum class Tile { kRows64, kRows128, kRows256 };
+// regime of small batches) use a 64-row tile so that all rows share one pass over W. Between 64
+// and 384 rows the pick is the tile that pads least, and among equal padding the larger tile,
+// which copies fewer bytes per MFMA (interleaved comparisons on MI355X, V = 151936: the 192-row
+// tile is 14% faster than two 128-row tiles at 150-180 rows and 4-7% faster than three at
+// 260-384 rows; at 200 rows the 128- and 256-row tiles tie). Beyond 384 rows, 256x256 tiles.
+enum class Tile { kRows64, kRows128, kRows192, kRows256 };
 
 Tile pick_tile(int N) {
   if (N <= 64) return Tile::kRows64;
-  if (N <= 384) return Tile::kRows128;
+  if (N <= 128) return Tile::kRows128;
+  if (N <= 192) return Tile::kRows192;
+  if (N <= 256) return Tile::kRows128;
+  if (N <= 384) return Tile::kRows192;
   return Tile::kRows256;
 }
-
-int tile_rows(Tile t) { return t == Tile::kRows64 ? 64 : t == Tile::kRows128 ? 128 : 256; }
 
 struct Layout {
   int S = 0;       // vocabulary slabs
@@ -279,11 +282,12 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
     // K loop>, each the fastest of a sweep on MI355X for its row range. The weight-streaming
     // 64-row tile keeps two workgroups per CU (80 KB of LDS each) with the burst ring; a 3-deep
     // ring with one workgroup per CU was 0.7% slower in an interleaved comparison over ten
-    // placements of W. The 128- and 256-row tiles run the spread K loops (copies spaced
+    // placements of W. The 128-, 192- and 256-row tiles run the spread K loops (copies spaced
     // between the MFMAs), in interleaved comparisons 28% faster than the burst ring at 378
     // rows and 20% at 2048 and 3048 rows.
     case Tile::kRows64: launch_lmhead<256, 64, 4, 1, 64, 2>(a, L, ws, s); break;
     case Tile::kRows128: launch_lmhead<256, 128, 2, 2, 64, 3, 3>(a, L, ws, s); break;
+    case Tile::kRows192: launch_lmhead<256, 192, 2, 2, 64, 2, 2>(a, L, ws, s); break;
     case Tile::kRows256: launch_lmhead<256, 256, 2, 2, 64, 2, 2>(a, L, ws, s); break;
   }
   if (int rc = launch_status("k_lmhead_partial")) return rc;

@@ -62,10 +62,12 @@ def _chain_and_fans(n_req, size):
 
 
 # one tree set per K1 tile family: 20 rows (64-row tile, burst ring), 200 rows (128-row tile,
-# three-slot spread loop), 520 rows (256-row tile, two-slot spread loop)
+# three-slot spread loop), 300 rows (192-row tile) and 520 rows (256-row tile, both two-slot
+# spread loop)
 GRAPH_TREES = {
     "rows64": [[-1, 0, 0, 1, 1, 2, 3], [-1, 0, 1], [-1] + [0] * 9],
     "rows128": _chain_and_fans(5, 40),
+    "rows192": _chain_and_fans(6, 50),
     "rows256": _chain_and_fans(8, 65),
 }
 

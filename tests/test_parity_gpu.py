@@ -121,11 +121,20 @@ def _case(name):
         trees = [_rand_tree(rng, int(rng.integers(40, 120)), 8, 4) for _ in range(9)]
         return custom_workload(name, 320, 1500, trees, 0.2, seed=13, w_std=0.07,
                                draft_logits=True)
+    if name == "rows192_two_tiles":
+        # 192-row tiles (two-slot spread loop) over H = 320: two row tiles, the second ragged
+        trees = [_rand_tree(rng, int(rng.integers(30, 80)), 8, 4) for _ in range(6)]
+        return custom_workload(name, 320, 1800, trees, 0.2, seed=14, w_std=0.07,
+                               draft_logits=True)
+    if name == "rows192_one_tile":
+        # one ragged 192-row tile over H = 192 (three K stages)
+        trees = [_rand_tree(rng, int(rng.integers(36, 48)), 6, 4) for _ in range(4)]
+        return custom_workload(name, 192, 1300, trees, 0.3, seed=15, w_std=0.09)
     raise KeyError(name)
 
 
 CASES = ["tiny_config", "rows64_eagle60_ragged_vocab", "rows128_mixed", "rows256_three_tiles",
-         "rows128_five_stages", "rows256_five_stages",
+         "rows128_five_stages", "rows256_five_stages", "rows192_two_tiles", "rows192_one_tile",
          "deep_chain_and_wide", "root_only_requests", "many_tiny_requests",
          "unfused_large_batch", "request_over_lds_stage", "unfused_with_large_request",
          "single_row_single_slab", "vocab_over_one_merge_round"]
