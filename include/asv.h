@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define ASV_VERSION 120          /* 1.2.0 */
+#define ASV_VERSION 130          /* 1.3.0 */
 
 /* Return codes. */
 #define ASV_OK          0
@@ -133,6 +133,10 @@ typedef struct asv_verify_args {
   void *k1_begin_event;           /* optional hipEvent_t recorded just before the LM-head
                                      kernel, or NULL */
   void *k1_end_event;             /* optional hipEvent_t recorded just after it, or NULL */
+  int32_t k1_tile_rows;           /* tree rows per LM-head tile: 0 picks it from N, V and the
+                                     device's compute-unit count; 64, 128, 192 or 256 force
+                                     that tile (tuning and tests; every tile gives the same
+                                     results); any other value: ASV_EINVAL */
 } asv_verify_args;
 
 /* ---- Draft side (Sec. 2, "Draft"): the draft model runs nsteps forwards, every frontier node

@@ -135,13 +135,14 @@ def _need(t, name, dtype, shape):
 
 def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None, state=None,
            params: Optional[AsvParams] = None, out: Optional[VerifyOut] = None,
-           workspace=None, k1_events=None) -> VerifyOut:
+           workspace=None, k1_events=None, k1_tile: int = 0) -> VerifyOut:
     """One verification step through ``asv_verify`` on torch's current stream.
 
     hidden bf16 [N, H]; w_lm bf16 [V, H]; draft_tok, parent int32 [N]; req_offsets int32
     [B+1]; tau float32 [B]; draft_logits float32 [N, V] or None; state u8 [B, 112] (in/out) or
     None. ``out`` and ``workspace`` may be passed to reuse buffers. ``k1_events`` is an
-    optional pair of raw hipEvent_t handles recorded around the LM-head kernel.
+    optional pair of raw hipEvent_t handles recorded around the LM-head kernel. ``k1_tile``
+    forces the LM-head tile (64, 128, 192 or 256 tree rows); 0 lets the library pick it.
     """
     import torch
     N, H = hidden.shape
@@ -179,6 +180,7 @@ def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None,
     a.params = params or make_params()
     if k1_events is not None:
         a.k1_begin_event, a.k1_end_event = k1_events
+    a.k1_tile_rows = k1_tile
     _check(load().asv_verify(ctypes.byref(a), workspace.data_ptr(), workspace.numel(),
                              _stream_handle(dev)))
     return out

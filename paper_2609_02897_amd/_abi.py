@@ -50,7 +50,7 @@ class AsvVerifyArgs(ctypes.Structure):
                 ("accepted_len", _P), ("bonus_token", _P), ("accepted_path", _P),
                 ("draft_conf", _P), ("state", _P), ("req_status", _P),
                 ("params", AsvParams),
-                ("k1_begin_event", _P), ("k1_end_event", _P)]
+                ("k1_begin_event", _P), ("k1_end_event", _P), ("k1_tile_rows", ctypes.c_int32)]
 
 
 class AsvDraftTree(ctypes.Structure):

@@ -3,6 +3,8 @@
 // tree-attention metadata and the commit. Every entry point is declared in include/asv.h.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
+
 #include <cstdio>
 
 #include "asv.h"
@@ -39,21 +41,58 @@ int launch_status(const char* what) {
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
-// Tile families of K1, chosen from the number of tree rows. Few rows (the weight-streaming
-// regime of small batches) use a 64-row tile so that all rows share one pass over W. Between 64
-// and 384 rows the pick is the tile that pads least, and among equal padding the larger tile,
-// which copies fewer bytes per MFMA (interleaved comparisons on MI355X, V = 151936: the 192-row
-// tile is 14% faster than two 128-row tiles at 150-180 rows and 4-7% faster than three at
-// 260-384 rows; at 200 rows the 128- and 256-row tiles tie). Beyond 384 rows, 256x256 tiles.
+// Tile families of K1. Few rows (the weight-streaming regime of small batches) use a 64-row
+// tile so that all rows share one pass over W. Beyond 64 rows the pick minimises an estimate of
+// the launch time: the rounds of workgroups over the CUs times the time of one tile, 60 : 83 :
+// 103 for the 128-, 192- and 256-row tiles (per-tile times of the spread loops on MI355X); ties
+// go to the larger tile. Interleaved comparisons at V = 151936 (records bit-identical across
+// the tiles) agree with the estimate from 150 to 3048 rows: e.g. at 540 rows three 192-row
+// tiles beat three 256-row tiles by 19%, at 700 rows three 256-row tiles beat four 192-row
+// tiles by 7%.
 enum class Tile { kRows64, kRows128, kRows192, kRows256 };
 
-Tile pick_tile(int N) {
+// Compute units of the current device, queried once per device.
+int cu_count() {
+  static std::atomic<int> cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        n <= 0)
+      n = 256;
+    cached[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
+}
+
+Tile pick_tile(int N, int S, int cus) {
   if (N <= 64) return Tile::kRows64;
-  if (N <= 128) return Tile::kRows128;
-  if (N <= 192) return Tile::kRows192;
-  if (N <= 256) return Tile::kRows128;
-  if (N <= 384) return Tile::kRows192;
-  return Tile::kRows256;
+  struct Family { Tile tile; int rows; int cost; };
+  const Family families[3] = {{Tile::kRows128, 128, 60}, {Tile::kRows192, 192, 83},
+                              {Tile::kRows256, 256, 103}};
+  Tile best = Tile::kRows128;
+  int64_t best_est = INT64_MAX;
+  for (const Family& f : families) {
+    const int64_t tiles = (int64_t)((N + f.rows - 1) / f.rows) * S;
+    const int64_t est = (tiles + cus - 1) / cus * f.cost;
+    if (est <= best_est) {
+      best_est = est;
+      best = f.tile;
+    }
+  }
+  return best;
+}
+
+// The tile asv_verify_args.k1_tile_rows asks for; false for a value that names no tile.
+bool forced_tile(int rows, Tile* t) {
+  switch (rows) {
+    case 64: *t = Tile::kRows64; return true;
+    case 128: *t = Tile::kRows128; return true;
+    case 192: *t = Tile::kRows192; return true;
+    case 256: *t = Tile::kRows256; return true;
+    default: return false;
+  }
 }
 
 struct Layout {
@@ -245,6 +284,8 @@ extern "C" int asv_tree_policy(const float* conf, asv_req_state* state, int32_t 
 extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t workspace_bytes,
                           void* stream) {
   if (!a || !sizes_ok(a->B, a->N, a->H, a->V)) return ASV_EINVAL;
+  Tile forced = Tile::kRows64;
+  if (a->k1_tile_rows != 0 && !forced_tile(a->k1_tile_rows, &forced)) return ASV_EINVAL;
   if (a->B == 0) return ASV_OK;
   if (!a->hidden || !a->w_lm || !a->draft_tok || !a->parent || !a->req_offsets || !a->tau ||
       !a->row_max || !a->row_lse || !a->row_argmax || !a->drafted_logit || !a->accept ||
@@ -277,7 +318,8 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
       return ASV_EHIP;
     }
   }
-  switch (pick_tile(a->N)) {
+  const Tile tile = a->k1_tile_rows != 0 ? forced : pick_tile(a->N, L.S, cu_count());
+  switch (tile) {
     // <vocab rows, tree rows, waves along vocab, waves along rows, K per stage, ring depth,
     // K loop>, each the fastest of a sweep on MI355X for its row range. The weight-streaming
     // 64-row tile keeps two workgroups per CU (80 KB of LDS each) with the burst ring; a 3-deep

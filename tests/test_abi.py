@@ -36,7 +36,7 @@ def test_exports(lib):
 
 
 def test_version_and_status(lib):
-    assert lib.asv_version() == 120
+    assert lib.asv_version() == 130
     for code in (0, -1, -2, -3, 7):
         assert lib.asv_status_string(code)
 
@@ -45,7 +45,7 @@ def test_struct_layouts():
     assert ctypes.sizeof(_abi.AsvReqState) == 112
     assert ctypes.sizeof(_abi.AsvParams) == 60
     # 4 ints, 18 pointers, params (60 B, padded to 64), 2 event pointers
-    assert ctypes.sizeof(_abi.AsvVerifyArgs) == 16 + 18 * 8 + 64 + 2 * 8
+    assert ctypes.sizeof(_abi.AsvVerifyArgs) == 16 + 18 * 8 + 64 + 2 * 8 + 8
     assert ctypes.sizeof(_abi.AsvDraftTree) == 64 + 3 * 4 * 256
     # 4 ints, 4 pointers, 3 ints (+4 padding), 8 pointers
     assert ctypes.sizeof(_abi.AsvDraftArgs) == 16 + 4 * 8 + 16 + 8 * 8
@@ -95,10 +95,17 @@ def test_verify_rejects_on_host(lib):
     fake = 0x100000
     for f, _ in _abi.AsvVerifyArgs._fields_[4:]:
         if f not in ("params", "draft_logits", "draft_conf", "state", "k1_begin_event",
-                     "k1_end_event"):
+                     "k1_end_event", "k1_tile_rows"):
             setattr(a, f, fake)
     a.params = asv.make_params()
     assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EWORKSPACE
+    for rows in (64, 128, 192, 256):                # a forced LM-head tile is accepted
+        a.k1_tile_rows = rows
+        assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EWORKSPACE
+    for rows in (-1, 1, 100, 512):                  # a value that names no tile is not
+        a.k1_tile_rows = rows
+        assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
+    a.k1_tile_rows = 0
     a.params = asv.make_params(alpha=0.0)
     assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
     a.params = asv.make_params(breaker_n=0)

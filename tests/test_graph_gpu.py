@@ -61,15 +61,16 @@ def _chain_and_fans(n_req, size):
     return [[-1, 0, 1, 2] + [3] * (size - 4) for _ in range(n_req)]
 
 
-# one tree set per K1 tile family: 20 rows (64-row tile, burst ring), 200 rows (128-row tile,
-# three-slot spread loop), 300 rows (192-row tile) and 520 rows (256-row tile, both two-slot
-# spread loop)
+# one tree set per K1 tile family, the tile pinned: 20 rows (64-row tile, burst ring), 200 rows
+# (128-row tile, three-slot spread loop), 300 rows (192-row tile) and 520 rows (256-row tile,
+# both two-slot spread loop)
 GRAPH_TREES = {
     "rows64": [[-1, 0, 0, 1, 1, 2, 3], [-1, 0, 1], [-1] + [0] * 9],
     "rows128": _chain_and_fans(5, 40),
     "rows192": _chain_and_fans(6, 50),
     "rows256": _chain_and_fans(8, 65),
 }
+GRAPH_TILE = {"rows64": 64, "rows128": 128, "rows192": 192, "rows256": 256}
 
 
 @pytest.mark.parametrize("family", list(GRAPH_TREES))
@@ -92,13 +93,16 @@ def test_verify_graph_replays(asv, dev, family):
     # warm-up on a side stream, as torch requires before capture
     s = torch.cuda.Stream()
     s.wait_stream(torch.cuda.current_stream())
+    tile = GRAPH_TILE[family]
     with torch.cuda.stream(s):
-        asv.verify(hidden, W, tok, par, off, tau, state=state_g, out=out_g, workspace=ws_g)
+        asv.verify(hidden, W, tok, par, off, tau, state=state_g, out=out_g, workspace=ws_g,
+                   k1_tile=tile)
     torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        asv.verify(hidden, W, tok, par, off, tau, state=state_g, out=out_g, workspace=ws_g)
+        asv.verify(hidden, W, tok, par, off, tau, state=state_g, out=out_g, workspace=ws_g,
+                   k1_tile=tile)
     for r in range(4):
         x = np.random.default_rng([9, r]).standard_normal((w.N, w.H)).astype(np.float32)
         hidden.copy_(_bf16((x.view(np.uint32) >> 16).astype(np.uint16), dev))
@@ -109,7 +113,7 @@ def test_verify_graph_replays(asv, dev, family):
         g.replay()
         torch.cuda.synchronize()
         st_e = st0.clone()
-        ref = asv.verify(hidden, W, tok, par, off, tau, state=st_e)
+        ref = asv.verify(hidden, W, tok, par, off, tau, state=st_e, k1_tile=tile)
         torch.cuda.synchronize()
         nonroot = torch.from_numpy(w.parent >= 0).to(dev)
         for f in ref._fields:

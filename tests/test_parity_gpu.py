@@ -33,11 +33,12 @@ def asv():
     return m
 
 
-def _run(asv, w, W, dev, tau=None, state=None, params=None, out=None):
+def _run(asv, w, W, dev, tau=None, state=None, params=None, out=None, k1_tile=0):
     import torch
     d = device_inputs(w, W, dev, tau)
     o = asv.verify(d["hidden"], d["w_lm"], d["draft_tok"], d["parent"], d["req_offsets"],
-                   d["tau"], d["draft_logits"], state=state, params=params, out=out)
+                   d["tau"], d["draft_logits"], state=state, params=params, out=out,
+                   k1_tile=k1_tile)
     torch.cuda.synchronize()
     return to_host(o)
 
@@ -133,6 +134,14 @@ def _case(name):
     raise KeyError(name)
 
 
+# Cases that pin the LM-head tile, so that every tile family and both spread loops run with
+# ragged row tiles and slabs and with one, two, three and five K stages (the other cases take the
+# library's pick, which at these small vocabularies is the 128-row tile).
+CASE_TILE = {"rows128_mixed": 128, "rows128_five_stages": 128, "rows192_one_tile": 192,
+             "rows192_two_tiles": 192, "request_over_lds_stage": 192,
+             "rows256_three_tiles": 256, "rows256_five_stages": 256, "many_tiny_requests": 256,
+             "unfused_large_batch": 256}
+
 CASES = ["tiny_config", "rows64_eagle60_ragged_vocab", "rows128_mixed", "rows256_three_tiles",
          "rows128_five_stages", "rows256_five_stages", "rows192_two_tiles", "rows192_one_tile",
          "deep_chain_and_wide", "root_only_requests", "many_tiny_requests",
@@ -150,7 +159,7 @@ def test_parity_small(asv, dev, name, tau):
     resolve_with_oracle(w, w64)
     taus = None if tau is None else np.full(w.B, tau, dtype=np.float32)
     ref = reference(w, w64, tau=taus)
-    got = _run(asv, w, W, dev, tau=taus)
+    got = _run(asv, w, W, dev, tau=taus, k1_tile=CASE_TILE.get(name, 0))
     rep = compare(w, ref, got)
     print(f"  {rep}", flush=True)
     if tau == 0.0:
@@ -166,11 +175,29 @@ def test_determinism(asv, dev):
     w = _case("rows256_three_tiles")
     W = w.weights()
     resolve_with_oracle(w, oracle.widen_weights(W))
-    a = _run(asv, w, W, dev)
-    b = _run(asv, w, W, dev)
+    a = _run(asv, w, W, dev, k1_tile=256)
+    b = _run(asv, w, W, dev, k1_tile=256)
     for k in a:
         if a[k] is not None:
             assert np.array_equal(a[k], b[k], equal_nan=True), k
+
+
+def test_every_tile_same_results(asv, dev):
+    """Every K1 tile accumulates K in the same order, so the logits and every decision taken
+    from them are the same bit for bit on all four tiles; row_lse may differ in the last bits
+    (the slab records of a row are merged across a different number of waves)."""
+    w = _case("rows192_two_tiles")
+    W = w.weights()
+    resolve_with_oracle(w, oracle.widen_weights(W))
+    runs = {rows: _run(asv, w, W, dev, k1_tile=rows) for rows in (64, 128, 192, 256)}
+    base = runs[64]
+    nonroot = w.parent >= 0
+    for rows, got in runs.items():
+        for k in ("row_max", "row_argmax", "accept", "accepted_len", "accepted_path",
+                  "bonus_token", "draft_conf"):
+            assert np.array_equal(got[k], base[k], equal_nan=True), (rows, k)
+        assert np.array_equal(got["drafted_logit"][nonroot], base["drafted_logit"][nonroot]), rows
+        assert np.allclose(got["row_lse"], base["row_lse"], rtol=1e-6, atol=1e-6), rows
 
 
 @pytest.mark.parametrize("name", ["deep_chain_and_wide", "request_over_lds_stage"])
