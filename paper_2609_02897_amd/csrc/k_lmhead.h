@@ -122,6 +122,83 @@ __device__ __forceinline__ int xcd_tile(int bid, int G) {
   return xcd * q + min(xcd, rem) + loc;
 }
 
+// What every K loop of a tile shares: this wave's place in the tile; one buffer resource per
+// operand covering only the tile's valid rows (rows past V in the last slab or past N in the
+// last row tile read as zeros and never touch memory outside the arrays; their results are
+// discarded by the caller); the source offsets of this wave's stage copies; the LDS addresses
+// of the MFMA fragments. Copy j of a stage region fills rows R j .. R j + R - 1
+// (R = kRowsPerCopy): lane t supplies 16 bytes of row R j + t / CPR at swizzled position
+// t % CPR, i.e. the logical chunk (t % CPR) ^ f(R j + t / CPR).
+template <int TV, int TR, int WV, int WR, int BK, int NST>
+struct TileIo {
+  using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
+  static constexpr int CPR = C::CPR;
+  const uint4* lds;
+  int lane, wave, wv, wr, lds0, frag_row, frag_half;
+  __amdgpu_buffer_rsrc_t w_rsrc, x_rsrc;
+  int w_voff[C::DW], x_voff[C::DX];
+
+  __device__ __forceinline__ TileIo(const uint16_t* X, const uint16_t* W, int N, int H, int V,
+                                    int v0, int r0, const uint4* smem)
+      : lds(smem) {
+    lane = threadIdx.x & 63;
+    wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    wv = wave % WV;
+    wr = wave / WV;
+    frag_row = lane & 31;
+    frag_half = lane >> 5;
+    lds0 = __builtin_amdgcn_readfirstlane((int)(size_t)smem);
+    const int v_end = min(v0 + TV, V);
+    const int r_last = min(r0 + TR, N) - 1;
+    w_rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(W + (size_t)v0 * H),
+                                               (short)0, (v_end - v0) * H * 2, kRsrcWord3);
+    x_rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(X + (size_t)r0 * H),
+                                               (short)0, (r_last + 1 - r0) * H * 2, kRsrcWord3);
+#pragma unroll
+    for (int i = 0; i < C::DW; ++i) w_voff[i] = copy_voff(i * C::kWaves + wave, H);
+#pragma unroll
+    for (int i = 0; i < C::DX; ++i) x_voff[i] = copy_voff(i * C::kWaves + wave, H);
+  }
+  __device__ __forceinline__ int copy_voff(int j, int H) const {
+    const int row = j * C::kRowsPerCopy + lane / CPR;
+    return row * H * 2 + ((lane % CPR) ^ swz_phase<CPR>(row)) * 16;
+  }
+  // copy c of this wave (the W copies first, then the X copies) of K stage ks into ring slot
+  // `slot`
+  template <int c>
+  __device__ __forceinline__ void copy(int slot, int ks) const {
+    const int k2 = ks * BK * 2;
+    const int base = lds0 + slot * C::kStage;
+    if constexpr (c < C::DW)
+      dma16(base + (c * C::kWaves + wave) * 1024, w_voff[c] + k2, w_rsrc);
+    else
+      dma16(base + C::kStageW + ((c - C::DW) * C::kWaves + wave) * 1024, x_voff[c - C::DW] + k2,
+            x_rsrc);
+  }
+  // the fragment of W block i (of this wave's vocabulary rows), or of X block j (of its tree
+  // rows), for K16 step s of ring slot `slot`
+  __device__ __forceinline__ bf16x8 w_frag(int slot, int s, int i) const {
+    const uint4* w = lds + slot * (C::kStage / 16);
+    return __builtin_bit_cast(
+        bf16x8, w[swz<CPR>(wv * C::kWaveV + 32 * i + frag_row, 2 * s + frag_half)]);
+  }
+  __device__ __forceinline__ bf16x8 x_frag(int slot, int s, int j) const {
+    const uint4* x = lds + slot * (C::kStage / 16) + C::kStageW / 16;
+    return __builtin_bit_cast(
+        bf16x8, x[swz<CPR>(wr * C::kWaveR + 32 * j + frag_row, 2 * s + frag_half)]);
+  }
+};
+
+template <int MV, int MR>
+__device__ __forceinline__ void zero_acc(f32x16 (&acc)[MV][MR]) {
+#pragma unroll
+  for (int i = 0; i < MV; ++i)
+#pragma unroll
+    for (int j = 0; j < MR; ++j)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+}
+
 // The logits of one tile, left in the MFMA accumulators: acc[i][j] holds the 32x32 block of
 // vocabulary rows v0 + wv * kWaveV + 32 i .. and tree rows r0 + wr * kWaveR + 32 j .. of this
 // wave, summed over all of H. Rows past V or past N read as zeros. On return every stage copy
@@ -132,69 +209,20 @@ __device__ __forceinline__ void lmhead_tile(
     int v0, int r0, uint4* smem,
     f32x16 (&acc)[LmheadCfg<TV, TR, WV, WR, BK, NST>::MV][LmheadCfg<TV, TR, WV, WR, BK, NST>::MR]) {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
-  constexpr int CPR = C::CPR;
-
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wv = wave % WV, wr = wave / WV;
-  const int v_end = min(v0 + TV, V);
-  const int r_last = min(r0 + TR, N) - 1;
-  const int lds0 = __builtin_amdgcn_readfirstlane((int)(size_t)smem);
-
-  // ---- one buffer resource per operand covering only this tile's valid rows: rows past V
-  // (last slab) or past N (last row tile) read as zeros and never touch memory outside the
-  // arrays; their results are discarded by the caller.
-  const __amdgpu_buffer_rsrc_t w_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(W + (size_t)v0 * H), (short)0, (v_end - v0) * H * 2, kRsrcWord3);
-  const __amdgpu_buffer_rsrc_t x_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(X + (size_t)r0 * H), (short)0, (r_last + 1 - r0) * H * 2,
-      kRsrcWord3);
-  // Copy j of a stage region fills rows R j .. R j + R - 1 (R = kRowsPerCopy); lane t
-  // supplies 16 bytes of row R j + t / CPR at swizzled position t % CPR, i.e. the logical
-  // chunk (t % CPR) ^ f(R j + t / CPR).
-  auto copy_voff = [&](int j) {
-    const int row = j * C::kRowsPerCopy + lane / CPR;
-    return row * H * 2 + ((lane % CPR) ^ swz_phase<CPR>(row)) * 16;
-  };
-  int w_voff[C::DW], x_voff[C::DX];
-#pragma unroll
-  for (int i = 0; i < C::DW; ++i) w_voff[i] = copy_voff(i * C::kWaves + wave);
-#pragma unroll
-  for (int i = 0; i < C::DX; ++i) x_voff[i] = copy_voff(i * C::kWaves + wave);
+  const TileIo<TV, TR, WV, WR, BK, NST> io(X, W, N, H, V, v0, r0, smem);
   const int KT = H / BK;
   auto issue_stage = [&](int ks) {
-    const int k2 = ks * BK * 2;
-    const int base = lds0 + (ks % NST) * C::kStage;
-#pragma unroll
-    for (int i = 0; i < C::DW; ++i)
-      dma16(base + (i * C::kWaves + wave) * 1024, w_voff[i] + k2, w_rsrc);
-#pragma unroll
-    for (int i = 0; i < C::DX; ++i)
-      dma16(base + C::kStageW + (i * C::kWaves + wave) * 1024, x_voff[i] + k2, x_rsrc);
+    static_for<C::kLoads>([&](auto cc) { io.template copy<decltype(cc)::value>(ks % NST, ks); });
   };
+  zero_acc(acc);
 
-#pragma unroll
-  for (int i = 0; i < C::MV; ++i)
-#pragma unroll
-    for (int j = 0; j < C::MR; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-
-  const int frag_row = lane & 31, frag_half = lane >> 5;
-  const uint4* const lds_u4 = smem;
   bf16x8 a0[C::MV], b0[C::MR], a1[C::MV], b1[C::MR];
   // Fragments of K16 step `half` (0 or 1) of the stage in ring slot `slot`.
   auto load_frags = [&](int slot, int half, bf16x8* a, bf16x8* b) {   // half: K16 step
-    const uint4* w = lds_u4 + slot * (C::kStage / 16);
-    const uint4* x = w + C::kStageW / 16;
 #pragma unroll
-    for (int i = 0; i < C::MV; ++i)
-      a[i] = __builtin_bit_cast(
-          bf16x8, w[swz<CPR>(wv * C::kWaveV + 32 * i + frag_row, 2 * half + frag_half)]);
+    for (int i = 0; i < C::MV; ++i) a[i] = io.w_frag(slot, half, i);
 #pragma unroll
-    for (int j = 0; j < C::MR; ++j)
-      b[j] = __builtin_bit_cast(
-          bf16x8, x[swz<CPR>(wr * C::kWaveR + 32 * j + frag_row, 2 * half + frag_half)]);
+    for (int j = 0; j < C::MR; ++j) b[j] = io.x_frag(slot, half, j);
   };
   auto mfmas = [&](const bf16x8* a, const bf16x8* b) {
 #pragma unroll
@@ -286,58 +314,18 @@ __device__ __forceinline__ void lmhead_tile_spread(
     return n;
   }();
 
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wv = wave % WV, wr = wave / WV;
-  const int v_end = min(v0 + TV, V);
-  const int r_last = min(r0 + TR, N) - 1;
-  const int lds0 = __builtin_amdgcn_readfirstlane((int)(size_t)smem);
-  const __amdgpu_buffer_rsrc_t w_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(W + (size_t)v0 * H), (short)0, (v_end - v0) * H * 2, kRsrcWord3);
-  const __amdgpu_buffer_rsrc_t x_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(X + (size_t)r0 * H), (short)0, (r_last + 1 - r0) * H * 2,
-      kRsrcWord3);
-  auto copy_voff = [&](int j) {
-    const int row = j * C::kRowsPerCopy + lane / CPR;
-    return row * H * 2 + ((lane % CPR) ^ swz_phase<CPR>(row)) * 16;
-  };
-  int w_voff[C::DW], x_voff[C::DX];
-#pragma unroll
-  for (int i = 0; i < C::DW; ++i) w_voff[i] = copy_voff(i * C::kWaves + wave);
-#pragma unroll
-  for (int i = 0; i < C::DX; ++i) x_voff[i] = copy_voff(i * C::kWaves + wave);
+  const TileIo<TV, TR, WV, WR, BK, NST> io(X, W, N, H, V, v0, r0, smem);
   const int KT = H / BK;
-  // copy c (W copies first, then X) of K stage ks into ring slot `slot`
   auto issue_copy = [&](int slot, int ks, auto cc) {
-    constexpr int c = decltype(cc)::value;
-    const int k2 = ks * BK * 2;
-    const int base = lds0 + slot * C::kStage;
-    if constexpr (c < C::DW)
-      dma16(base + (c * C::kWaves + wave) * 1024, w_voff[c] + k2, w_rsrc);
-    else
-      dma16(base + C::kStageW + ((c - C::DW) * C::kWaves + wave) * 1024, x_voff[c - C::DW] + k2,
-            x_rsrc);
+    io.template copy<decltype(cc)::value>(slot, ks);
   };
+  zero_acc(acc);
 
-#pragma unroll
-  for (int i = 0; i < MV; ++i)
-#pragma unroll
-    for (int j = 0; j < MR; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-
-  const int frag_row = lane & 31, frag_half = lane >> 5;
   bf16x8 fa[4][MV], fb[4][MR];
   // fragment f (W for f < MV, else X) of K16 step s of ring slot `slot`
   auto read_frag = [&](int slot, int s, int f) {
-    const uint4* w = smem + slot * (C::kStage / 16);
-    const uint4* x = w + C::kStageW / 16;
-    if (f < MV)
-      fa[s][f] = __builtin_bit_cast(
-          bf16x8, w[swz<CPR>(wv * C::kWaveV + 32 * f + frag_row, 2 * s + frag_half)]);
-    else
-      fb[s][f - MV] = __builtin_bit_cast(
-          bf16x8, x[swz<CPR>(wr * C::kWaveR + 32 * (f - MV) + frag_row, 2 * s + frag_half)]);
+    if (f < MV) fa[s][f] = io.w_frag(slot, s, f);
+    else fb[s][f - MV] = io.x_frag(slot, s, f - MV);
   };
 
   // Prologue: stages 0 and 1, wait for stage 0, read its F0 and F1.
@@ -412,57 +400,18 @@ __device__ __forceinline__ void lmhead_tile_spread3(
     return n;
   }();
 
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wv = wave % WV, wr = wave / WV;
-  const int v_end = min(v0 + TV, V);
-  const int r_last = min(r0 + TR, N) - 1;
-  const int lds0 = __builtin_amdgcn_readfirstlane((int)(size_t)smem);
-  const __amdgpu_buffer_rsrc_t w_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(W + (size_t)v0 * H), (short)0, (v_end - v0) * H * 2, kRsrcWord3);
-  const __amdgpu_buffer_rsrc_t x_rsrc = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(X + (size_t)r0 * H), (short)0, (r_last + 1 - r0) * H * 2,
-      kRsrcWord3);
-  auto copy_voff = [&](int j) {
-    const int row = j * C::kRowsPerCopy + lane / CPR;
-    return row * H * 2 + ((lane % CPR) ^ swz_phase<CPR>(row)) * 16;
-  };
-  int w_voff[C::DW], x_voff[C::DX];
-#pragma unroll
-  for (int i = 0; i < C::DW; ++i) w_voff[i] = copy_voff(i * C::kWaves + wave);
-#pragma unroll
-  for (int i = 0; i < C::DX; ++i) x_voff[i] = copy_voff(i * C::kWaves + wave);
+  const TileIo<TV, TR, WV, WR, BK, NST> io(X, W, N, H, V, v0, r0, smem);
   const int KT = H / BK;
-  // copy c (W copies first, then X) of stage j into slot j % 3, from K stage min(j, KT - 1)
+  // copy c of stage j into slot j % 3, from K stage min(j, KT - 1)
   auto issue_copy = [&](int j, auto cc) {
-    constexpr int c = decltype(cc)::value;
-    const int k2 = min(j, KT - 1) * BK * 2;
-    const int base = lds0 + (j % NST) * C::kStage;
-    if constexpr (c < C::DW)
-      dma16(base + (c * C::kWaves + wave) * 1024, w_voff[c] + k2, w_rsrc);
-    else
-      dma16(base + C::kStageW + ((c - C::DW) * C::kWaves + wave) * 1024, x_voff[c - C::DW] + k2,
-            x_rsrc);
+    io.template copy<decltype(cc)::value>(j % NST, min(j, KT - 1));
   };
+  zero_acc(acc);
 
-#pragma unroll
-  for (int i = 0; i < MV; ++i)
-#pragma unroll
-    for (int j = 0; j < MR; ++j)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
-
-  const int frag_row = lane & 31, frag_half = lane >> 5;
   bf16x8 fa[4][MV], fb[4][MR];
   auto read_frag = [&](int slot, int s, int f) {
-    const uint4* w = smem + slot * (C::kStage / 16);
-    const uint4* x = w + C::kStageW / 16;
-    if (f < MV)
-      fa[s][f] = __builtin_bit_cast(
-          bf16x8, w[swz<CPR>(wv * C::kWaveV + 32 * f + frag_row, 2 * s + frag_half)]);
-    else
-      fb[s][f - MV] = __builtin_bit_cast(
-          bf16x8, x[swz<CPR>(wr * C::kWaveR + 32 * (f - MV) + frag_row, 2 * s + frag_half)]);
+    if (f < MV) fa[s][f] = io.w_frag(slot, s, f);
+    else fb[s][f - MV] = io.x_frag(slot, s, f - MV);
   };
 
   // Prologue: stages 0 and 1 and the first n1 copies of stage 2 (what the window of a stage
