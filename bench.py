@@ -130,7 +130,11 @@ def _per_call_us(fn, reps: int) -> float:
     return 1e6 * (time.perf_counter() - t0) / reps
 
 
-def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents, tau=None):
+def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents, tau=None,
+            layout: str = "packed"):
+    """Time asv_verify on configuration `cfg`. With layout "packed" the LM-head weight is
+    packed once (asv_pack_lm_head, as at model load; timed alone as pack_ms) and the row-major
+    copy freed before anything is timed; "row-major" passes the [V, H] weight as it is."""
     import torch
     import paper_2609_02897_amd as asv
     w, c = load_workload(cfg)
@@ -138,6 +142,15 @@ def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents, tau=None):
         w.tau[:] = np.float32(tau)
     W = w.weights()
     d = to_device(w, W, dev)
+    pack_ms = None
+    if layout == "packed":
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        packed = asv.pack_lm_head(d["w_lm"])
+        torch.cuda.synchronize()
+        pack_ms = 1e3 * (time.perf_counter() - t0)
+        d["w_lm"] = packed
+        torch.cuda.empty_cache()
     out = asv.alloc_outputs(w.B, w.N, dev, d["draft_logits"] is not None)
     ws = asv.alloc_workspace(w.B, w.N, w.H, w.V, dev)
     state = asv.state_init(w.B, device=dev)
@@ -186,8 +199,9 @@ def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents, tau=None):
     nodes = w.N * steps
     bytes_alg = 2 * w.V * w.H + 2 * w.N * w.H
     flops_alg = 2 * w.N * w.V * w.H
-    res = dict(cfg=cfg, name=c["name"], N=w.N, B=w.B, H=w.H, V=w.V,
-               tau=float(w.tau[0]), value=nodes / dt, ms_per_step=1e3 * dt / steps,
+    res = dict(cfg=cfg, name=c["name"], N=w.N, B=w.B, H=w.H, V=w.V, layout=layout,
+               pack_ms=pack_ms, tau=float(w.tau[0]), value=nodes / dt,
+               ms_per_step=1e3 * dt / steps,
                k1_avg_ms=k1_avg, k1_min_ms=float(np.min(k1_ms)),
                k1_share=k1_avg * steps / (1e3 * dt),
                hbm_gbs=bytes_alg / (k1_avg * 1e-3) / 1e9,
@@ -488,6 +502,10 @@ def main():
                     help="only time the vendor references on the bench shapes and exit: "
                          "torch.matmul (hipBLASLt) of the logits alone, and a 1 GiB "
                          "device-to-device copy")
+    ap.add_argument("--w-layout", choices=("packed", "row-major"), default="packed",
+                    help="layout of the target LM-head weight in every verify workload: packed "
+                         "once by asv_pack_lm_head before timing (default), or row-major "
+                         "[V, H]; both give bit-identical results")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB five times (the "
                          "reference dispatch for scaling HBM traffic counters) and exit")
@@ -519,7 +537,7 @@ def main():
     asv.load()
     dev = torch.device("cuda:0")
     hip = HipEvents()
-    r, w, W = measure(args.config, args.steps, args.warmup, dev, hip)
+    r, w, W = measure(args.config, args.steps, args.warmup, dev, hip, layout=args.w_layout)
     print(f"# cfg{r['cfg']} {r['name']}: {r['ms_per_step']*1e3:.1f} us/step, "
           f"K1 {r['k1_avg_ms']*1e3:.1f} us, {r['hbm_gbs']:.0f} GB/s, "
           f"{r['mfma_tflops']:.0f} TFLOP/s", file=sys.stderr, flush=True)
@@ -530,13 +548,17 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded bf16 W~N(0,0.02), hidden~N(0,1), EAGLE-style trees)",
         "config": {"workload": r["name"], "H": r["H"], "V": r["V"], "rows": r["N"],
-                   "requests": r["B"], "tau": r["tau"], "parallelism": "single GPU"},
+                   "requests": r["B"], "tau": r["tau"], "w_layout": r["layout"],
+                   "parallelism": "single GPU"},
         "roofline": None,
         "around_target_forward": r["around"],
     }
+    if r["pack_ms"] is not None:
+        line["w_pack_ms_once"] = round(r["pack_ms"], 3)
     if args.secondary != "none" and int(args.secondary) != args.config:
         del w, W
-        r2, _, _ = measure(int(args.secondary), args.steps, args.warmup, dev, hip)
+        r2, _, _ = measure(int(args.secondary), args.steps, args.warmup, dev, hip,
+                           layout=args.w_layout)
         print(f"# cfg{r2['cfg']} {r2['name']}: {r2['ms_per_step']*1e3:.1f} us/step, "
               f"K1 {r2['k1_avg_ms']*1e3:.1f} us, {r2['mfma_tflops']:.0f} TFLOP/s",
               file=sys.stderr, flush=True)
@@ -563,7 +585,8 @@ def main():
         line["other_configs"] = []
         for cfg in (int(x) for x in args.others.split(",")):
             for tau in (CONFIGS[cfg]["taus"] if cfg == 4 else (None,)):
-                ro, _, _ = measure(cfg, args.steps, args.warmup, dev, hip, tau)
+                ro, _, _ = measure(cfg, args.steps, args.warmup, dev, hip, tau,
+                                   layout=args.w_layout)
                 print(f"# cfg{cfg} {ro['name']} tau={ro['tau']:.2f}: "
                       f"{ro['ms_per_step']*1e3:.1f} us/step, K1 {ro['k1_avg_ms']*1e3:.1f} us",
                       file=sys.stderr, flush=True)

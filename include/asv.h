@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define ASV_VERSION 130          /* 1.3.0 */
+#define ASV_VERSION 140          /* 1.4.0 */
 
 /* Return codes. */
 #define ASV_OK          0
@@ -106,7 +106,8 @@ typedef struct asv_verify_args {
   int32_t B, N, H, V;             /* host ints: B >= 0, N >= B (N == 0 iff B == 0),
                                      H > 0 with H % 64 == 0, V > 0 */
   const uint16_t *hidden;         /* [N][H] bf16 final hidden states, 16-byte aligned */
-  const uint16_t *w_lm;           /* [V][H] bf16 LM-head weight, 16-byte aligned */
+  const uint16_t *w_lm;           /* [V][H] bf16 LM-head weight, or its packed copy (see
+                                     w_lm_layout), 16-byte aligned */
   const int32_t  *draft_tok;      /* [N] drafted token ids; root entries ignored */
   const int32_t  *parent;         /* [N] global row id of each node's parent; -1 at roots;
                                      req_offsets[b] <= parent[c] < c inside request b */
@@ -137,7 +138,40 @@ typedef struct asv_verify_args {
                                      device's compute-unit count; 64, 128, 192 or 256 force
                                      that tile (tuning and tests; every tile gives the same
                                      results); any other value: ASV_EINVAL */
+  int32_t w_lm_layout;            /* ASV_W_ROW_MAJOR: w_lm is [V][H] as above.
+                                     ASV_W_PACKED: w_lm is the output of asv_pack_lm_head for
+                                     this V and H. Both give bit-identical results. Any other
+                                     value, or ASV_W_PACKED for sizes asv_packed_lm_head_bytes
+                                     rejects: ASV_EINVAL */
 } asv_verify_args;
+
+/* Layouts of the LM-head weight that asv_verify reads. */
+#define ASV_W_ROW_MAJOR 0
+#define ASV_W_PACKED    1
+
+/* The packed layout: the [V][H] weight cut into S = ceil(V / 256) slabs of 256 vocabulary rows
+ * and K = H / 64 column blocks of 64; block (slab s, columns k) is a [256][64] tile, and the
+ * tiles are stored column block major:
+ *   packed[((k * S + s) * 256 + r) * 64 + c] = w[256 s + r][64 k + c],
+ * zero where 256 s + r >= V. It holds S * 256 * H bf16 values. Each 64-deep step of the
+ * LM-head kernel reads one [256][64] tile per slab, and the slabs advance through K together,
+ * so at every step the whole launch reads one contiguous window instead of 256 runs of 128
+ * bytes per slab, each 2 H bytes apart. The rate of those strided runs depends on where the
+ * weight sits in physical memory; the contiguous window streams at the same rate wherever it
+ * sits. The logits are summed in the same order from the same values. Pack once when the
+ * weights are loaded: the LM-head weight is a constant of the model. */
+
+/* Bytes of the packed copy of a [V][H] LM-head weight. Returns ASV_EINVAL for V <= 0, for an
+ * H that asv_verify would reject, or for a packed copy of 4 GiB or more (S * H / 64 >= 2^17):
+ * pass such weights row-major. */
+int asv_packed_lm_head_bytes(int32_t V, int32_t H, uint64_t *bytes);
+
+/* Write the packed copy of the [V][H] bf16 weight w (16-byte aligned) into `packed`
+ * (16-byte aligned, packed_bytes >= asv_packed_lm_head_bytes(V, H), not overlapping w).
+ * Enqueued on `stream`. Returns ASV_EINVAL for bad sizes, null, misaligned or overlapping
+ * pointers, a packed_bytes too small; ASV_EHIP if the launch fails. */
+int asv_pack_lm_head(const uint16_t *w, int32_t V, int32_t H, uint16_t *packed,
+                     uint64_t packed_bytes, void *stream);
 
 /* ---- Draft side (Sec. 2, "Draft"): the draft model runs nsteps forwards, every frontier node
  * branches topk ways, and the tree is pruned to a verification budget of ndt tokens (ndt counts

@@ -14,8 +14,8 @@ from typing import NamedTuple, Optional
 from ._abi import (  # noqa: F401
     ASV_EHIP, ASV_EINVAL, ASV_EWORKSPACE, ASV_OK, DS_BAD_SHAPE, DS_OVERFLOW, EXPORTS, LIB_PATH,
     POOL_MAX, RS_BAD_OFFSETS, RS_BAD_PARENT, RS_BAD_PATH, RS_BAD_ROOT, RS_BAD_TAU,
-    RS_BAD_TOKEN, RS_MASK_SMALL, TOPK_MAX, AsvCommitArgs, AsvDraftArgs, AsvDraftTree,
-    AsvParams, AsvReqState, AsvVerifyArgs, LibraryMissing, load)
+    RS_BAD_TOKEN, RS_MASK_SMALL, TOPK_MAX, W_PACKED, W_ROW_MAJOR, AsvCommitArgs, AsvDraftArgs,
+    AsvDraftTree, AsvParams, AsvReqState, AsvVerifyArgs, LibraryMissing, load)
 
 STATE_BYTES = ctypes.sizeof(AsvReqState)
 TREE_BYTES = ctypes.sizeof(AsvDraftTree)
@@ -133,23 +133,57 @@ def _need(t, name, dtype, shape):
         raise ValueError(f"{name}: must be contiguous")
 
 
+class PackedLmHead(NamedTuple):
+    """An LM-head weight in the packed layout of ``asv_pack_lm_head``: [256 rows][64 columns]
+    tiles of (vocabulary slab s, column block k), stored at tile index k * S + s with
+    S = ceil(V / 256), zero rows past V."""
+    data: "torch.Tensor"             # bf16, flat, packed_lm_head_bytes(V, H) / 2 values
+    V: int
+    H: int
+
+
+def packed_lm_head_bytes(V: int, H: int) -> int:
+    out = ctypes.c_uint64()
+    _check(load().asv_packed_lm_head_bytes(V, H, ctypes.byref(out)))
+    return out.value
+
+
+def pack_lm_head(w_lm) -> PackedLmHead:
+    """The packed copy of a bf16 [V, H] LM-head weight (``asv_pack_lm_head`` on torch's current
+    stream). ``verify`` takes it in place of the row-major weight, with bit-identical results."""
+    import torch
+    V, H = w_lm.shape
+    _need(w_lm, "w_lm", torch.bfloat16, (V, H))
+    n = packed_lm_head_bytes(V, H)
+    data = torch.empty(n // 2, dtype=torch.bfloat16, device=w_lm.device)
+    _check(load().asv_pack_lm_head(w_lm.data_ptr(), V, H, data.data_ptr(), n,
+                                   _stream_handle(w_lm.device)))
+    return PackedLmHead(data, V, H)
+
+
 def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None, state=None,
            params: Optional[AsvParams] = None, out: Optional[VerifyOut] = None,
            workspace=None, k1_events=None, k1_tile: int = 0) -> VerifyOut:
     """One verification step through ``asv_verify`` on torch's current stream.
 
-    hidden bf16 [N, H]; w_lm bf16 [V, H]; draft_tok, parent int32 [N]; req_offsets int32
-    [B+1]; tau float32 [B]; draft_logits float32 [N, V] or None; state u8 [B, 112] (in/out) or
-    None. ``out`` and ``workspace`` may be passed to reuse buffers. ``k1_events`` is an
+    hidden bf16 [N, H]; w_lm bf16 [V, H] or its ``PackedLmHead``; draft_tok, parent int32 [N];
+    req_offsets int32 [B+1]; tau float32 [B]; draft_logits float32 [N, V] or None; state u8
+    [B, 112] (in/out) or None. ``out`` and ``workspace`` may be passed to reuse buffers. ``k1_events`` is an
     optional pair of raw hipEvent_t handles recorded around the LM-head kernel. ``k1_tile``
     forces the LM-head tile (64, 128, 192 or 256 tree rows); 0 lets the library pick it.
     """
     import torch
     N, H = hidden.shape
-    V = w_lm.shape[0]
+    packed = isinstance(w_lm, PackedLmHead)
+    V = w_lm.V if packed else w_lm.shape[0]
     B = req_offsets.shape[0] - 1
     _need(hidden, "hidden", torch.bfloat16, (N, H))
-    _need(w_lm, "w_lm", torch.bfloat16, (V, H))
+    if packed:
+        if w_lm.H != H:
+            raise ValueError(f"w_lm: packed for H = {w_lm.H}, hidden has H = {H}")
+        _need(w_lm.data, "w_lm.data", torch.bfloat16, (packed_lm_head_bytes(V, H) // 2,))
+    else:
+        _need(w_lm, "w_lm", torch.bfloat16, (V, H))
     _need(draft_tok, "draft_tok", torch.int32, (N,))
     _need(parent, "parent", torch.int32, (N,))
     _need(req_offsets, "req_offsets", torch.int32, (B + 1,))
@@ -165,7 +199,9 @@ def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None,
         workspace = alloc_workspace(B, N, H, V, dev)
     a = AsvVerifyArgs()
     a.B, a.N, a.H, a.V = B, N, H, V
-    a.hidden, a.w_lm = hidden.data_ptr(), w_lm.data_ptr()
+    a.hidden = hidden.data_ptr()
+    a.w_lm = w_lm.data.data_ptr() if packed else w_lm.data_ptr()
+    a.w_lm_layout = W_PACKED if packed else W_ROW_MAJOR
     a.draft_tok, a.parent = draft_tok.data_ptr(), parent.data_ptr()
     a.req_offsets, a.tau = req_offsets.data_ptr(), tau.data_ptr()
     a.draft_logits = _ptr(draft_logits)

@@ -9,6 +9,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libasv.so")
 
 ASV_OK, ASV_EINVAL, ASV_EWORKSPACE, ASV_EHIP = 0, -1, -2, -3
+W_ROW_MAJOR, W_PACKED = 0, 1     # asv_verify_args.w_lm_layout
 RS_BAD_ROOT, RS_BAD_PARENT, RS_BAD_TOKEN, RS_BAD_OFFSETS, RS_BAD_TAU = 1, 2, 4, 16, 32
 RS_MASK_SMALL, RS_BAD_PATH = 64, 128
 DS_BAD_SHAPE, DS_OVERFLOW = 1, 2
@@ -18,7 +19,8 @@ TOPK_MAX, POOL_MAX = 4, 256
 # Every entry point include/asv.h declares.
 EXPORTS = ("asv_version", "asv_status_string", "asv_last_error", "asv_workspace_bytes",
            "asv_tree_policy", "asv_state_init", "asv_verify", "asv_draft_workspace_bytes",
-           "asv_draft_step", "asv_draft_prune", "asv_tree_meta", "asv_commit")
+           "asv_draft_step", "asv_draft_prune", "asv_tree_meta", "asv_commit",
+           "asv_packed_lm_head_bytes", "asv_pack_lm_head")
 
 
 class AsvReqState(ctypes.Structure):
@@ -50,7 +52,8 @@ class AsvVerifyArgs(ctypes.Structure):
                 ("accepted_len", _P), ("bonus_token", _P), ("accepted_path", _P),
                 ("draft_conf", _P), ("state", _P), ("req_status", _P),
                 ("params", AsvParams),
-                ("k1_begin_event", _P), ("k1_end_event", _P), ("k1_tile_rows", ctypes.c_int32)]
+                ("k1_begin_event", _P), ("k1_end_event", _P), ("k1_tile_rows", ctypes.c_int32),
+                ("w_lm_layout", ctypes.c_int32)]
 
 
 class AsvDraftTree(ctypes.Structure):
@@ -132,5 +135,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                   _P, _P, _P, _P]
     lib.asv_commit.restype = ctypes.c_int
     lib.asv_commit.argtypes = [ctypes.POINTER(AsvCommitArgs), _P]
+    lib.asv_packed_lm_head_bytes.restype = ctypes.c_int
+    lib.asv_packed_lm_head_bytes.argtypes = [ctypes.c_int32, ctypes.c_int32,
+                                             ctypes.POINTER(ctypes.c_uint64)]
+    lib.asv_pack_lm_head.restype = ctypes.c_int
+    lib.asv_pack_lm_head.argtypes = [_P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_uint64,
+                                     _P]
     _lib = lib
     return lib

@@ -142,13 +142,25 @@ bool params_ok(const asv_params& p) {
 template <int TV, int TR, int WV, int WR, int BK, int NST, int LOOP = 0>
 void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStream_t s) {
   static_assert(TV == kSlab, "tiles span exactly one record slab");
+  static_assert(TV == kPackRows && BK == kPackDepth, "a stage is one block of the packed layout");
   const int RT = (a->N + TR - 1) / TR;
   const int grid = L.S * RT;
   k_lmhead_partial<TV, TR, WV, WR, BK, NST, LOOP><<<grid, WV * WR * kWave, 0, s>>>(
       a->hidden, a->w_lm, a->parent, a->draft_tok, a->req_offsets, a->B, a->N, a->H, a->V,
       L.S, RT, reinterpret_cast<float*>(ws + L.off_rec_m),
       reinterpret_cast<float*>(ws + L.off_rec_s), reinterpret_cast<int32_t*>(ws + L.off_rec_a),
-      a->drafted_logit, reinterpret_cast<int32_t*>(ws + L.off_cnt), a->B + 1);
+      a->drafted_logit, reinterpret_cast<int32_t*>(ws + L.off_cnt), a->B + 1,
+      a->w_lm_layout == ASV_W_PACKED ? 1 : 0);
+}
+
+// Total bytes of the packed copy of a [V][H] weight; false for sizes asv_verify rejects and
+// for copies of 4 GiB or more (2^17 tiles of 32 KB), past the 32-bit offsets K1 uses in it.
+bool packed_size(int V, int H, uint64_t* bytes) {
+  if (V <= 0 || H <= 0 || H % kPackDepth != 0 || H > (1 << 20)) return false;
+  const uint64_t S = ((uint64_t)V + kPackRows - 1) / kPackRows;
+  if (S * (uint64_t)(H / kPackDepth) >= ((uint64_t)1 << 17)) return false;
+  *bytes = S * kPackRows * (uint64_t)H * 2;
+  return true;
 }
 
 AcceptArgs accept_args(const asv_verify_args* a, const Layout& L, char* ws, bool conf) {
@@ -286,6 +298,10 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
   if (!a || !sizes_ok(a->B, a->N, a->H, a->V)) return ASV_EINVAL;
   Tile forced = Tile::kRows64;
   if (a->k1_tile_rows != 0 && !forced_tile(a->k1_tile_rows, &forced)) return ASV_EINVAL;
+  if (a->w_lm_layout != ASV_W_ROW_MAJOR && a->w_lm_layout != ASV_W_PACKED) return ASV_EINVAL;
+  uint64_t packed_bytes = 0;
+  if (a->w_lm_layout == ASV_W_PACKED && !packed_size(a->V, a->H, &packed_bytes))
+    return ASV_EINVAL;
   if (a->B == 0) return ASV_OK;
   if (!a->hidden || !a->w_lm || !a->draft_tok || !a->parent || !a->req_offsets || !a->tau ||
       !a->row_max || !a->row_lse || !a->row_argmax || !a->drafted_logit || !a->accept ||
@@ -358,6 +374,27 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
   if (int rc = launch_status("k_slab_merge")) return rc;
   k_tree_accept<<<a->B, kWave, 0, s>>>(cnt + a->B, acc);
   return launch_status("k_tree_accept");
+}
+
+extern "C" int asv_packed_lm_head_bytes(int32_t V, int32_t H, uint64_t* bytes) {
+  if (!bytes || !packed_size(V, H, bytes)) return ASV_EINVAL;
+  return ASV_OK;
+}
+
+extern "C" int asv_pack_lm_head(const uint16_t* w, int32_t V, int32_t H, uint16_t* packed,
+                                uint64_t packed_bytes, void* stream) {
+  uint64_t need = 0;
+  if (!packed_size(V, H, &need) || !w || !packed || !aligned16(w) || !aligned16(packed) ||
+      packed_bytes < need)
+    return ASV_EINVAL;
+  const uintptr_t w0 = reinterpret_cast<uintptr_t>(w), p0 = reinterpret_cast<uintptr_t>(packed);
+  if (w0 < p0 + need && p0 < w0 + (uint64_t)V * H * 2) return ASV_EINVAL;   // overlap
+  (void)hipGetLastError();
+  const int S = (V + kPackRows - 1) / kPackRows;
+  const int tiles = (int)((need / 2) / (kPackRows * kPackDepth));
+  k_pack_lm_head<<<tiles, kPackThreads, 0, reinterpret_cast<hipStream_t>(stream)>>>(
+      reinterpret_cast<const uint4*>(w), reinterpret_cast<uint4*>(packed), V, H, S);
+  return launch_status("k_pack_lm_head");
 }
 
 extern "C" int asv_draft_workspace_bytes(int32_t B, int32_t H, int32_t V, uint64_t* bytes) {

@@ -177,7 +177,7 @@ void k_draft_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict_
   const int v0 = slab * TV, r0 = rt * TR;
 
   f32x16 acc[C::MV][C::MR];
-  lmhead_tile<TV, TR, WV, WR, BK, NST>(X, W, R, H, V, v0, r0, smem, acc);
+  lmhead_tile<TV, TR, WV, WR, BK, NST>(X, W, R, H, V, v0, r0, smem, 0, acc);
 
   // Output block (i, j), register e of a lane holds vocabulary row
   //   v0 + wv * kWaveV + 32 i + 8 (e / 4) + 4 (lane / 32) + e % 4   and

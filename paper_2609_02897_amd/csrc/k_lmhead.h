@@ -129,17 +129,23 @@ __device__ __forceinline__ int xcd_tile(int bid, int G) {
 // of the MFMA fragments. Copy j of a stage region fills rows R j .. R j + R - 1
 // (R = kRowsPerCopy): lane t supplies 16 bytes of row R j + t / CPR at swizzled position
 // t % CPR, i.e. the logical chunk (t % CPR) ^ f(R j + t / CPR).
+// W is row-major [V][H], or packed (w_packed != 0, written by k_pack_lm_head for TV = 256,
+// BK = 64): [TV][BK] tiles stored K-block major, tile (slab s, K block k) at element
+// (k S + s) TV BK with S = ceil(V / TV), rows past V zero. A stage of a packed slab is one
+// contiguous tile, and the slabs' tiles of one K block lie side by side. Offsets within the
+// packed buffer are 32-bit unsigned (the host keeps it under 4 GiB).
 template <int TV, int TR, int WV, int WR, int BK, int NST>
 struct TileIo {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
   static constexpr int CPR = C::CPR;
   const uint4* lds;
   int lane, wave, wv, wr, lds0, frag_row, frag_half;
+  unsigned w_kstep;             // bytes between the W data of consecutive K stages
   __amdgpu_buffer_rsrc_t w_rsrc, x_rsrc;
   int w_voff[C::DW], x_voff[C::DX];
 
   __device__ __forceinline__ TileIo(const uint16_t* X, const uint16_t* W, int N, int H, int V,
-                                    int v0, int r0, const uint4* smem)
+                                    int v0, int r0, const uint4* smem, int w_packed)
       : lds(smem) {
     lane = threadIdx.x & 63;
     wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -150,30 +156,41 @@ struct TileIo {
     lds0 = __builtin_amdgcn_readfirstlane((int)(size_t)smem);
     const int v_end = min(v0 + TV, V);
     const int r_last = min(r0 + TR, N) - 1;
-    w_rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(W + (size_t)v0 * H),
-                                               (short)0, (v_end - v0) * H * 2, kRsrcWord3);
+    if (w_packed) {
+      const unsigned S = (V + TV - 1) / TV, tile = TV * BK * 2;
+      w_kstep = S * tile;
+      w_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<uint16_t*>(W + (size_t)v0 * BK), (short)0,
+          (int)((unsigned)(H / BK - 1) * w_kstep + tile), kRsrcWord3);
+    } else {
+      w_kstep = BK * 2;
+      w_rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(W + (size_t)v0 * H),
+                                                 (short)0, (v_end - v0) * H * 2, kRsrcWord3);
+    }
     x_rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(X + (size_t)r0 * H),
                                                (short)0, (r_last + 1 - r0) * H * 2, kRsrcWord3);
 #pragma unroll
-    for (int i = 0; i < C::DW; ++i) w_voff[i] = copy_voff(i * C::kWaves + wave, H);
+    for (int i = 0; i < C::DW; ++i)
+      w_voff[i] = copy_voff(i * C::kWaves + wave, w_packed ? BK : H);
 #pragma unroll
     for (int i = 0; i < C::DX; ++i) x_voff[i] = copy_voff(i * C::kWaves + wave, H);
   }
-  __device__ __forceinline__ int copy_voff(int j, int H) const {
+  // byte offset of this lane's 16 bytes of copy j at K stage 0; `pitch` elements per row
+  __device__ __forceinline__ int copy_voff(int j, int pitch) const {
     const int row = j * C::kRowsPerCopy + lane / CPR;
-    return row * H * 2 + ((lane % CPR) ^ swz_phase<CPR>(row)) * 16;
+    return row * pitch * 2 + ((lane % CPR) ^ swz_phase<CPR>(row)) * 16;
   }
   // copy c of this wave (the W copies first, then the X copies) of K stage ks into ring slot
   // `slot`
   template <int c>
   __device__ __forceinline__ void copy(int slot, int ks) const {
-    const int k2 = ks * BK * 2;
     const int base = lds0 + slot * C::kStage;
     if constexpr (c < C::DW)
-      dma16(base + (c * C::kWaves + wave) * 1024, w_voff[c] + k2, w_rsrc);
+      dma16(base + (c * C::kWaves + wave) * 1024,
+            (int)((unsigned)w_voff[c] + (unsigned)ks * w_kstep), w_rsrc);
     else
-      dma16(base + C::kStageW + ((c - C::DW) * C::kWaves + wave) * 1024, x_voff[c - C::DW] + k2,
-            x_rsrc);
+      dma16(base + C::kStageW + ((c - C::DW) * C::kWaves + wave) * 1024,
+            x_voff[c - C::DW] + ks * BK * 2, x_rsrc);
   }
   // the fragment of W block i (of this wave's vocabulary rows), or of X block j (of its tree
   // rows), for K16 step s of ring slot `slot`
@@ -206,10 +223,10 @@ __device__ __forceinline__ void zero_acc(f32x16 (&acc)[MV][MR]) {
 template <int TV, int TR, int WV, int WR, int BK, int NST>
 __device__ __forceinline__ void lmhead_tile(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int N, int H, int V,
-    int v0, int r0, uint4* smem,
+    int v0, int r0, uint4* smem, int w_packed,
     f32x16 (&acc)[LmheadCfg<TV, TR, WV, WR, BK, NST>::MV][LmheadCfg<TV, TR, WV, WR, BK, NST>::MR]) {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
-  const TileIo<TV, TR, WV, WR, BK, NST> io(X, W, N, H, V, v0, r0, smem);
+  const TileIo<TV, TR, WV, WR, BK, NST> io(X, W, N, H, V, v0, r0, smem, w_packed);
   const int KT = H / BK;
   auto issue_stage = [&](int ks) {
     static_for<C::kLoads>([&](auto cc) { io.template copy<decltype(cc)::value>(ks % NST, ks); });
@@ -291,7 +308,7 @@ __device__ __forceinline__ void wait_lds_barrier() {
 template <int TV, int TR, int WV, int WR>
 __device__ __forceinline__ void lmhead_tile_spread(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int N, int H, int V,
-    int v0, int r0, uint4* smem,
+    int v0, int r0, uint4* smem, int w_packed,
     f32x16 (&acc)[LmheadCfg<TV, TR, WV, WR, 64, 2>::MV][LmheadCfg<TV, TR, WV, WR, 64, 2>::MR]) {
   constexpr int BK = 64, NST = 2;
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
@@ -314,7 +331,7 @@ __device__ __forceinline__ void lmhead_tile_spread(
     return n;
   }();
 
-  const TileIo<TV, TR, WV, WR, BK, NST> io(X, W, N, H, V, v0, r0, smem);
+  const TileIo<TV, TR, WV, WR, BK, NST> io(X, W, N, H, V, v0, r0, smem, w_packed);
   const int KT = H / BK;
   auto issue_copy = [&](int slot, int ks, auto cc) {
     io.template copy<decltype(cc)::value>(slot, ks);
@@ -377,7 +394,7 @@ __device__ __forceinline__ void lmhead_tile_spread(
 template <int TV, int TR, int WV, int WR>
 __device__ __forceinline__ void lmhead_tile_spread3(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int N, int H, int V,
-    int v0, int r0, uint4* smem,
+    int v0, int r0, uint4* smem, int w_packed,
     f32x16 (&acc)[LmheadCfg<TV, TR, WV, WR, 64, 3>::MV][LmheadCfg<TV, TR, WV, WR, 64, 3>::MR]) {
   constexpr int BK = 64, NST = 3;
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
@@ -400,7 +417,7 @@ __device__ __forceinline__ void lmhead_tile_spread3(
     return n;
   }();
 
-  const TileIo<TV, TR, WV, WR, BK, NST> io(X, W, N, H, V, v0, r0, smem);
+  const TileIo<TV, TR, WV, WR, BK, NST> io(X, W, N, H, V, v0, r0, smem, w_packed);
   const int KT = H / BK;
   // copy c of stage j into slot j % 3, from K stage min(j, KT - 1)
   auto issue_copy = [&](int j, auto cc) {
@@ -461,7 +478,7 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
                       const int32_t* __restrict__ req_offsets, int B, int N, int H, int V,
                       int S, int RT, float* __restrict__ rec_m, float* __restrict__ rec_s,
                       int32_t* __restrict__ rec_a, float* __restrict__ drafted_logit,
-                      int32_t* __restrict__ done_cnt, int n_cnt) {
+                      int32_t* __restrict__ done_cnt, int n_cnt, int w_packed) {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
   constexpr int T = C::kThreads;
   __shared__ uint4 smem[C::kLds / 16];
@@ -503,13 +520,13 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
   f32x16 acc[C::MV][C::MR];
   if constexpr (LOOP == 2) {
     static_assert(BK == 64 && NST == 2, "two-slot spread loop: 64-deep stages");
-    lmhead_tile_spread<TV, TR, WV, WR>(X, W, N, H, V, v0, r0, smem, acc);
+    lmhead_tile_spread<TV, TR, WV, WR>(X, W, N, H, V, v0, r0, smem, w_packed, acc);
   } else if constexpr (LOOP == 3) {
     static_assert(BK == 64 && NST == 3, "three-slot spread loop: 64-deep stages");
-    lmhead_tile_spread3<TV, TR, WV, WR>(X, W, N, H, V, v0, r0, smem, acc);
+    lmhead_tile_spread3<TV, TR, WV, WR>(X, W, N, H, V, v0, r0, smem, w_packed, acc);
   } else {
     static_assert(LOOP == 0, "K loop");
-    lmhead_tile<TV, TR, WV, WR, BK, NST>(X, W, N, H, V, v0, r0, smem, acc);
+    lmhead_tile<TV, TR, WV, WR, BK, NST>(X, W, N, H, V, v0, r0, smem, w_packed, acc);
   }
   const int frag_half = lane >> 5;
 
@@ -661,6 +678,28 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
       rec_s[at] = r.s;
       rec_a[at] = r.a;
     }
+  }
+}
+
+// ---- the packed LM-head weight
+// packed[((k S + s) 256 + r) 64 + c] = W[256 s + r][64 k + c], zero where 256 s + r >= V,
+// S = ceil(V / 256). Workgroup b writes tile b = k S + s, 32 KB: thread t stores the 16-byte
+// units t + 256 i (i < 8), i.e. row t / 8 + 32 i, columns 64 k + 8 (t % 8) .. + 7. Stores are
+// contiguous; each group of 8 lanes reads 128 contiguous bytes of one row.
+constexpr int kPackRows = 256, kPackDepth = 64, kPackThreads = 256;
+
+__global__ __launch_bounds__(kPackThreads)
+void k_pack_lm_head(const uint4* __restrict__ W, uint4* __restrict__ P, int V, int H, int S) {
+  const int b = blockIdx.x, s = b % S, k = b / S, t = threadIdx.x;
+  const int row_units = H / 8;                        // 16-byte units per row of W
+  uint4* out = P + (size_t)b * (kPackRows * kPackDepth / 8);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int r = t / 8 + 32 * i;
+    const int v = s * kPackRows + r;
+    uint4 val = make_uint4(0u, 0u, 0u, 0u);
+    if (v < V) val = W[(size_t)v * row_units + k * (kPackDepth / 8) + (t & 7)];
+    out[t + kPackThreads * i] = val;
   }
 }
 

@@ -36,7 +36,7 @@ def test_exports(lib):
 
 
 def test_version_and_status(lib):
-    assert lib.asv_version() == 130
+    assert lib.asv_version() == 140
     for code in (0, -1, -2, -3, 7):
         assert lib.asv_status_string(code)
 
@@ -44,8 +44,8 @@ def test_version_and_status(lib):
 def test_struct_layouts():
     assert ctypes.sizeof(_abi.AsvReqState) == 112
     assert ctypes.sizeof(_abi.AsvParams) == 60
-    # 4 ints, 18 pointers, params (60 B, padded to 64), 2 event pointers
-    assert ctypes.sizeof(_abi.AsvVerifyArgs) == 16 + 18 * 8 + 64 + 2 * 8 + 8
+    # 4 ints, 18 pointers, params (60 B, padded to 64), 2 event pointers, 2 ints
+    assert ctypes.sizeof(_abi.AsvVerifyArgs) == 16 + 18 * 8 + 64 + 2 * 8 + 2 * 4
     assert ctypes.sizeof(_abi.AsvDraftTree) == 64 + 3 * 4 * 256
     # 4 ints, 4 pointers, 3 ints (+4 padding), 8 pointers
     assert ctypes.sizeof(_abi.AsvDraftArgs) == 16 + 4 * 8 + 16 + 8 * 8
@@ -95,7 +95,7 @@ def test_verify_rejects_on_host(lib):
     fake = 0x100000
     for f, _ in _abi.AsvVerifyArgs._fields_[4:]:
         if f not in ("params", "draft_logits", "draft_conf", "state", "k1_begin_event",
-                     "k1_end_event", "k1_tile_rows"):
+                     "k1_end_event", "k1_tile_rows", "w_lm_layout"):
             setattr(a, f, fake)
     a.params = asv.make_params()
     assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EWORKSPACE
@@ -106,6 +106,13 @@ def test_verify_rejects_on_host(lib):
         a.k1_tile_rows = rows
         assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
     a.k1_tile_rows = 0
+    for layout in (asv.W_ROW_MAJOR, asv.W_PACKED):  # both weight layouts are accepted
+        a.w_lm_layout = layout
+        assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EWORKSPACE
+    for layout in (-1, 2, 7):
+        a.w_lm_layout = layout
+        assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
+    a.w_lm_layout = asv.W_ROW_MAJOR
     a.params = asv.make_params(alpha=0.0)
     assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
     a.params = asv.make_params(breaker_n=0)
@@ -124,6 +131,34 @@ def test_verify_rejects_on_host(lib):
                           None) == asv.ASV_EWORKSPACE          # too small
     a.B, a.N = 0, 0                              # empty batch: nothing to do
     assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_OK
+
+
+def test_packed_lm_head_sizes_and_rejections(lib):
+    """The packed weight holds ceil(V / 256) slabs of 256 rows; bad arguments are rejected
+    before anything is enqueued."""
+    out = ctypes.c_uint64(0)
+    for V, H in ((128256, 4096), (151936, 4096), (1, 64), (256, 64), (257, 128)):
+        assert lib.asv_packed_lm_head_bytes(V, H, ctypes.byref(out)) == asv.ASV_OK
+        assert out.value == -(-V // 256) * 256 * H * 2
+    assert lib.asv_packed_lm_head_bytes(128256, 16384, ctypes.byref(out)) == asv.ASV_OK
+    assert out.value == 501 * 256 * 16384 * 2                 # 3.9 GiB: the largest kind
+    for V, H in ((0, 64), (-1, 64), (10, 0), (10, 100), (10, 1 << 21),
+                 (2048 * 256, 4096), (1 << 20, 4096)):      # 4 GiB and more
+        assert lib.asv_packed_lm_head_bytes(V, H, ctypes.byref(out)) == asv.ASV_EINVAL
+    assert lib.asv_packed_lm_head_bytes(10, 64, None) == asv.ASV_EINVAL
+    V, H = 300, 64
+    need = 2 * 256 * H * 2
+    w, p = 0x100000, 0x100000 + (1 << 20)
+    pk = lib.asv_pack_lm_head
+    assert pk(None, V, H, p, need, None) == asv.ASV_EINVAL
+    assert pk(w, V, H, None, need, None) == asv.ASV_EINVAL
+    assert pk(w + 2, V, H, p, need, None) == asv.ASV_EINVAL        # misaligned weight
+    assert pk(w, V, H, p + 8, need, None) == asv.ASV_EINVAL        # misaligned output
+    assert pk(w, V, H, p, need - 1, None) == asv.ASV_EINVAL        # output too small
+    assert pk(w, V, 100, p, need, None) == asv.ASV_EINVAL          # H not a multiple of 64
+    assert pk(w, 0, H, p, need, None) == asv.ASV_EINVAL
+    assert pk(w, V, H, w + V * H * 2 - 16, need, None) == asv.ASV_EINVAL   # overlap
+    assert pk(p + need - 16, V, H, p, need, None) == asv.ASV_EINVAL        # overlap
 
 
 def test_state_init_rejects(lib):

@@ -74,10 +74,11 @@ def _ref(w, tab, step, tau=None, state=None, params=oracle.Params()):
                   w.req_offsets, w.tau if tau is None else tau, w.draft_logits, state, params)
 
 
-def _gpu(asv, w, W, dev, tau=None, state=None):
+def _gpu(asv, w, W, dev, tau=None, state=None, packed=False):
     import torch
     d = device_inputs(w, W, dev, tau)
-    o = asv.verify(d["hidden"], d["w_lm"], d["draft_tok"], d["parent"], d["req_offsets"],
+    w_lm = asv.pack_lm_head(d["w_lm"]) if packed else d["w_lm"]
+    o = asv.verify(d["hidden"], w_lm, d["draft_tok"], d["parent"], d["req_offsets"],
                    d["tau"], d["draft_logits"], state=state)
     torch.cuda.synchronize()
     return to_host(o)
@@ -170,3 +171,20 @@ def test_full_live_sample(asv, dev, cfg):
         for c in kids:
             assert abs(z[i, w.draft_tok[c]] - tab["drafted_logit_s0"][c]) < 1e-9
             assert abs(got["drafted_logit"][c] - z[i, w.draft_tok[c]]) < TOL_F
+
+
+@pytest.mark.parametrize("cfg", [1, 3, 2])
+def test_full_packed_weight(asv, dev, cfg):
+    """The packed LM-head weight at full size: parity with the oracle's tables, and every
+    output bit for bit equal to the row-major weight's."""
+    tab = _table(cfg)
+    w, W = _workload(cfg, 0, tab)
+    got = _gpu(asv, w, W, dev, packed=True)
+    rep = compare(w, _ref(w, tab, 0), got)
+    _report(f"cfg{cfg} packed weight", rep)
+    base = _gpu(asv, w, W, dev)
+    nonroot = w.parent >= 0                 # drafted_logit is unspecified at roots
+    for k, v in base.items():
+        if v is not None:
+            sel = nonroot if k == "drafted_logit" else slice(None)
+            assert np.array_equal(got[k][sel], v[sel], equal_nan=True), k

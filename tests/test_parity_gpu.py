@@ -33,10 +33,11 @@ def asv():
     return m
 
 
-def _run(asv, w, W, dev, tau=None, state=None, params=None, out=None, k1_tile=0):
+def _run(asv, w, W, dev, tau=None, state=None, params=None, out=None, k1_tile=0, packed=False):
     import torch
     d = device_inputs(w, W, dev, tau)
-    o = asv.verify(d["hidden"], d["w_lm"], d["draft_tok"], d["parent"], d["req_offsets"],
+    w_lm = asv.pack_lm_head(d["w_lm"]) if packed else d["w_lm"]
+    o = asv.verify(d["hidden"], w_lm, d["draft_tok"], d["parent"], d["req_offsets"],
                    d["tau"], d["draft_logits"], state=state, params=params, out=out,
                    k1_tile=k1_tile)
     torch.cuda.synchronize()
@@ -198,6 +199,63 @@ def test_every_tile_same_results(asv, dev):
             assert np.array_equal(got[k], base[k], equal_nan=True), (rows, k)
         assert np.array_equal(got["drafted_logit"][nonroot], base["drafted_logit"][nonroot]), rows
         assert np.allclose(got["row_lse"], base["row_lse"], rtol=1e-6, atol=1e-6), rows
+
+
+@pytest.mark.parametrize("V,H", [(1, 64), (256, 64), (1000, 192), (2 * 256 + 77, 320),
+                                 (151936, 4096)])
+def test_pack_layout(asv, dev, V, H):
+    """asv_pack_lm_head writes packed[((k S + s) 256 + r) 64 + c] = w[256 s + r][64 k + c],
+    zero past V: checked against torch's reshape and permute of the zero-padded weight."""
+    import torch
+    print(f"[pack] V={V} H={H}", flush=True)
+    g = torch.Generator(device=dev)
+    g.manual_seed(V * 7919 + H)
+    bits = torch.randint(-32768, 32768, (V, H), dtype=torch.int32, device=dev,
+                         generator=g).to(torch.int16)
+    w = bits.view(torch.bfloat16)
+    p = asv.pack_lm_head(w)
+    torch.cuda.synchronize()
+    S, KT = -(-V // 256), H // 64
+    assert (p.V, p.H) == (V, H) and p.data.numel() == S * 256 * H
+    pad = torch.zeros((S * 256, H), dtype=torch.int16, device=dev)
+    pad[:V] = bits
+    ref = pad.view(S, 256, KT, 64).permute(2, 0, 1, 3).contiguous().view(-1)
+    assert torch.equal(p.data.view(torch.int16), ref)
+
+
+@pytest.mark.parametrize("name", ["rows64_eagle60_ragged_vocab", "rows128_five_stages",
+                                  "rows192_one_tile", "rows256_five_stages",
+                                  "single_row_single_slab", "vocab_over_one_merge_round"])
+def test_packed_weight_same_results(asv, dev, name):
+    """The packed weight feeds the MFMAs the same values in the same K order, so every output
+    is bit for bit the row-major weight's; the packed run also meets the oracle."""
+    w = _case(name)
+    W = w.weights()
+    w64 = oracle.widen_weights(W)
+    resolve_with_oracle(w, w64)
+    tile = CASE_TILE.get(name, 0)
+    got = _run(asv, w, W, dev, k1_tile=tile, packed=True)
+    compare(w, reference(w, w64), got)
+    base = _run(asv, w, W, dev, k1_tile=tile)
+    nonroot = w.parent >= 0                 # drafted_logit is unspecified at roots
+    for k, v in base.items():
+        if v is not None:
+            sel = nonroot if k == "drafted_logit" else slice(None)
+            assert np.array_equal(got[k][sel], v[sel], equal_nan=True), k
+
+
+def test_packed_weight_every_tile(asv, dev):
+    """Packed and row-major weights agree bit for bit on each of the four tile families."""
+    w = _case("rows192_two_tiles")
+    W = w.weights()
+    resolve_with_oracle(w, oracle.widen_weights(W))
+    for rows in (64, 128, 192, 256):
+        got = _run(asv, w, W, dev, k1_tile=rows, packed=True)
+        base = _run(asv, w, W, dev, k1_tile=rows)
+        for k, v in base.items():
+            if v is not None:
+                sel = w.parent >= 0 if k == "drafted_logit" else slice(None)
+                assert np.array_equal(got[k][sel], v[sel], equal_nan=True), (rows, k)
 
 
 @pytest.mark.parametrize("name", ["deep_chain_and_wide", "request_over_lds_stage"])
