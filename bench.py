@@ -221,7 +221,8 @@ def _microbench_lib():
     return lib
 
 
-def measure_draft(name: str, steps: int, warmup: int, dev, hip: HipEvents, cpu: bool) -> dict:
+def measure_draft(name: str, steps: int, warmup: int, dev, hip: HipEvents, cpu: bool,
+                  layout: str = "packed") -> dict:
     """One draft step (asv_draft_step: the draft LM head with its top-4 epilogue, then the slab
     merge and one tree-growth step) on the EAGLE-3-shaped draft head (H=4096, 32000 draft ids),
     trees of the wide end of the paper's range (3,4,4): four draft rows per request.
@@ -240,6 +241,10 @@ def measure_draft(name: str, steps: int, warmup: int, dev, hip: HipEvents, cpu: 
         return torch.from_numpy(np.ascontiguousarray(a)).to(dev)
 
     wd = t(W.view(np.int16)).view(torch.bfloat16)
+    if layout == "packed":          # once, as at model load; the row-major copy is freed
+        wd = asv.pack_draft_head(wd)
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
     xd = t(x.view(np.int16)).view(torch.bfloat16)
     vm = t(vmap)
     B, R = dw.B, 4 * dw.B
@@ -307,6 +312,7 @@ def measure_draft(name: str, steps: int, warmup: int, dev, hip: HipEvents, cpu: 
     bytes_alg = 2 * dw.V * dw.H + 2 * R * dw.H + R * S * 36
     flops_alg = 2 * R * dw.V * dw.H
     res = dict(workload=name, requests=B, rows=R, H=dw.H, V=dw.V, tree_shape=list(shape),
+               w_layout=layout,
                us_per_step=round(1e6 * dt / steps, 2),
                draft_steps_per_s=round(steps / dt, 1),
                prune_us_per_call=round(prune_us, 2),
@@ -503,9 +509,9 @@ def main():
                          "torch.matmul (hipBLASLt) of the logits alone, and a 1 GiB "
                          "device-to-device copy")
     ap.add_argument("--w-layout", choices=("packed", "row-major"), default="packed",
-                    help="layout of the target LM-head weight in every verify workload: packed "
-                         "once by asv_pack_lm_head before timing (default), or row-major "
-                         "[V, H]; both give bit-identical results")
+                    help="layout of the target and draft LM-head weights in every workload: "
+                         "packed once by asv_pack_lm_head / asv_pack_draft_head before timing "
+                         "(default), or row-major [V, H]; both give bit-identical results")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB five times (the "
                          "reference dispatch for scaling HBM traffic counters) and exit")
@@ -598,7 +604,8 @@ def main():
                     "roofline": roofline(ro, ceilings),
                     "roofline_other_bound": other_bound(ro)})
     if not args.no_draft:
-        line["draft"] = [measure_draft(n, args.steps, args.warmup, dev, hip, not args.no_cpu)
+        line["draft"] = [measure_draft(n, args.steps, args.warmup, dev, hip, not args.no_cpu,
+                                       args.w_layout)
                          for n in ("llama31_8b_draft_b1", "llama31_8b_draft_b32")]
         for d in line["draft"]:
             print(f"# draft {d['workload']}: {d['us_per_step']} us/step, K5 cold "

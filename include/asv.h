@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define ASV_VERSION 140          /* 1.4.0 */
+#define ASV_VERSION 150          /* 1.5.0 */
 
 /* Return codes. */
 #define ASV_OK          0
@@ -233,11 +233,27 @@ typedef struct asv_draft_args {
                                      the root row), the confidence Eq. (2) reads */
   void *k_begin_event;            /* optional hipEvent_t recorded around the LM-head kernel */
   void *k_end_event;
+  int32_t w_draft_layout;         /* ASV_W_ROW_MAJOR: w_draft is [V][H] as above.
+                                     ASV_W_PACKED: w_draft is the output of asv_pack_draft_head
+                                     for this V and H. Both give bit-identical results. Any
+                                     other value, or ASV_W_PACKED for sizes
+                                     asv_packed_draft_head_bytes rejects: ASV_EINVAL */
 } asv_draft_args;
 
 /* Workspace asv_draft_step needs (per-vocabulary-slab top-4 records); 256-byte aligned, no
  * initialisation needed. Returns ASV_EINVAL for sizes asv_draft_step would reject. */
 int asv_draft_workspace_bytes(int32_t B, int32_t H, int32_t V, uint64_t *bytes);
+
+/* The packed draft LM-head weight: the same idea as asv_pack_lm_head with [64][64] tiles, since
+ * the draft LM-head kernel reads slabs of 64 or 128 vocabulary rows. With Vp = V rounded up to
+ * a multiple of 128 and T = Vp / 64 tiles per 64-column block:
+ *   packed[((k * T + s) * 64 + r) * 64 + c] = w[64 s + r][64 k + c], zero where 64 s + r >= V.
+ * It holds Vp * H bf16 values. asv_packed_draft_head_bytes returns ASV_EINVAL for sizes
+ * asv_draft_step would reject or a copy of 4 GiB or more; asv_pack_draft_head takes the same
+ * arguments and gives the same errors as asv_pack_lm_head. */
+int asv_packed_draft_head_bytes(int32_t V, int32_t H, uint64_t *bytes);
+int asv_pack_draft_head(const uint16_t *w, int32_t V, int32_t H, uint16_t *packed,
+                        uint64_t packed_bytes, void *stream);
 
 /* One draft step for a batch (Sec. 2, "Draft"): the draft LM head over all 4B rows (bf16 inputs,
  * fp32 accumulation) reduced on the fly to each row's top-4 and log-sum-exp (the [4B][V] logits

@@ -134,31 +134,62 @@ def _need(t, name, dtype, shape):
 
 
 class PackedLmHead(NamedTuple):
-    """An LM-head weight in the packed layout of ``asv_pack_lm_head``: [256 rows][64 columns]
-    tiles of (vocabulary slab s, column block k), stored at tile index k * S + s with
-    S = ceil(V / 256), zero rows past V."""
-    data: "torch.Tensor"             # bf16, flat, packed_lm_head_bytes(V, H) / 2 values
+    """An LM-head weight in a packed tile layout: ``kind`` "target" (``asv_pack_lm_head``,
+    [256 rows][64 columns] tiles, for ``verify``) or "draft" (``asv_pack_draft_head``, [64][64]
+    tiles, for ``draft_step``). Tiles are stored 64-column block major, zero rows past V."""
+    data: "torch.Tensor"             # bf16, flat, packed_*_bytes(V, H) / 2 values
     V: int
     H: int
+    kind: str
 
 
-def packed_lm_head_bytes(V: int, H: int) -> int:
+def packed_lm_head_bytes(V: int, H: int, kind: str = "target") -> int:
     out = ctypes.c_uint64()
-    _check(load().asv_packed_lm_head_bytes(V, H, ctypes.byref(out)))
+    lib = load()
+    f = lib.asv_packed_lm_head_bytes if kind == "target" else lib.asv_packed_draft_head_bytes
+    _check(f(V, H, ctypes.byref(out)))
     return out.value
 
 
-def pack_lm_head(w_lm) -> PackedLmHead:
-    """The packed copy of a bf16 [V, H] LM-head weight (``asv_pack_lm_head`` on torch's current
-    stream). ``verify`` takes it in place of the row-major weight, with bit-identical results."""
+def _pack(w, kind: str) -> PackedLmHead:
     import torch
-    V, H = w_lm.shape
-    _need(w_lm, "w_lm", torch.bfloat16, (V, H))
-    n = packed_lm_head_bytes(V, H)
-    data = torch.empty(n // 2, dtype=torch.bfloat16, device=w_lm.device)
-    _check(load().asv_pack_lm_head(w_lm.data_ptr(), V, H, data.data_ptr(), n,
-                                   _stream_handle(w_lm.device)))
-    return PackedLmHead(data, V, H)
+    V, H = w.shape
+    _need(w, "weight", torch.bfloat16, (V, H))
+    n = packed_lm_head_bytes(V, H, kind)
+    data = torch.empty(n // 2, dtype=torch.bfloat16, device=w.device)
+    lib = load()
+    f = lib.asv_pack_lm_head if kind == "target" else lib.asv_pack_draft_head
+    _check(f(w.data_ptr(), V, H, data.data_ptr(), n, _stream_handle(w.device)))
+    return PackedLmHead(data, V, H, kind)
+
+
+def pack_lm_head(w_lm) -> PackedLmHead:
+    """The packed copy of a bf16 [V, H] target LM-head weight (``asv_pack_lm_head`` on torch's
+    current stream). ``verify`` takes it in place of the row-major weight, with bit-identical
+    results."""
+    return _pack(w_lm, "target")
+
+
+def pack_draft_head(w_draft) -> PackedLmHead:
+    """The packed copy of a bf16 [V, H] draft LM-head weight (``asv_pack_draft_head``).
+    ``draft_step`` takes it in place of the row-major weight, with bit-identical results."""
+    return _pack(w_draft, "draft")
+
+
+def _weight(w, kind: str, name: str, H: int):
+    """(pointer, V, layout) of a row-major [V, H] weight or its packed copy of this kind."""
+    import torch
+    if isinstance(w, PackedLmHead):
+        if w.kind != kind:
+            raise ValueError(f"{name}: packed for the {w.kind} LM head, not the {kind}")
+        if w.H != H:
+            raise ValueError(f"{name}: packed for H = {w.H}, the hidden states have H = {H}")
+        _need(w.data, f"{name}.data", torch.bfloat16,
+              (packed_lm_head_bytes(w.V, H, kind) // 2,))
+        return w.data.data_ptr(), w.V, W_PACKED
+    V = w.shape[0] if isinstance(w, torch.Tensor) and w.dim() == 2 else -1
+    _need(w, name, torch.bfloat16, (V, H))
+    return w.data_ptr(), V, W_ROW_MAJOR
 
 
 def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None, state=None,
@@ -174,16 +205,9 @@ def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None,
     """
     import torch
     N, H = hidden.shape
-    packed = isinstance(w_lm, PackedLmHead)
-    V = w_lm.V if packed else w_lm.shape[0]
     B = req_offsets.shape[0] - 1
     _need(hidden, "hidden", torch.bfloat16, (N, H))
-    if packed:
-        if w_lm.H != H:
-            raise ValueError(f"w_lm: packed for H = {w_lm.H}, hidden has H = {H}")
-        _need(w_lm.data, "w_lm.data", torch.bfloat16, (packed_lm_head_bytes(V, H) // 2,))
-    else:
-        _need(w_lm, "w_lm", torch.bfloat16, (V, H))
+    w_ptr, V, layout = _weight(w_lm, "target", "w_lm", H)
     _need(draft_tok, "draft_tok", torch.int32, (N,))
     _need(parent, "parent", torch.int32, (N,))
     _need(req_offsets, "req_offsets", torch.int32, (B + 1,))
@@ -199,9 +223,7 @@ def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None,
         workspace = alloc_workspace(B, N, H, V, dev)
     a = AsvVerifyArgs()
     a.B, a.N, a.H, a.V = B, N, H, V
-    a.hidden = hidden.data_ptr()
-    a.w_lm = w_lm.data.data_ptr() if packed else w_lm.data_ptr()
-    a.w_lm_layout = W_PACKED if packed else W_ROW_MAJOR
+    a.hidden, a.w_lm, a.w_lm_layout = hidden.data_ptr(), w_ptr, layout
     a.draft_tok, a.parent = draft_tok.data_ptr(), parent.data_ptr()
     a.req_offsets, a.tau = req_offsets.data_ptr(), tau.data_ptr()
     a.draft_logits = _ptr(draft_logits)
@@ -257,18 +279,18 @@ def draft_step(hidden, w_draft, trees, step: int, state=None, shape=None, vocab_
                events=None) -> DraftOut:
     """One draft step through ``asv_draft_step`` on torch's current stream.
 
-    hidden bf16 [4B, H] (row 4b + j = frontier slot j of request b); w_draft bf16 [V, H];
+    hidden bf16 [4B, H] (row 4b + j = frontier slot j of request b); w_draft bf16 [V, H] or its
+    ``PackedLmHead`` from ``pack_draft_head``;
     trees u8 [B, 3136] (in/out); state u8 [B, 112] supplies each tree's shape at step 0, else
     ``shape`` = (nsteps, topk, ndt) for all; vocab_map int32 [V] or None.
     """
     import torch
     R, H = hidden.shape
-    V = w_draft.shape[0]
     B = trees.shape[0]
     if R != TOPK_MAX * B:
         raise ValueError(f"hidden: expected {TOPK_MAX * B} rows (4 per request), got {R}")
     _need(hidden, "hidden", torch.bfloat16, (R, H))
-    _need(w_draft, "w_draft", torch.bfloat16, (V, H))
+    w_ptr, V, layout = _weight(w_draft, "draft", "w_draft", H)
     _need(trees, "trees", torch.uint8, (B, TREE_BYTES))
     if vocab_map is not None:
         _need(vocab_map, "vocab_map", torch.int32, (V,))
@@ -286,7 +308,7 @@ def draft_step(hidden, w_draft, trees, step: int, state=None, shape=None, vocab_
                                 device=dev)
     a = AsvDraftArgs()
     a.B, a.H, a.V, a.step = B, H, V, step
-    a.hidden, a.w_draft = hidden.data_ptr(), w_draft.data_ptr()
+    a.hidden, a.w_draft, a.w_draft_layout = hidden.data_ptr(), w_ptr, layout
     a.vocab_map, a.state = _ptr(vocab_map), _ptr(state)
     a.shape = (ctypes.c_int32 * 3)(*(shape or (1, 1, 1)))
     a.tree = trees.data_ptr()

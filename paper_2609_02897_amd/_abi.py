@@ -20,7 +20,8 @@ TOPK_MAX, POOL_MAX = 4, 256
 EXPORTS = ("asv_version", "asv_status_string", "asv_last_error", "asv_workspace_bytes",
            "asv_tree_policy", "asv_state_init", "asv_verify", "asv_draft_workspace_bytes",
            "asv_draft_step", "asv_draft_prune", "asv_tree_meta", "asv_commit",
-           "asv_packed_lm_head_bytes", "asv_pack_lm_head")
+           "asv_packed_lm_head_bytes", "asv_pack_lm_head", "asv_packed_draft_head_bytes",
+           "asv_pack_draft_head")
 
 
 class AsvReqState(ctypes.Structure):
@@ -70,7 +71,7 @@ class AsvDraftArgs(ctypes.Structure):
                 ("step", ctypes.c_int32), ("hidden", _P), ("w_draft", _P), ("vocab_map", _P),
                 ("state", _P), ("shape", ctypes.c_int32 * 3), ("tree", _P), ("topk_id", _P),
                 ("topk_logp", _P), ("row_lse", _P), ("front_tok", _P), ("draft_conf", _P),
-                ("k_begin_event", _P), ("k_end_event", _P)]
+                ("k_begin_event", _P), ("k_end_event", _P), ("w_draft_layout", ctypes.c_int32)]
 
 
 class AsvCommitArgs(ctypes.Structure):
@@ -135,11 +136,11 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
                                   _P, _P, _P, _P]
     lib.asv_commit.restype = ctypes.c_int
     lib.asv_commit.argtypes = [ctypes.POINTER(AsvCommitArgs), _P]
-    lib.asv_packed_lm_head_bytes.restype = ctypes.c_int
-    lib.asv_packed_lm_head_bytes.argtypes = [ctypes.c_int32, ctypes.c_int32,
-                                             ctypes.POINTER(ctypes.c_uint64)]
-    lib.asv_pack_lm_head.restype = ctypes.c_int
-    lib.asv_pack_lm_head.argtypes = [_P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_uint64,
-                                     _P]
+    for f in (lib.asv_packed_lm_head_bytes, lib.asv_packed_draft_head_bytes):
+        f.restype = ctypes.c_int
+        f.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.POINTER(ctypes.c_uint64)]
+    for f in (lib.asv_pack_lm_head, lib.asv_pack_draft_head):
+        f.restype = ctypes.c_int
+        f.argtypes = [_P, ctypes.c_int32, ctypes.c_int32, _P, ctypes.c_uint64, _P]
     _lib = lib
     return lib

@@ -22,6 +22,8 @@ constexpr size_t kAlign = 256;
 // Vocabulary rows per K1 workgroup tile = width of one record slab; every tile family below
 // uses this width, so the record layout depends only on V.
 constexpr int kSlab = 256;
+constexpr int kPackRowsTarget = 256;   // rows per tile of the packed target LM-head weight
+constexpr int kPackRowsDraft = 64;     // rows per tile of the packed draft LM-head weight
 
 // Text of the most recent failure on this host thread (see asv_last_error).
 thread_local char g_last_error[256] = "";
@@ -142,7 +144,7 @@ bool params_ok(const asv_params& p) {
 template <int TV, int TR, int WV, int WR, int BK, int NST, int LOOP = 0>
 void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStream_t s) {
   static_assert(TV == kSlab, "tiles span exactly one record slab");
-  static_assert(TV == kPackRows && BK == kPackDepth, "a stage is one block of the packed layout");
+  static_assert(TV == kPackRowsTarget && BK == kPackDepth, "a stage is one packed tile");
   const int RT = (a->N + TR - 1) / TR;
   const int grid = L.S * RT;
   k_lmhead_partial<TV, TR, WV, WR, BK, NST, LOOP><<<grid, WV * WR * kWave, 0, s>>>(
@@ -153,14 +155,35 @@ void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStrea
       a->w_lm_layout == ASV_W_PACKED ? 1 : 0);
 }
 
-// Total bytes of the packed copy of a [V][H] weight; false for sizes asv_verify rejects and
-// for copies of 4 GiB or more (2^17 tiles of 32 KB), past the 32-bit offsets K1 uses in it.
-bool packed_size(int V, int H, uint64_t* bytes) {
+// Total bytes of the packed copy of a [V][H] weight whose K blocks hold V rounded up to
+// `align` rows; false for sizes the LM-head kernels reject and for copies of 4 GiB or more,
+// past the 32-bit offsets they use in it.
+bool packed_size(int V, int H, int align, uint64_t* bytes) {
   if (V <= 0 || H <= 0 || H % kPackDepth != 0 || H > (1 << 20)) return false;
-  const uint64_t S = ((uint64_t)V + kPackRows - 1) / kPackRows;
-  if (S * (uint64_t)(H / kPackDepth) >= ((uint64_t)1 << 17)) return false;
-  *bytes = S * kPackRows * (uint64_t)H * 2;
+  const uint64_t Vp = ((uint64_t)V + align - 1) / align * align;
+  const uint64_t total = Vp * (uint64_t)H * 2;
+  if (total >= ((uint64_t)1 << 32)) return false;
+  *bytes = total;
   return true;
+}
+
+// Pack w into tiles of PR rows (k_pack_tiles), after the checks both pack entry points share.
+template <int PR>
+int pack_tiles(const uint16_t* w, int V, int H, uint16_t* packed, uint64_t packed_bytes,
+               void* stream) {
+  constexpr int kAlign = PR > 128 ? PR : 128;
+  uint64_t need = 0;
+  if (!packed_size(V, H, kAlign, &need) || !w || !packed || !aligned16(w) ||
+      !aligned16(packed) || packed_bytes < need)
+    return ASV_EINVAL;
+  const uintptr_t w0 = reinterpret_cast<uintptr_t>(w), p0 = reinterpret_cast<uintptr_t>(packed);
+  if (w0 < p0 + need && p0 < w0 + (uint64_t)V * H * 2) return ASV_EINVAL;   // overlap
+  (void)hipGetLastError();
+  const int T = (int)((need / 2 / H) / PR);        // tiles per 64-column block
+  const int tiles = T * (H / kPackDepth);
+  k_pack_tiles<PR><<<tiles, kPackThreads, 0, reinterpret_cast<hipStream_t>(stream)>>>(
+      reinterpret_cast<const uint4*>(w), reinterpret_cast<uint4*>(packed), V, H, T);
+  return launch_status("k_pack_tiles");
 }
 
 AcceptArgs accept_args(const asv_verify_args* a, const Layout& L, char* ws, bool conf) {
@@ -232,11 +255,13 @@ bool draft_sizes_ok(int B, int H, int V) {
 
 template <int TV, int TR, int WV, int WR, int BK, int NST>
 void launch_draft(const asv_draft_args* a, const DraftLayout& L, char* ws, hipStream_t s) {
+  static_assert(BK == kPackDepth && TV % kPackRowsDraft == 0 && 128 % TV == 0,
+                "a stage is one or two consecutive packed draft tiles");
   const int R = a->B * kTopK;
   const int RT = (R + TR - 1) / TR;
   k_draft_partial<TV, TR, WV, WR, BK, NST><<<L.S * RT, WV * WR * kWave, 0, s>>>(
       a->hidden, a->w_draft, R, a->H, a->V, L.S, RT, reinterpret_cast<uint64_t*>(ws + L.off_k),
-      reinterpret_cast<float*>(ws + L.off_s));
+      reinterpret_cast<float*>(ws + L.off_s), a->w_draft_layout == ASV_W_PACKED ? 1 : 0);
 }
 
 int record_event(void* ev, hipStream_t s, const char* what) {
@@ -300,7 +325,8 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
   if (a->k1_tile_rows != 0 && !forced_tile(a->k1_tile_rows, &forced)) return ASV_EINVAL;
   if (a->w_lm_layout != ASV_W_ROW_MAJOR && a->w_lm_layout != ASV_W_PACKED) return ASV_EINVAL;
   uint64_t packed_bytes = 0;
-  if (a->w_lm_layout == ASV_W_PACKED && !packed_size(a->V, a->H, &packed_bytes))
+  if (a->w_lm_layout == ASV_W_PACKED &&
+      !packed_size(a->V, a->H, kPackRowsTarget, &packed_bytes))
     return ASV_EINVAL;
   if (a->B == 0) return ASV_OK;
   if (!a->hidden || !a->w_lm || !a->draft_tok || !a->parent || !a->req_offsets || !a->tau ||
@@ -377,24 +403,24 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
 }
 
 extern "C" int asv_packed_lm_head_bytes(int32_t V, int32_t H, uint64_t* bytes) {
-  if (!bytes || !packed_size(V, H, bytes)) return ASV_EINVAL;
+  if (!bytes || !packed_size(V, H, kPackRowsTarget, bytes)) return ASV_EINVAL;
   return ASV_OK;
 }
 
 extern "C" int asv_pack_lm_head(const uint16_t* w, int32_t V, int32_t H, uint16_t* packed,
                                 uint64_t packed_bytes, void* stream) {
-  uint64_t need = 0;
-  if (!packed_size(V, H, &need) || !w || !packed || !aligned16(w) || !aligned16(packed) ||
-      packed_bytes < need)
-    return ASV_EINVAL;
-  const uintptr_t w0 = reinterpret_cast<uintptr_t>(w), p0 = reinterpret_cast<uintptr_t>(packed);
-  if (w0 < p0 + need && p0 < w0 + (uint64_t)V * H * 2) return ASV_EINVAL;   // overlap
-  (void)hipGetLastError();
-  const int S = (V + kPackRows - 1) / kPackRows;
-  const int tiles = (int)((need / 2) / (kPackRows * kPackDepth));
-  k_pack_lm_head<<<tiles, kPackThreads, 0, reinterpret_cast<hipStream_t>(stream)>>>(
-      reinterpret_cast<const uint4*>(w), reinterpret_cast<uint4*>(packed), V, H, S);
-  return launch_status("k_pack_lm_head");
+  return pack_tiles<kPackRowsTarget>(w, V, H, packed, packed_bytes, stream);
+}
+
+extern "C" int asv_packed_draft_head_bytes(int32_t V, int32_t H, uint64_t* bytes) {
+  if (!bytes || V < kTopK || !packed_size(V, H, 128, bytes)) return ASV_EINVAL;
+  return ASV_OK;
+}
+
+extern "C" int asv_pack_draft_head(const uint16_t* w, int32_t V, int32_t H, uint16_t* packed,
+                                   uint64_t packed_bytes, void* stream) {
+  if (V < kTopK) return ASV_EINVAL;
+  return pack_tiles<kPackRowsDraft>(w, V, H, packed, packed_bytes, stream);
 }
 
 extern "C" int asv_draft_workspace_bytes(int32_t B, int32_t H, int32_t V, uint64_t* bytes) {
@@ -406,6 +432,11 @@ extern "C" int asv_draft_workspace_bytes(int32_t B, int32_t H, int32_t V, uint64
 extern "C" int asv_draft_step(const asv_draft_args* a, void* workspace, uint64_t workspace_bytes,
                               void* stream) {
   if (!a || !draft_sizes_ok(a->B, a->H, a->V) || a->step < 0) return ASV_EINVAL;
+  if (a->w_draft_layout != ASV_W_ROW_MAJOR && a->w_draft_layout != ASV_W_PACKED)
+    return ASV_EINVAL;
+  uint64_t packed_bytes = 0;
+  if (a->w_draft_layout == ASV_W_PACKED && !packed_size(a->V, a->H, 128, &packed_bytes))
+    return ASV_EINVAL;
   if (a->B == 0) return ASV_OK;
   if (!a->hidden || !a->w_draft || !a->tree || !a->topk_id || !a->topk_logp || !a->row_lse ||
       !a->front_tok)

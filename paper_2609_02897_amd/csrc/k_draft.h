@@ -164,7 +164,7 @@ template <int TV, int TR, int WV, int WR, int BK, int NST>
 __global__ __launch_bounds__(WV * WR * kWave, 1)
 void k_draft_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int R,
                      int H, int V, int S, int RT, uint64_t* __restrict__ rec_k,
-                     float* __restrict__ rec_s) {
+                     float* __restrict__ rec_s, int w_packed) {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
   constexpr int T = C::kThreads;
   __shared__ uint4 smem[C::kLds / 16];
@@ -177,7 +177,7 @@ void k_draft_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict_
   const int v0 = slab * TV, r0 = rt * TR;
 
   f32x16 acc[C::MV][C::MR];
-  lmhead_tile<TV, TR, WV, WR, BK, NST>(X, W, R, H, V, v0, r0, smem, 0, acc);
+  lmhead_tile<TV, TR, WV, WR, BK, NST>(X, W, R, H, V, v0, r0, smem, w_packed, acc);
 
   // Output block (i, j), register e of a lane holds vocabulary row
   //   v0 + wv * kWaveV + 32 i + 8 (e / 4) + 4 (lane / 32) + e % 4   and

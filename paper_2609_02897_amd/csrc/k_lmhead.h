@@ -129,11 +129,11 @@ __device__ __forceinline__ int xcd_tile(int bid, int G) {
 // of the MFMA fragments. Copy j of a stage region fills rows R j .. R j + R - 1
 // (R = kRowsPerCopy): lane t supplies 16 bytes of row R j + t / CPR at swizzled position
 // t % CPR, i.e. the logical chunk (t % CPR) ^ f(R j + t / CPR).
-// W is row-major [V][H], or packed (w_packed != 0, written by k_pack_lm_head for TV = 256,
-// BK = 64): [TV][BK] tiles stored K-block major, tile (slab s, K block k) at element
-// (k S + s) TV BK with S = ceil(V / TV), rows past V zero. A stage of a packed slab is one
-// contiguous tile, and the slabs' tiles of one K block lie side by side. Offsets within the
-// packed buffer are 32-bit unsigned (the host keeps it under 4 GiB).
+// W is row-major [V][H], or packed (w_packed != 0, written by k_pack_tiles with BK = 64):
+// K block k holds rows 0 .. Vp - 1 (V rounded up to max(TV, 128) rows, zero past V) as
+// consecutive [BK]-wide row segments, so the TV rows of slab s at K block k are one contiguous
+// run starting at element k Vp BK + v0 BK. Offsets within the packed buffer are 32-bit
+// unsigned (the host keeps it under 4 GiB).
 template <int TV, int TR, int WV, int WR, int BK, int NST>
 struct TileIo {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
@@ -157,8 +157,9 @@ struct TileIo {
     const int v_end = min(v0 + TV, V);
     const int r_last = min(r0 + TR, N) - 1;
     if (w_packed) {
-      const unsigned S = (V + TV - 1) / TV, tile = TV * BK * 2;
-      w_kstep = S * tile;
+      constexpr unsigned kAlign = TV > 128 ? TV : 128;
+      const unsigned Vp = (V + kAlign - 1) / kAlign * kAlign, tile = TV * BK * 2;
+      w_kstep = Vp * BK * 2;
       w_rsrc = __builtin_amdgcn_make_buffer_rsrc(
           const_cast<uint16_t*>(W + (size_t)v0 * BK), (short)0,
           (int)((unsigned)(H / BK - 1) * w_kstep + tile), kRsrcWord3);
@@ -681,22 +682,25 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
   }
 }
 
-// ---- the packed LM-head weight
-// packed[((k S + s) 256 + r) 64 + c] = W[256 s + r][64 k + c], zero where 256 s + r >= V,
-// S = ceil(V / 256). Workgroup b writes tile b = k S + s, 32 KB: thread t stores the 16-byte
-// units t + 256 i (i < 8), i.e. row t / 8 + 32 i, columns 64 k + 8 (t % 8) .. + 7. Stores are
-// contiguous; each group of 8 lanes reads 128 contiguous bytes of one row.
-constexpr int kPackRows = 256, kPackDepth = 64, kPackThreads = 256;
+// ---- packed weights
+// packed[((k T + s) PR + r) 64 + c] = W[PR s + r][64 k + c], zero where PR s + r >= V, with T
+// tiles of PR rows per 64-column block (T PR = V rounded up to max(PR, 128) rows). Workgroup b
+// writes tile b = k T + s, PR x 128 bytes: thread t stores the 16-byte units t + 256 i, i.e.
+// row t / 8 + 32 i, columns 64 k + 8 (t % 8) .. + 7. Stores are contiguous; each group of 8
+// lanes reads 128 contiguous bytes of one row.
+constexpr int kPackDepth = 64, kPackThreads = 256;
 
+template <int PR>
 __global__ __launch_bounds__(kPackThreads)
-void k_pack_lm_head(const uint4* __restrict__ W, uint4* __restrict__ P, int V, int H, int S) {
-  const int b = blockIdx.x, s = b % S, k = b / S, t = threadIdx.x;
+void k_pack_tiles(const uint4* __restrict__ W, uint4* __restrict__ P, int V, int H, int T) {
+  static_assert(PR % 32 == 0, "whole rows per pass");
+  const int b = blockIdx.x, s = b % T, k = b / T, t = threadIdx.x;
   const int row_units = H / 8;                        // 16-byte units per row of W
-  uint4* out = P + (size_t)b * (kPackRows * kPackDepth / 8);
+  uint4* out = P + (size_t)b * (PR * kPackDepth / 8);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < PR / 32; ++i) {
     const int r = t / 8 + 32 * i;
-    const int v = s * kPackRows + r;
+    const int v = s * PR + r;
     uint4 val = make_uint4(0u, 0u, 0u, 0u);
     if (v < V) val = W[(size_t)v * row_units + k * (kPackDepth / 8) + (t & 7)];
     out[t + kPackThreads * i] = val;

@@ -36,7 +36,7 @@ def test_exports(lib):
 
 
 def test_version_and_status(lib):
-    assert lib.asv_version() == 140
+    assert lib.asv_version() == 150
     for code in (0, -1, -2, -3, 7):
         assert lib.asv_status_string(code)
 
@@ -47,8 +47,8 @@ def test_struct_layouts():
     # 4 ints, 18 pointers, params (60 B, padded to 64), 2 event pointers, 2 ints
     assert ctypes.sizeof(_abi.AsvVerifyArgs) == 16 + 18 * 8 + 64 + 2 * 8 + 2 * 4
     assert ctypes.sizeof(_abi.AsvDraftTree) == 64 + 3 * 4 * 256
-    # 4 ints, 4 pointers, 3 ints (+4 padding), 8 pointers
-    assert ctypes.sizeof(_abi.AsvDraftArgs) == 16 + 4 * 8 + 16 + 8 * 8
+    # 4 ints, 4 pointers, 3 ints (+4 padding), 8 pointers, 1 int (+4 padding)
+    assert ctypes.sizeof(_abi.AsvDraftArgs) == 16 + 4 * 8 + 16 + 8 * 8 + 8
     # 2 ints, 10 pointers, an int64, a pointer
     assert ctypes.sizeof(_abi.AsvCommitArgs) == 8 + 10 * 8 + 8 + 8
 
@@ -159,6 +159,34 @@ def test_packed_lm_head_sizes_and_rejections(lib):
     assert pk(w, 0, H, p, need, None) == asv.ASV_EINVAL
     assert pk(w, V, H, w + V * H * 2 - 16, need, None) == asv.ASV_EINVAL   # overlap
     assert pk(p + need - 16, V, H, p, need, None) == asv.ASV_EINVAL        # overlap
+
+
+def test_packed_draft_head_sizes_and_rejections(lib):
+    """The packed draft weight holds V rounded up to a multiple of 128 rows; bad arguments and
+    bad layouts are rejected before anything is enqueued."""
+    out = ctypes.c_uint64(0)
+    for V, H in ((32000, 4096), (4, 64), (128, 64), (129, 128), (777, 128)):
+        assert lib.asv_packed_draft_head_bytes(V, H, ctypes.byref(out)) == asv.ASV_OK
+        assert out.value == -(-V // 128) * 128 * H * 2
+    for V, H in ((3, 64), (0, 64), (10, 100), (1 << 19, 4096)):
+        assert lib.asv_packed_draft_head_bytes(V, H, ctypes.byref(out)) == asv.ASV_EINVAL
+    V, H = 300, 64
+    need = 384 * H * 2
+    w, p = 0x100000, 0x100000 + (1 << 20)
+    pk = lib.asv_pack_draft_head
+    assert pk(None, V, H, p, need, None) == asv.ASV_EINVAL
+    assert pk(w, V, H, p, need - 1, None) == asv.ASV_EINVAL
+    assert pk(w, 3, H, p, need, None) == asv.ASV_EINVAL
+    assert pk(w, V, H, w + 64, need, None) == asv.ASV_EINVAL              # overlap
+    a = _abi.AsvDraftArgs()
+    a.B, a.H, a.V = 1, 64, 300
+    for layout in (-1, 2):
+        a.w_draft_layout = layout
+        assert lib.asv_draft_step(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
+    a.B = 0                                   # an empty batch with a valid layout is a no-op
+    for layout in (asv.W_ROW_MAJOR, asv.W_PACKED):
+        a.w_draft_layout = layout
+        assert lib.asv_draft_step(ctypes.byref(a), None, 0, None) == asv.ASV_OK
 
 
 def test_state_init_rejects(lib):

@@ -136,6 +136,48 @@ def test_draft_topk_exact_ties_and_nan(asv, dev):
         assert abs(logp[r, 0] - (64.0 - lse[r])) < 1e-5
 
 
+@pytest.mark.parametrize("B,V,H", [(1, 1000, 256), (9, 1000, 256), (17, 1000, 256),
+                                   (40, 777, 128), (2, 4, 64), (32, 32000, 4096)])
+def test_draft_packed_weight(asv, dev, B, V, H):
+    """asv_pack_draft_head writes packed[((k T + s) 64 + r) 64 + c] = w[64 s + r][64 k + c]
+    (64 T = V rounded up to a multiple of 128, zero rows past V), checked against torch's
+    reshape and permute; draft_step then gives every output and tree bit for bit as with the
+    row-major weight, on every draft tile family (4, 36, 68 and 160 rows)."""
+    import torch
+    print(f"case B={B} V={V} H={H}", flush=True)
+    W = bf16_weights(V, H, 0.5, 13)
+    x = draft_hidden(B, H, 0, seed=V + 1)
+    w = _bf16(W, dev)
+    p = asv.pack_draft_head(w)
+    torch.cuda.synchronize()
+    Vp, KT = -(-V // 128) * 128, H // 64
+    assert p.kind == "draft" and p.data.numel() == Vp * H
+    pad = torch.zeros((Vp, H), dtype=torch.int16, device=dev)
+    pad[:V] = w.view(torch.int16)
+    ref = pad.view(Vp // 64, 64, KT, 64).permute(2, 0, 1, 3).contiguous().view(-1)
+    assert torch.equal(p.data.view(torch.int16), ref)
+    runs = []
+    for weight in (w, p):
+        trees = asv.alloc_draft_trees(B, dev)
+        out = asv.draft_step(_bf16(x, dev), weight, trees, 0, shape=(3, 4, 4), with_conf=True)
+        torch.cuda.synchronize()
+        runs.append((out, trees))
+    (o0, t0), (o1, t1) = runs
+    for f in o0._fields:
+        assert torch.equal(getattr(o0, f), getattr(o1, f)), f
+    for g0, g1 in zip(asv.draft_tree_fields(t0), asv.draft_tree_fields(t1)):
+        n, F = g0.n_pool, g0.n_front            # pool entries past n_pool are never written
+        assert (g0.nsteps, g0.topk, g0.ndt, g0.steps, g0.status, F, n) == \
+               (g1.nsteps, g1.topk, g1.ndt, g1.steps, g1.status, g1.n_front, g1.n_pool)
+        assert list(g0.front[:F]) == list(g1.front[:F])
+        assert list(g0.front_score[:F]) == list(g1.front_score[:F])
+        assert (list(g0.tok[:n]), list(g0.par[:n]), list(g0.score[:n])) == \
+               (list(g1.tok[:n]), list(g1.par[:n]), list(g1.score[:n]))
+    with pytest.raises(ValueError):
+        asv.draft_step(_bf16(x, dev), asv.pack_lm_head(w), asv.alloc_draft_trees(B, dev), 0,
+                       shape=(3, 4, 4))
+
+
 # ----------------------------------------------------------------------------- tree growth
 
 def _oracle_step(trees_ref, ids, logp):
