@@ -216,8 +216,9 @@ def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents, tau=None,
 
 def _microbench_lib():
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_02897_amd", "libasv_microbench.so"))
-    lib.asvb_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p,
-                                     ctypes.c_int32, ctypes.c_void_p]
+    for f in (lib.asvb_stream_read, lib.asvb_stream_read_nt):
+        f.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_int32,
+                      ctypes.c_void_p]
     return lib
 
 
@@ -280,19 +281,20 @@ def measure_draft(name: str, steps: int, warmup: int, dev, hip: HipEvents, cpu: 
         step(i, evs[i])
     torch.cuda.synchronize()
     k_ms = [hip.elapsed_ms(a, b) for a, b in evs]
-    # the achievable ceiling for this launch: a plain streaming read of the same number of
-    # bytes after the same flush, best of two grid sizes
+    # the achievable ceiling for this launch: a streaming read of the same number of bytes
+    # after the same flush, best of the plain and the non-temporal read at two grid sizes
     n_rd = (2 * dw.V * dw.H) // 16 * 16
     rd = torch.ones(n_rd // 4, dtype=torch.int32, device=dev)
     rd_ms = []
-    for grid in (1024, 2048):
+    for read, grid in ((mb.asvb_stream_read, 1024), (mb.asvb_stream_read, 2048),
+                       (mb.asvb_stream_read_nt, 512), (mb.asvb_stream_read_nt, 1024)):
         t_ms = []
         for i in range(20):
             assert mb.asvb_stream_read(flush.data_ptr(), 1 << 30, sink.data_ptr(), 1024,
                                        handle) == 0
             a, b = evs[i]
             hip.record(a, handle)
-            assert mb.asvb_stream_read(rd.data_ptr(), n_rd, sink.data_ptr(), grid, handle) == 0
+            assert read(rd.data_ptr(), n_rd, sink.data_ptr(), grid, handle) == 0
             hip.record(b, handle)
             torch.cuda.synchronize()
             t_ms.append(hip.elapsed_ms(a, b))
@@ -418,14 +420,15 @@ def cpu_baseline(w, W, budget_s: float = 12.0) -> dict:
 
 def measured_ceilings(dev) -> dict:
     """Achievable peaks on this GPU from the microbenchmark library (include/asv_microbench.h):
-    a streaming read of 2 GiB (larger than the 256 MB last-level cache), best of two grid
-    sizes, and a register-only bf16 MFMA loop on every SIMD. Timed with HIP events on the
-    stream the kernels are launched on."""
+    a streaming read of 2 GiB (larger than the 256 MB last-level cache), the best of the plain
+    and the non-temporal read at two grid sizes each, and a register-only bf16 MFMA loop on
+    every SIMD. Timed with HIP events on the stream the kernels are launched on."""
     import torch
     torch.cuda.init()
     lib = ctypes.CDLL(os.path.join(ROOT, "paper_2609_02897_amd", "libasv_microbench.so"))
-    lib.asvb_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p,
-                                     ctypes.c_int32, ctypes.c_void_p]
+    for f in (lib.asvb_stream_read, lib.asvb_stream_read_nt):
+        f.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_int32,
+                      ctypes.c_void_p]
     lib.asvb_mfma_loop.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                    ctypes.c_void_p]
     stream = torch.cuda.current_stream(dev)
@@ -446,9 +449,9 @@ def measured_ceilings(dev) -> dict:
     buf = torch.full((nbytes // 4,), 0x01020304, dtype=torch.int32, device=dev)
     sink = torch.zeros(1 << 16, dtype=torch.int32, device=dev)
     best = 0.0
-    for grid in (1024, 2048):
-        sec = timed(lambda: lib.asvb_stream_read(buf.data_ptr(), nbytes, sink.data_ptr(),
-                                                 grid, handle), 10)
+    for read, grid in ((lib.asvb_stream_read, 1024), (lib.asvb_stream_read, 2048),
+                       (lib.asvb_stream_read_nt, 512), (lib.asvb_stream_read_nt, 1024)):
+        sec = timed(lambda: read(buf.data_ptr(), nbytes, sink.data_ptr(), grid, handle), 10)
         best = max(best, nbytes / sec / 1e9)
     del buf
     grid, iters = 256, 16384

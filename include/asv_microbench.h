@@ -21,6 +21,13 @@ extern "C" {
 int asvb_stream_read(const void *buf, uint64_t bytes, uint32_t *sink, int32_t grid,
                      void *stream);
 
+/* The same read with the non-temporal hint on every load, interleaved across workgroups
+ * (round k of workgroup g reads 16-byte words (k grid + g) 1024 .. + 1023): the fastest plain
+ * read of HBM measured on this GPU. Unlike asvb_stream_read it does not fill the caches, so it
+ * is no cache flush. Same arguments and checks. */
+int asvb_stream_read_nt(const void *buf, uint64_t bytes, uint32_t *sink, int32_t grid,
+                        void *stream);
+
 /* Dense bf16 MFMA loop: `grid` workgroups of 256 threads; each wave runs `iters` rounds of
  * eight independent v_mfma_f32_32x32x16_bf16 on register operands (no memory traffic) and
  * writes one float per lane to sink[(workgroup * 256) + thread] at the end.

@@ -66,6 +66,14 @@ __device__ __forceinline__ void dma16(int lds, int voff, __amdgpu_buffer_rsrc_t 
                : "s"(lds), "v"(voff), "s"(r)
                : "memory", "m0");
 }
+// The same copy with the non-temporal hint (nt): for data read once and streamed, which the
+// caches should not try to keep.
+__device__ __forceinline__ void dma16_stream(int lds, int voff, __amdgpu_buffer_rsrc_t r) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen nt lds"
+               :
+               : "s"(lds), "v"(voff), "s"(r)
+               : "memory", "m0");
+}
 #pragma clang diagnostic pop
 
 // Wait until at most N vector-memory operations of this wave are outstanding and its LDS
@@ -138,6 +146,11 @@ template <int TV, int TR, int WV, int WR, int BK, int NST>
 struct TileIo {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
   static constexpr int CPR = C::CPR;
+  // Tiles of up to 128 rows stream W: their launches are weight-bound or close to it, and
+  // copies with the non-temporal hint read W faster (60 rows: 13% less time). The larger
+  // tiles share each W slab between the row tiles of one XCD through its L2 and keep the
+  // default policy (the hint measured within noise there).
+  static constexpr bool kStreamW = TR <= 128;
   const uint4* lds;
   int lane, wave, wv, wr, lds0, frag_row, frag_half;
   unsigned w_kstep;             // bytes between the W data of consecutive K stages
@@ -186,9 +199,14 @@ struct TileIo {
   template <int c>
   __device__ __forceinline__ void copy(int slot, int ks) const {
     const int base = lds0 + slot * C::kStage;
-    if constexpr (c < C::DW)
-      dma16(base + (c * C::kWaves + wave) * 1024,
-            (int)((unsigned)w_voff[c] + (unsigned)ks * w_kstep), w_rsrc);
+    if constexpr (c < C::DW) {
+      const int lds_at = base + (c * C::kWaves + wave) * 1024;
+      const int at = (int)((unsigned)w_voff[c] + (unsigned)ks * w_kstep);
+      if constexpr (kStreamW)
+        dma16_stream(lds_at, at, w_rsrc);
+      else
+        dma16(lds_at, at, w_rsrc);
+    }
     else
       dma16(base + C::kStageW + ((c - C::DW) * C::kWaves + wave) * 1024,
             x_voff[c - C::DW] + ks * BK * 2, x_rsrc);

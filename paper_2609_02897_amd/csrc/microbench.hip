@@ -28,6 +28,29 @@ __global__ __launch_bounds__(kThreads) void k_stream_read(const uint4* __restric
   if (acc == 0x9e3779b9u) sink[blockIdx.x] = acc;
 }
 
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+constexpr int kUnrollNt = 4;
+
+// Interleaved read with the non-temporal hint: round k of workgroup g reads the 16-byte words
+// (k grid + g) 1024 + u 256 + t, u < 4 (t = thread).
+__global__ __launch_bounds__(kThreads) void k_stream_read_nt(const u32x4* __restrict__ p,
+                                                              size_t n16,
+                                                              uint32_t* __restrict__ sink) {
+  uint32_t acc = 0;
+  const size_t step = (size_t)gridDim.x * kThreads * kUnrollNt;
+  for (size_t i = blockIdx.x * (size_t)kThreads * kUnrollNt + threadIdx.x; i < n16; i += step) {
+    u32x4 v[kUnrollNt];
+#pragma unroll
+    for (int u = 0; u < kUnrollNt; ++u) {
+      const size_t j = i + (size_t)u * kThreads;
+      v[u] = j < n16 ? __builtin_nontemporal_load(p + j) : u32x4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int u = 0; u < kUnrollNt; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  if (acc == 0x9e3779b9u) sink[blockIdx.x] = acc;
+}
+
 typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
 
@@ -67,6 +90,17 @@ extern "C" int asvb_stream_read(const void* buf, uint64_t bytes, uint32_t* sink,
   (void)hipGetLastError();
   k_stream_read<<<grid, kThreads, 0, reinterpret_cast<hipStream_t>(stream)>>>(
       static_cast<const uint4*>(buf), n16, per, sink);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+extern "C" int asvb_stream_read_nt(const void* buf, uint64_t bytes, uint32_t* sink,
+                                   int32_t grid, void* stream) {
+  if (!buf || !sink || grid < 1 || bytes == 0 || bytes % 16 != 0 ||
+      (reinterpret_cast<uintptr_t>(buf) & 15u) != 0)
+    return -1;
+  (void)hipGetLastError();
+  k_stream_read_nt<<<grid, kThreads, 0, reinterpret_cast<hipStream_t>(stream)>>>(
+      static_cast<const u32x4*>(buf), bytes / 16, sink);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }
 

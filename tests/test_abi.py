@@ -205,11 +205,12 @@ def test_microbench_library_exports_and_checks():
     src = open(os.path.join(ROOT, "include", "asv_microbench.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     names = sorted(set(re.findall(r"\b(asvb_[a-z_]+)\s*\(", src)))
-    assert names == ["asvb_mfma_loop", "asvb_stream_read"]
+    assert names == ["asvb_mfma_loop", "asvb_stream_read", "asvb_stream_read_nt"]
     for n in names:
         assert hasattr(mb, n), n
-    mb.asvb_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p,
-                                    ctypes.c_int32, ctypes.c_void_p]
+    for f in (mb.asvb_stream_read, mb.asvb_stream_read_nt):
+        f.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_void_p, ctypes.c_int32,
+                      ctypes.c_void_p]
     mb.asvb_mfma_loop.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_int32,
                                   ctypes.c_void_p]
     p = ctypes.c_void_p(0x1000)
@@ -217,6 +218,9 @@ def test_microbench_library_exports_and_checks():
     assert mb.asvb_stream_read(p, 65, p, 4, None) == -1           # not a multiple of 16
     assert mb.asvb_stream_read(ctypes.c_void_p(0x1004), 64, p, 4, None) == -1
     assert mb.asvb_stream_read(p, 64, p, 0, None) == -1
+    for bad in ((None, 64, p, 4), (p, 65, p, 4), (ctypes.c_void_p(0x1004), 64, p, 4),
+                (p, 64, p, 0), (p, 64, None, 4)):
+        assert mb.asvb_stream_read_nt(*bad, None) == -1
     assert mb.asvb_mfma_loop(None, 4, 4, None) == -1
     assert mb.asvb_mfma_loop(p, 0, 4, None) == -1
 
