@@ -73,15 +73,19 @@ GRAPH_TREES = {
 GRAPH_TILE = {"rows64": 64, "rows128": 128, "rows192": 192, "rows256": 256}
 
 
+@pytest.mark.parametrize("packed", [False, True])
 @pytest.mark.parametrize("family", list(GRAPH_TREES))
-def test_verify_graph_replays(asv, dev, family):
+def test_verify_graph_replays(asv, dev, family, packed):
+    """The graph is captured on the row-major or the packed weight; every replay is compared
+    with an eager call on the row-major weight."""
     import torch
-    print(f"[graph] verify {family}", flush=True)
+    print(f"[graph] verify {family} packed={packed}", flush=True)
     trees = GRAPH_TREES[family]
     w = custom_workload("graph", 256, 3000, trees, 0.2, seed=41, w_std=0.1)
     rng = np.random.default_rng(5)
     w.draft_tok = rng.integers(0, 3000, w.N).astype(np.int32)
     W = _bf16(w.weights(), dev)
+    Wg = asv.pack_lm_head(W) if packed else W
     hidden = _bf16(w.hidden, dev)
     tok = torch.from_numpy(w.draft_tok).to(dev)
     par = torch.from_numpy(w.parent.astype(np.int32)).to(dev)
@@ -95,13 +99,13 @@ def test_verify_graph_replays(asv, dev, family):
     s.wait_stream(torch.cuda.current_stream())
     tile = GRAPH_TILE[family]
     with torch.cuda.stream(s):
-        asv.verify(hidden, W, tok, par, off, tau, state=state_g, out=out_g, workspace=ws_g,
+        asv.verify(hidden, Wg, tok, par, off, tau, state=state_g, out=out_g, workspace=ws_g,
                    k1_tile=tile)
     torch.cuda.current_stream().wait_stream(s)
     torch.cuda.synchronize()
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
-        asv.verify(hidden, W, tok, par, off, tau, state=state_g, out=out_g, workspace=ws_g,
+        asv.verify(hidden, Wg, tok, par, off, tau, state=state_g, out=out_g, workspace=ws_g,
                    k1_tile=tile)
     for r in range(4):
         x = np.random.default_rng([9, r]).standard_normal((w.N, w.H)).astype(np.float32)
@@ -124,14 +128,19 @@ def test_verify_graph_replays(asv, dev, family):
         assert torch.equal(st_e, state_g), r
 
 
-def test_draft_phase_graph_replays(asv, dev):
+@pytest.mark.parametrize("packed", [False, True])
+def test_draft_phase_graph_replays(asv, dev, packed):
+    """Captured on the row-major or the packed draft weight; every replay is compared with
+    eager calls on the row-major weight."""
     import torch
+    print(f"[graph] draft phase packed={packed}", flush=True)
     B, H, V = 3, 128, 700
     Wd = _bf16(bf16_weights(V, H, 0.5, 42), dev)
+    Wg = asv.pack_draft_head(Wd) if packed else Wd
     xs = [_bf16(draft_hidden(B, H, k, seed=11), dev) for k in range(3)]
     trees_g = asv.alloc_draft_trees(B, dev)
     ws = torch.empty(asv.draft_workspace_bytes(B, H, V), dtype=torch.uint8, device=dev)
-    outs = [asv.draft_step(xs[k], Wd, trees_g, k, shape=(3, 3, 7), workspace=ws)
+    outs = [asv.draft_step(xs[k], Wg, trees_g, k, shape=(3, 3, 7), workspace=ws)
             for k in range(3)]
     n_cap = B * 7
     par_g = torch.empty(n_cap, dtype=torch.int32, device=dev)
@@ -146,7 +155,7 @@ def test_draft_phase_graph_replays(asv, dev):
 
     def phase():
         for k in range(3):
-            asv.draft_step(xs[k], Wd, trees_g, k, shape=(3, 3, 7), out=outs[k], workspace=ws)
+            asv.draft_step(xs[k], Wg, trees_g, k, shape=(3, 3, 7), out=outs[k], workspace=ws)
         prune()
 
     s = torch.cuda.Stream()
