@@ -491,7 +491,7 @@ extern "C" int asv_draft_prune(const asv_draft_tree* tree, int32_t B, const int3
   if (!tree || !parent || !draft_tok || !req_offsets || !req_status) return ASV_EINVAL;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   (void)hipGetLastError();
-  k_draft_prune<<<B, kPruneThreads, 0, s>>>(tree, B, root_tok, n_cap, parent, draft_tok,
+  k_draft_prune<<<B, kPruneThreads, 0, s>>>(tree, root_tok, n_cap, parent, draft_tok,
                                             req_offsets, req_status);
   return launch_status("k_draft_prune");
 }

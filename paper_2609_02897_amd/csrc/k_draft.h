@@ -482,7 +482,7 @@ __device__ __forceinline__ int draft_tree_rows(const asv_draft_tree* t) {
 }
 
 __global__ __launch_bounds__(kPruneThreads)
-void k_draft_prune(const asv_draft_tree* __restrict__ trees, int B,
+void k_draft_prune(const asv_draft_tree* __restrict__ trees,
                    const int32_t* __restrict__ root_tok, int n_cap, int32_t* __restrict__ parent,
                    int32_t* __restrict__ draft_tok, int32_t* __restrict__ req_offsets,
                    int32_t* __restrict__ req_status) {

@@ -331,7 +331,6 @@ __device__ __forceinline__ void lmhead_tile_spread(
     f32x16 (&acc)[LmheadCfg<TV, TR, WV, WR, 64, 2>::MV][LmheadCfg<TV, TR, WV, WR, 64, 2>::MR]) {
   constexpr int BK = 64, NST = 2;
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
-  constexpr int CPR = C::CPR;
   constexpr int MV = C::MV, MR = C::MR;
   constexpr int NF = MV + MR;                 // fragments per K16 step
   constexpr int NM = 4 * MV * MR;             // MFMAs per stage
@@ -417,7 +416,6 @@ __device__ __forceinline__ void lmhead_tile_spread3(
     f32x16 (&acc)[LmheadCfg<TV, TR, WV, WR, 64, 3>::MV][LmheadCfg<TV, TR, WV, WR, 64, 3>::MR]) {
   constexpr int BK = 64, NST = 3;
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
-  constexpr int CPR = C::CPR;
   constexpr int MV = C::MV, MR = C::MR;
   constexpr int NF = MV + MR;                 // fragments per K16 step
   constexpr int NM = 4 * MV * MR;             // MFMAs per stage
