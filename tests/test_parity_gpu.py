@@ -258,6 +258,50 @@ def test_packed_weight_every_tile(asv, dev):
                 assert np.array_equal(got[k][sel], v[sel], equal_nan=True), (rows, k)
 
 
+def test_packed_weight_past_2gib(asv, dev):
+    """A 3.9 GiB packed weight (V = 128256, H = 16384: K-block offsets past 2^31, held in
+    32-bit unsigned arithmetic) against the row-major weight, bit for bit, on the 64- and
+    128-row tiles; the draft layout likewise at 2.1 GiB."""
+    import torch
+    V, H, N = 128256, 16384, 100
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    w = (torch.randn((V, H), device=dev, generator=g) * 0.01).to(torch.bfloat16)
+    hidden = torch.randn((N, H), device=dev, generator=g).to(torch.bfloat16)
+    parent = torch.tensor([-1] + list(range(N - 1)), dtype=torch.int32, device=dev)
+    tok = torch.randint(0, V, (N,), dtype=torch.int32, device=dev, generator=g)
+    off = torch.tensor([0, N], dtype=torch.int32, device=dev)
+    tau = torch.full((1,), 0.3, dtype=torch.float32, device=dev)
+    p = asv.pack_lm_head(w)
+    assert p.data.numel() * 2 >= 3.9 * 2**30
+    for tile in (64, 128):
+        n = 60 if tile == 64 else N
+        args = (hidden[:n], None, tok[:n], parent[:n], torch.tensor([0, n], dtype=torch.int32,
+                                                                     device=dev), tau)
+        got = asv.verify(args[0], p, *args[2:], k1_tile=tile)
+        ref = asv.verify(args[0], w, *args[2:], k1_tile=tile)
+        torch.cuda.synchronize()
+        assert torch.isfinite(ref.row_max).all()
+        for f in ("row_max", "row_lse", "row_argmax", "accept", "accepted_len",
+                  "accepted_path", "bonus_token"):
+            assert torch.equal(getattr(got, f), getattr(ref, f)), (tile, f)
+        assert torch.equal(got.drafted_logit[1:], ref.drafted_logit[1:]), tile
+    del p
+    # the draft layout at V = 64000, H = 16384 (2.1 GiB packed)
+    wd = w[:64000]
+    pd = asv.pack_draft_head(wd)
+    x = hidden[:8]
+    for weight_pair in ((wd, pd),):
+        outs = []
+        for weight in weight_pair:
+            trees = asv.alloc_draft_trees(2, dev)
+            outs.append(asv.draft_step(x, weight, trees, 0, shape=(3, 4, 4)))
+        torch.cuda.synchronize()
+        for f in outs[0]._fields:
+            if getattr(outs[0], f) is not None:
+                assert torch.equal(getattr(outs[0], f), getattr(outs[1], f)), f
+
+
 @pytest.mark.parametrize("name", ["deep_chain_and_wide", "request_over_lds_stage"])
 @pytest.mark.parametrize("max_promotions", [0, 1, 2])
 def test_promotion_cap(asv, dev, max_promotions, name):
