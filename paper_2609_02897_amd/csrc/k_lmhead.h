@@ -206,8 +206,7 @@ struct TileIo {
         dma16_stream(lds_at, at, w_rsrc);
       else
         dma16(lds_at, at, w_rsrc);
-    }
-    else
+    } else
       dma16(base + C::kStageW + ((c - C::DW) * C::kWaves + wave) * 1024,
             x_voff[c - C::DW] + ks * BK * 2, x_rsrc);
   }
