@@ -6,12 +6,15 @@
 
 namespace asv {
 
-constexpr int kConfChunk = 8192;        // draft logits per K4 workgroup
+constexpr int kConfPerThread = 8;
 constexpr int kConfThreads = 256;
+constexpr int kConfChunk = kConfPerThread * kConfThreads;   // draft logits per K4 workgroup
 
 // Grid (chunks, B). Workgroup (ch, b) reduces draft_logits[root_b][ch*kConfChunk ...] to one
-// (max, sum of exp(q - max)) record. An out-of-range root (malformed offsets, reported by K3)
-// yields an empty record and reads nothing.
+// (max, sum of exp(q - max)) record in one pass: each thread issues its eight loads (entry
+// lo + 256 i + t, coalesced per wave) before using any, then reduces them in registers.
+// Entries past V read as -inf and add nothing. An out-of-range root (malformed offsets,
+// reported by K3) yields an empty record and reads nothing.
 __global__ __launch_bounds__(kConfThreads)
 void k_draft_conf_partial(int N, int V, const int32_t* __restrict__ req_offsets,
                           const float* __restrict__ q, float* __restrict__ part_m,
@@ -23,12 +26,21 @@ void k_draft_conf_partial(int N, int V, const int32_t* __restrict__ req_offsets,
   Rec r = rec_empty();
   if (root >= 0 && root < N) {
     const float* row = q + (size_t)root * V;
-    float m = kNegInf;
-    for (int v = lo + threadIdx.x; v < hi; v += kConfThreads) m = fmaxf(m, row[v]);
+    float x[kConfPerThread];
+#pragma unroll
+    for (int i = 0; i < kConfPerThread; ++i) {
+      const int v = lo + i * kConfThreads + (int)threadIdx.x;
+      x[i] = v < hi ? row[v] : kNegInf;
+    }
+    float m = x[0];
+#pragma unroll
+    for (int i = 1; i < kConfPerThread; ++i) m = fmaxf(m, x[i]);
     float s = 0.f;
-    const float mb = m * kLog2e;
-    for (int v = lo + threadIdx.x; v < hi; v += kConfThreads)
-      s += exp2_rel(fmaf(row[v], kLog2e, -mb));
+    if (m != kNegInf) {
+      const float mb = m * kLog2e;
+#pragma unroll
+      for (int i = 0; i < kConfPerThread; ++i) s += exp2_rel(fmaf(x[i], kLog2e, -mb));
+    }
     r = Rec{m, s, 0};
   }
   r = rec_wave_reduce(r);
