@@ -45,12 +45,12 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Tile families of K1. Few rows (the weight-streaming regime of small batches) use a 64-row
 // tile so that all rows share one pass over W. Beyond 64 rows the pick minimises an estimate of
-// the launch time: the rounds of workgroups over the CUs times the time of one tile, 60 : 83 :
-// 103 for the 128-, 192- and 256-row tiles (per-tile times of the spread loops on MI355X); ties
-// go to the larger tile. Interleaved comparisons at V = 151936 (records bit-identical across
-// the tiles) agree with the estimate from 150 to 3048 rows: e.g. at 540 rows three 192-row
-// tiles beat three 256-row tiles by 19%, at 700 rows three 256-row tiles beat four 192-row
-// tiles by 7%.
+// the launch time: the rounds of workgroups over the CUs times the time of one tile, 62 : 80 :
+// 98 for the 128-, 192- and 256-row tiles (per-round times of the spread loops on MI355X, with
+// the packed weight); ties go to the larger tile. Interleaved comparisons at V = 151936
+// (records bit-identical across the tiles) agree with the estimate at every row count measured
+// from 150 to 3048 rows: e.g. at 540 rows three 192-row tiles beat three 256-row tiles by 17%,
+// at 700 rows three 256-row tiles beat four 192-row tiles by 9%.
 enum class Tile { kRows64, kRows128, kRows192, kRows256 };
 
 // Compute units of the current device, queried once per device.
@@ -71,8 +71,8 @@ int cu_count() {
 Tile pick_tile(int N, int S, int cus) {
   if (N <= 64) return Tile::kRows64;
   struct Family { Tile tile; int rows; int cost; };
-  const Family families[3] = {{Tile::kRows128, 128, 60}, {Tile::kRows192, 192, 83},
-                              {Tile::kRows256, 256, 103}};
+  const Family families[3] = {{Tile::kRows128, 128, 62}, {Tile::kRows192, 192, 80},
+                              {Tile::kRows256, 256, 98}};
   Tile best = Tile::kRows128;
   int64_t best_est = INT64_MAX;
   for (const Family& f : families) {
