@@ -142,15 +142,15 @@ __device__ __forceinline__ int xcd_tile(int bid, int G) {
 // consecutive [BK]-wide row segments, so the TV rows of slab s at K block k are one contiguous
 // run starting at element k Vp BK + v0 BK. Offsets within the packed buffer are 32-bit
 // unsigned (the host keeps it under 4 GiB).
-template <int TV, int TR, int WV, int WR, int BK, int NST>
+// STREAM_W: copy W with the non-temporal hint. The default suits K1: its tiles of up to 128
+// rows are weight-bound or close to it and read W faster with the hint (60 rows: 13% less
+// time), while the larger tiles share each W slab between the row tiles of one XCD through
+// its L2 and keep the default policy (the hint measured within noise there).
+template <int TV, int TR, int WV, int WR, int BK, int NST, bool STREAM_W = (TR <= 128)>
 struct TileIo {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
   static constexpr int CPR = C::CPR;
-  // Tiles of up to 128 rows stream W: their launches are weight-bound or close to it, and
-  // copies with the non-temporal hint read W faster (60 rows: 13% less time). The larger
-  // tiles share each W slab between the row tiles of one XCD through its L2 and keep the
-  // default policy (the hint measured within noise there).
-  static constexpr bool kStreamW = TR <= 128;
+  static constexpr bool kStreamW = STREAM_W;
   const uint4* lds;
   int lane, wave, wv, wr, lds0, frag_row, frag_half;
   unsigned w_kstep;             // bytes between the W data of consecutive K stages
@@ -238,13 +238,13 @@ __device__ __forceinline__ void zero_acc(f32x16 (&acc)[MV][MR]) {
 // vocabulary rows v0 + wv * kWaveV + 32 i .. and tree rows r0 + wr * kWaveR + 32 j .. of this
 // wave, summed over all of H. Rows past V or past N read as zeros. On return every stage copy
 // has landed and the workgroup has passed a barrier, so the caller may reuse the LDS ring.
-template <int TV, int TR, int WV, int WR, int BK, int NST>
+template <int TV, int TR, int WV, int WR, int BK, int NST, bool STREAM_W = (TR <= 128)>
 __device__ __forceinline__ void lmhead_tile(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int N, int H, int V,
     int v0, int r0, uint4* smem, int w_packed,
     f32x16 (&acc)[LmheadCfg<TV, TR, WV, WR, BK, NST>::MV][LmheadCfg<TV, TR, WV, WR, BK, NST>::MR]) {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
-  const TileIo<TV, TR, WV, WR, BK, NST> io(X, W, N, H, V, v0, r0, smem, w_packed);
+  const TileIo<TV, TR, WV, WR, BK, NST, STREAM_W> io(X, W, N, H, V, v0, r0, smem, w_packed);
   const int KT = H / BK;
   auto issue_stage = [&](int ks) {
     static_for<C::kLoads>([&](auto cc) { io.template copy<decltype(cc)::value>(ks % NST, ks); });
