@@ -113,6 +113,27 @@ def test_draft_topk(asv, dev, B, V, H, mapped):
     _check_topk(f"B{B}V{V}", x, oracle.widen_weights(W), vmap, ids, logp, lse)
 
 
+@pytest.mark.parametrize("i", range(16))
+def test_draft_topk_random_shapes(asv, dev, i):
+    """Seeded random draft batches: B (every draft tile family), V (ragged slabs, down to the
+    four ids of a top-4), H, the id map and the weight layout, against the oracle's top-4."""
+    rng = np.random.default_rng([2609, 77, i])
+    B = int(rng.integers(1, 49))
+    V = int(rng.choice([int(rng.integers(4, 200)), int(rng.integers(200, 5000))]))
+    H = 64 * int(rng.integers(1, 9))
+    mapped, packed = bool(rng.integers(0, 2)), bool(rng.integers(0, 2))
+    print(f"case {i}: B={B} V={V} H={H} mapped={mapped} packed={packed}", flush=True)
+    W = bf16_weights(V, H, float(rng.uniform(0.2, 0.8)), 500 + i)
+    x = draft_hidden(B, H, 0, seed=700 + i)
+    vmap = draft_vocab_map(V, 3 * V + 11) if mapped else None
+    w = _bf16(W, dev)
+    trees = asv.alloc_draft_trees(B, dev)
+    out = asv.draft_step(_bf16(x, dev), asv.pack_draft_head(w) if packed else w, trees, 0,
+                         shape=(3, 4, 4), vocab_map=None if vmap is None else _t(vmap, dev))
+    ids, logp, lse, _, _ = _draft_host(out)
+    _check_topk(f"random{i}", x, oracle.widen_weights(W), vmap, ids, logp, lse)
+
+
 def test_draft_topk_exact_ties_and_nan(asv, dev):
     """Bit-identical logits (duplicated W rows in different slabs, one in the ragged last slab)
     come out lowest id first without bands; a row holding a non-number ranks every id as -inf."""
