@@ -460,7 +460,7 @@ extern "C" int asv_draft_step(const asv_draft_args* a, void* workspace, uint64_t
     // <vocab rows, draft rows, waves along vocab, waves along rows, K per stage, ring depth>
     case DraftTile::kRows32: launch_draft<64, 32, 2, 1, 64, 4>(a, L, ws, s); break;
     case DraftTile::kRows64: launch_draft<64, 64, 2, 2, 64, 4>(a, L, ws, s); break;
-    case DraftTile::kRows128: launch_draft<128, 128, 2, 2, 64, 3>(a, L, ws, s); break;
+    case DraftTile::kRows128: launch_draft<128, 128, 2, 4, 64, 3>(a, L, ws, s); break;
   }
   if (int rc = launch_status("k_draft_partial")) return rc;
   if (int rc = record_event(a->k_end_event, s, "hipEventRecord(k_end_event)")) return rc;
