@@ -9,6 +9,7 @@ and commit: bit-exact.
 """
 
 import ctypes
+import os
 
 import numpy as np
 import pytest
@@ -113,7 +114,7 @@ def test_draft_topk(asv, dev, B, V, H, mapped):
     _check_topk(f"B{B}V{V}", x, oracle.widen_weights(W), vmap, ids, logp, lse)
 
 
-@pytest.mark.parametrize("i", range(16))
+@pytest.mark.parametrize("i", range(int(os.environ.get("ASV_RANDOM_DRAFT_CASES", "16"))))
 def test_draft_topk_random_shapes(asv, dev, i):
     """Seeded random draft batches: B (every draft tile family), V (ragged slabs, down to the
     four ids of a top-4), H, the id map and the weight layout, against the oracle's top-4."""
