@@ -537,6 +537,6 @@ extern "C" int asv_commit(const asv_commit_args* a, void* stream) {
   c.status = a->req_status;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   (void)hipGetLastError();
-  k_commit<<<a->B, kCommitThreads, 0, s>>>(c);
+  k_commit<<<dim3(a->B, c.src ? kCommitSplit : 1), kCommitThreads, 0, s>>>(c);
   return launch_status("k_commit");
 }

@@ -85,6 +85,7 @@ void k_tree_meta(const int32_t* __restrict__ parent, const int32_t* __restrict__
 // ------------------------------------------------------------------------------------------ K9
 
 constexpr int kCommitThreads = 256;
+constexpr int kCommitSplit = 4;       // workgroups per request when rows are copied
 
 struct CommitArgs {
   int B, N;
@@ -117,10 +118,13 @@ __device__ __forceinline__ int commit_count(const CommitArgs& a, int q, int* bad
 __global__ __launch_bounds__(kCommitThreads)
 void k_commit(CommitArgs a) {
   __shared__ int s_base, s_bad;
-  const int b = blockIdx.x, tid = threadIdx.x;
+  // Grid (B, G): workgroup (b, g) copies kept rows g, g + G, ... of request b; all G
+  // workgroups of a request compute the same offset and checks, and only g = 0 writes the
+  // status, the tokens and the row ids.
+  const int b = blockIdx.x, g = blockIdx.y, G = gridDim.y, tid = threadIdx.x;
   if (!offsets_ok_block(a.off, a.B, a.N, tid, kCommitThreads)) {
     // nothing is committed: empty segments for every request
-    if (tid == 0) {
+    if (tid == 0 && g == 0) {
       a.status[b] = ASV_RS_BAD_OFFSETS;
       a.c_off[b + 1] = 0;
       if (b == 0) a.c_off[0] = 0;
@@ -150,12 +154,12 @@ void k_commit(CommitArgs a) {
   const int sbad = s_bad;
   if (sbad & ASV_RS_BAD_PATH) cnt = cnt > 0 ? 1 : 0;        // root row and bonus only
   const int len = cnt - 1;
-  if (tid == 0) {
+  if (tid == 0 && g == 0) {
     a.status[b] = sbad;
     a.c_off[b + 1] = base + cnt;
     if (b == 0) a.c_off[0] = 0;
   }
-  for (int j = tid; j < cnt; j += kCommitThreads) {
+  for (int j = tid; j < cnt && g == 0; j += kCommitThreads) {
     const int at = base + j;
     if (at >= a.N) break;
     const int row = j == 0 ? lo : a.path[lo + j - 1];
@@ -169,10 +173,12 @@ void k_commit(CommitArgs a) {
                                         reinterpret_cast<uintptr_t>(a.dst)) & 15) == 0;
   const long long unit = wide ? 16 : 4;
   const long long per_row = rb / unit;
-  const long long total = (long long)cnt * per_row;
+  const int mine = cnt > g ? (cnt - g + G - 1) / G : 0;     // kept rows g, g + G, ...
+  const long long total = (long long)mine * per_row;
   for (long long e = tid; e < total; e += kCommitThreads) {
-    const int j = (int)(e / per_row);
-    const long long u = e - (long long)j * per_row;
+    const int k = (int)(e / per_row);
+    const long long u = e - (long long)k * per_row;
+    const int j = g + k * G;
     const int at = base + j;
     if (at >= a.N) break;
     const int row = j == 0 ? lo : a.path[lo + j - 1];
