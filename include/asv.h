@@ -36,7 +36,7 @@
 extern "C" {
 #endif
 
-#define ASV_VERSION 150          /* 1.5.0 */
+#define ASV_VERSION 160          /* 1.6.0 */
 
 /* Return codes. */
 #define ASV_OK          0
@@ -131,13 +131,6 @@ typedef struct asv_verify_args {
   asv_req_state *state;           /* [B] in/out policy state, or NULL to skip the update */
   int32_t *req_status;            /* [B] ASV_RS_* bits, 0 when the request was well formed */
   asv_params params;
-  void *k1_begin_event;           /* optional hipEvent_t recorded just before the LM-head
-                                     kernel, or NULL */
-  void *k1_end_event;             /* optional hipEvent_t recorded just after it, or NULL */
-  int32_t k1_tile_rows;           /* tree rows per LM-head tile: 0 picks it from N, V and the
-                                     device's compute-unit count; 64, 128, 192 or 256 force
-                                     that tile (tuning and tests; every tile gives the same
-                                     results); any other value: ASV_EINVAL */
   int32_t w_lm_layout;            /* ASV_W_ROW_MAJOR: w_lm is [V][H] as above.
                                      ASV_W_PACKED: w_lm is the output of asv_pack_lm_head for
                                      this V and H. Both give bit-identical results. Any other
@@ -231,8 +224,6 @@ typedef struct asv_draft_args {
                                      trees that are done or invalid */
   float   *draft_conf;            /* [B] or NULL; at step 0, p_draft(top1) = exp(best log-prob of
                                      the root row), the confidence Eq. (2) reads */
-  void *k_begin_event;            /* optional hipEvent_t recorded around the LM-head kernel */
-  void *k_end_event;
   int32_t w_draft_layout;         /* ASV_W_ROW_MAJOR: w_draft is [V][H] as above.
                                      ASV_W_PACKED: w_draft is the output of asv_pack_draft_head
                                      for this V and H. Both give bit-identical results. Any
@@ -345,6 +336,29 @@ int asv_tree_policy(const float *conf, asv_req_state *state, int32_t B, const as
 /* Fill state[0..B) with the initial policy state for params *p (rar = hist_mean = rar0,
  * empty ring, zero counters, dcs 0, shape = shape_start) on `stream`. */
 int asv_state_init(asv_req_state *state, int32_t B, const asv_params *p, void *stream);
+
+/* ---- Measurement and tuning. Not needed to use the library: the product entry points
+ * (asv_verify, asv_draft_step) are these calls with a NULL asv_tuning. */
+
+typedef struct asv_tuning {
+  void   *begin_event;            /* optional hipEvent_t recorded on `stream` just before the
+                                     LM-head kernel (K1 of asv_verify, the draft LM head of
+                                     asv_draft_step), or NULL */
+  void   *end_event;              /* optional hipEvent_t recorded just after it, or NULL */
+  int32_t tile_rows;              /* asv_verify only: tree rows per LM-head tile. 0 lets the
+                                     library pick it from N, V and the device's compute-unit
+                                     count; 64, 128, 192 or 256 force that tile (every tile
+                                     gives the same results). Any other value, or a nonzero
+                                     value for asv_draft_step: ASV_EINVAL */
+} asv_tuning;
+
+/* asv_verify / asv_draft_step with measurement and tuning controls; `tuning` may be NULL.
+ * Same arguments, results and errors as the product calls; an event that cannot be recorded
+ * returns ASV_EHIP. */
+int asv_verify_tuned(const asv_verify_args *args, const asv_tuning *tuning, void *workspace,
+                     uint64_t workspace_bytes, void *stream);
+int asv_draft_step_tuned(const asv_draft_args *args, const asv_tuning *tuning, void *workspace,
+                         uint64_t workspace_bytes, void *stream);
 
 /* One verification step for a batch (Sec. 3.2, Eq. (1); Sec. 3.3, Eq. (2)):
  *   1. logits of every row against every vocabulary entry (bf16 inputs, fp32 accumulation),

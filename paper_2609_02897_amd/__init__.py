@@ -15,7 +15,7 @@ from ._abi import (  # noqa: F401
     ASV_EHIP, ASV_EINVAL, ASV_EWORKSPACE, ASV_OK, DS_BAD_SHAPE, DS_OVERFLOW, EXPORTS, LIB_PATH,
     POOL_MAX, RS_BAD_OFFSETS, RS_BAD_PARENT, RS_BAD_PATH, RS_BAD_ROOT, RS_BAD_TAU,
     RS_BAD_TOKEN, RS_MASK_SMALL, TOPK_MAX, W_PACKED, W_ROW_MAJOR, AsvCommitArgs, AsvDraftArgs,
-    AsvDraftTree, AsvParams, AsvReqState, AsvVerifyArgs, LibraryMissing, load)
+    AsvDraftTree, AsvParams, AsvReqState, AsvTuning, AsvVerifyArgs, LibraryMissing, load)
 
 STATE_BYTES = ctypes.sizeof(AsvReqState)
 TREE_BYTES = ctypes.sizeof(AsvDraftTree)
@@ -119,6 +119,35 @@ def alloc_outputs(B: int, N: int, device, with_conf: bool) -> VerifyOut:
         torch.empty(B, dtype=i32, device=device))
 
 
+def _verify_out_spec(B: int, N: int, with_conf: bool) -> dict:
+    import torch
+    f32, i32 = torch.float32, torch.int32
+    return dict(row_max=(f32, (N,)), row_lse=(f32, (N,)), row_argmax=(i32, (N,)),
+                drafted_logit=(f32, (N,)), accept=(torch.uint8, (N,)),
+                accepted_len=(i32, (B,)), bonus_token=(i32, (B,)), accepted_path=(i32, (N,)),
+                draft_conf=(f32, (B,)) if with_conf else None, req_status=(i32, (B,)))
+
+
+def _need_out(out, spec: dict, device):
+    """Caller-supplied output buffers: every field of the dtype and shape these sizes need,
+    contiguous and on the inputs' device (the kernels write exactly that many elements)."""
+    for name, want in spec.items():
+        t = getattr(out, name)
+        if want is None:
+            continue
+        _need(t, f"out.{name}", *want)
+        if t.device != device:
+            raise ValueError(f"out.{name}: on {t.device}, the inputs are on {device}")
+
+
+def _need_workspace(ws, need: int, device):
+    import torch
+    if not isinstance(ws, torch.Tensor) or ws.device != device or not ws.is_contiguous():
+        raise ValueError("workspace: a contiguous tensor on the inputs' device")
+    if ws.dtype != torch.uint8 or ws.numel() < need or ws.data_ptr() % 256:
+        raise ValueError(f"workspace: a 256-byte aligned uint8 tensor of >= {need} bytes")
+
+
 def _need(t, name, dtype, shape):
     import torch
     if t is None or not isinstance(t, torch.Tensor):
@@ -199,9 +228,11 @@ def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None,
 
     hidden bf16 [N, H]; w_lm bf16 [V, H] or its ``PackedLmHead``; draft_tok, parent int32 [N];
     req_offsets int32 [B+1]; tau float32 [B]; draft_logits float32 [N, V] or None; state u8
-    [B, 112] (in/out) or None. ``out`` and ``workspace`` may be passed to reuse buffers. ``k1_events`` is an
-    optional pair of raw hipEvent_t handles recorded around the LM-head kernel. ``k1_tile``
-    forces the LM-head tile (64, 128, 192 or 256 tree rows); 0 lets the library pick it.
+    [B, 112] (in/out) or None. ``out`` and ``workspace`` may be passed to reuse buffers
+    (checked against these sizes). Measurement and tuning go through ``asv_verify_tuned``:
+    ``k1_events`` is an optional pair of raw hipEvent_t handles recorded around the LM-head
+    kernel, and ``k1_tile`` forces the LM-head tile (64, 128, 192 or 256 tree rows); 0 lets the
+    library pick it. Without either, the product entry point ``asv_verify`` is called.
     """
     import torch
     N, H = hidden.shape
@@ -219,8 +250,12 @@ def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None,
     dev = hidden.device
     if out is None:
         out = alloc_outputs(B, N, dev, draft_logits is not None)
+    else:
+        _need_out(out, _verify_out_spec(B, N, out.draft_conf is not None), dev)
     if workspace is None:
         workspace = alloc_workspace(B, N, H, V, dev)
+    else:
+        _need_workspace(workspace, workspace_bytes(B, N, H, V), dev)
     a = AsvVerifyArgs()
     a.B, a.N, a.H, a.V = B, N, H, V
     a.hidden, a.w_lm, a.w_lm_layout = hidden.data_ptr(), w_ptr, layout
@@ -236,16 +271,27 @@ def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None,
     a.state = _ptr(state)
     a.req_status = out.req_status.data_ptr()
     a.params = params or make_params()
-    if k1_events is not None:
-        a.k1_begin_event, a.k1_end_event = k1_events
-    a.k1_tile_rows = k1_tile
-    _check(load().asv_verify(ctypes.byref(a), workspace.data_ptr(), workspace.numel(),
-                             _stream_handle(dev)))
+    lib = load()
+    if k1_events is None and not k1_tile:
+        _check(lib.asv_verify(ctypes.byref(a), workspace.data_ptr(), workspace.numel(),
+                              _stream_handle(dev)))
+    else:
+        tu = _tuning(k1_events, k1_tile)
+        _check(lib.asv_verify_tuned(ctypes.byref(a), ctypes.byref(tu), workspace.data_ptr(),
+                                    workspace.numel(), _stream_handle(dev)))
     return out
 
 
+def _tuning(events=None, tile_rows: int = 0) -> AsvTuning:
+    tu = AsvTuning()
+    if events is not None:
+        tu.begin_event, tu.end_event = events
+    tu.tile_rows = tile_rows
+    return tu
+
+
 def state_fields(state) -> list:
-    """Decode a [B, 96] u8 state tensor (copied to the host) into AsvReqState structs."""
+    """Decode a [B, 112] u8 state tensor (copied to the host) into AsvReqState structs."""
     raw = state.detach().cpu().contiguous().numpy().tobytes()
     return [AsvReqState.from_buffer_copy(raw[i * STATE_BYTES:(i + 1) * STATE_BYTES])
             for i in range(state.shape[0])]
@@ -303,9 +349,17 @@ def draft_step(hidden, w_draft, trees, step: int, state=None, shape=None, vocab_
                        torch.empty(R, dtype=torch.float32, device=dev),
                        torch.empty((B, TOPK_MAX), dtype=torch.int32, device=dev),
                        torch.empty(B, dtype=torch.float32, device=dev) if with_conf else None)
+    else:
+        f32, i32 = torch.float32, torch.int32
+        _need_out(out, dict(topk_id=(i32, (R, TOPK_MAX)), topk_logp=(f32, (R, TOPK_MAX)),
+                            row_lse=(f32, (R,)), front_tok=(i32, (B, TOPK_MAX)),
+                            draft_conf=(f32, (B,)) if out.draft_conf is not None else None),
+                  dev)
     if workspace is None:
         workspace = torch.empty(max(draft_workspace_bytes(B, H, V), 256), dtype=torch.uint8,
                                 device=dev)
+    else:
+        _need_workspace(workspace, draft_workspace_bytes(B, H, V), dev)
     a = AsvDraftArgs()
     a.B, a.H, a.V, a.step = B, H, V, step
     a.hidden, a.w_draft, a.w_draft_layout = hidden.data_ptr(), w_ptr, layout
@@ -315,10 +369,14 @@ def draft_step(hidden, w_draft, trees, step: int, state=None, shape=None, vocab_
     a.topk_id, a.topk_logp = out.topk_id.data_ptr(), out.topk_logp.data_ptr()
     a.row_lse, a.front_tok = out.row_lse.data_ptr(), out.front_tok.data_ptr()
     a.draft_conf = _ptr(out.draft_conf)
-    if events is not None:
-        a.k_begin_event, a.k_end_event = events
-    _check(load().asv_draft_step(ctypes.byref(a), workspace.data_ptr(), workspace.numel(),
-                                 _stream_handle(dev)))
+    lib = load()
+    if events is None:
+        _check(lib.asv_draft_step(ctypes.byref(a), workspace.data_ptr(), workspace.numel(),
+                                  _stream_handle(dev)))
+    else:
+        tu = _tuning(events)
+        _check(lib.asv_draft_step_tuned(ctypes.byref(a), ctypes.byref(tu), workspace.data_ptr(),
+                                        workspace.numel(), _stream_handle(dev)))
     return out
 
 

@@ -21,7 +21,7 @@ EXPORTS = ("asv_version", "asv_status_string", "asv_last_error", "asv_workspace_
            "asv_tree_policy", "asv_state_init", "asv_verify", "asv_draft_workspace_bytes",
            "asv_draft_step", "asv_draft_prune", "asv_tree_meta", "asv_commit",
            "asv_packed_lm_head_bytes", "asv_pack_lm_head", "asv_packed_draft_head_bytes",
-           "asv_pack_draft_head")
+           "asv_pack_draft_head", "asv_verify_tuned", "asv_draft_step_tuned")
 
 
 class AsvReqState(ctypes.Structure):
@@ -52,9 +52,11 @@ class AsvVerifyArgs(ctypes.Structure):
                 ("drafted_logit", _P), ("accept", _P),
                 ("accepted_len", _P), ("bonus_token", _P), ("accepted_path", _P),
                 ("draft_conf", _P), ("state", _P), ("req_status", _P),
-                ("params", AsvParams),
-                ("k1_begin_event", _P), ("k1_end_event", _P), ("k1_tile_rows", ctypes.c_int32),
-                ("w_lm_layout", ctypes.c_int32)]
+                ("params", AsvParams), ("w_lm_layout", ctypes.c_int32)]
+
+
+class AsvTuning(ctypes.Structure):
+    _fields_ = [("begin_event", _P), ("end_event", _P), ("tile_rows", ctypes.c_int32)]
 
 
 class AsvDraftTree(ctypes.Structure):
@@ -71,7 +73,7 @@ class AsvDraftArgs(ctypes.Structure):
                 ("step", ctypes.c_int32), ("hidden", _P), ("w_draft", _P), ("vocab_map", _P),
                 ("state", _P), ("shape", ctypes.c_int32 * 3), ("tree", _P), ("topk_id", _P),
                 ("topk_logp", _P), ("row_lse", _P), ("front_tok", _P), ("draft_conf", _P),
-                ("k_begin_event", _P), ("k_end_event", _P), ("w_draft_layout", ctypes.c_int32)]
+                ("w_draft_layout", ctypes.c_int32)]
 
 
 class AsvCommitArgs(ctypes.Structure):
@@ -129,6 +131,12 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         ctypes.POINTER(ctypes.c_uint64)]
     lib.asv_draft_step.restype = ctypes.c_int
     lib.asv_draft_step.argtypes = [ctypes.POINTER(AsvDraftArgs), _P, ctypes.c_uint64, _P]
+    lib.asv_verify_tuned.restype = ctypes.c_int
+    lib.asv_verify_tuned.argtypes = [ctypes.POINTER(AsvVerifyArgs), ctypes.POINTER(AsvTuning),
+                                     _P, ctypes.c_uint64, _P]
+    lib.asv_draft_step_tuned.restype = ctypes.c_int
+    lib.asv_draft_step_tuned.argtypes = [ctypes.POINTER(AsvDraftArgs),
+                                         ctypes.POINTER(AsvTuning), _P, ctypes.c_uint64, _P]
     lib.asv_draft_prune.restype = ctypes.c_int
     lib.asv_draft_prune.argtypes = [_P, ctypes.c_int32, _P, ctypes.c_int32, _P, _P, _P, _P, _P]
     lib.asv_tree_meta.restype = ctypes.c_int

@@ -318,11 +318,12 @@ extern "C" int asv_tree_policy(const float* conf, asv_req_state* state, int32_t 
   return launch_status("k_tree_policy");
 }
 
-extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t workspace_bytes,
-                          void* stream) {
+extern "C" int asv_verify_tuned(const asv_verify_args* a, const asv_tuning* tuning,
+                                void* workspace, uint64_t workspace_bytes, void* stream) {
   if (!a || !sizes_ok(a->B, a->N, a->H, a->V)) return ASV_EINVAL;
+  const asv_tuning tu = tuning ? *tuning : asv_tuning{nullptr, nullptr, 0};
   Tile forced = Tile::kRows64;
-  if (a->k1_tile_rows != 0 && !forced_tile(a->k1_tile_rows, &forced)) return ASV_EINVAL;
+  if (tu.tile_rows != 0 && !forced_tile(tu.tile_rows, &forced)) return ASV_EINVAL;
   if (a->w_lm_layout != ASV_W_ROW_MAJOR && a->w_lm_layout != ASV_W_PACKED) return ASV_EINVAL;
   uint64_t packed_bytes = 0;
   if (a->w_lm_layout == ASV_W_PACKED &&
@@ -353,14 +354,8 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
     if (int rc = launch_status("k_draft_conf_partial")) return rc;
   }
 
-  if (a->k1_begin_event) {
-    const hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(a->k1_begin_event), s);
-    if (e != hipSuccess) {
-      set_error("hipEventRecord(k1_begin_event)", e);
-      return ASV_EHIP;
-    }
-  }
-  const Tile tile = a->k1_tile_rows != 0 ? forced : pick_tile(a->N, L.S, cu_count());
+  if (int rc = record_event(tu.begin_event, s, "hipEventRecord(begin_event)")) return rc;
+  const Tile tile = tu.tile_rows != 0 ? forced : pick_tile(a->N, L.S, cu_count());
   switch (tile) {
     // <vocab rows, tree rows, waves along vocab, waves along rows, K per stage, ring depth,
     // K loop>, each the fastest of a sweep on MI355X for its row range. The weight-streaming
@@ -375,13 +370,7 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
     case Tile::kRows256: launch_lmhead<256, 256, 2, 2, 64, 2, 2>(a, L, ws, s); break;
   }
   if (int rc = launch_status("k_lmhead_partial")) return rc;
-  if (a->k1_end_event) {
-    const hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(a->k1_end_event), s);
-    if (e != hipSuccess) {
-      set_error("hipEventRecord(k1_end_event)", e);
-      return ASV_EHIP;
-    }
-  }
+  if (int rc = record_event(tu.end_event, s, "hipEventRecord(end_event)")) return rc;
 
   const AcceptArgs acc = accept_args(a, L, ws, conf);
   const float* rec_m = reinterpret_cast<const float*>(ws + L.off_rec_m);
@@ -400,6 +389,11 @@ extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t wo
   if (int rc = launch_status("k_slab_merge")) return rc;
   k_tree_accept<<<a->B, kWave, 0, s>>>(cnt + a->B, acc);
   return launch_status("k_tree_accept");
+}
+
+extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t workspace_bytes,
+                          void* stream) {
+  return asv_verify_tuned(a, nullptr, workspace, workspace_bytes, stream);
 }
 
 extern "C" int asv_packed_lm_head_bytes(int32_t V, int32_t H, uint64_t* bytes) {
@@ -429,9 +423,11 @@ extern "C" int asv_draft_workspace_bytes(int32_t B, int32_t H, int32_t V, uint64
   return ASV_OK;
 }
 
-extern "C" int asv_draft_step(const asv_draft_args* a, void* workspace, uint64_t workspace_bytes,
-                              void* stream) {
+extern "C" int asv_draft_step_tuned(const asv_draft_args* a, const asv_tuning* tuning,
+                                    void* workspace, uint64_t workspace_bytes, void* stream) {
   if (!a || !draft_sizes_ok(a->B, a->H, a->V) || a->step < 0) return ASV_EINVAL;
+  const asv_tuning tu = tuning ? *tuning : asv_tuning{nullptr, nullptr, 0};
+  if (tu.tile_rows != 0) return ASV_EINVAL;
   if (a->w_draft_layout != ASV_W_ROW_MAJOR && a->w_draft_layout != ASV_W_PACKED)
     return ASV_EINVAL;
   uint64_t packed_bytes = 0;
@@ -455,7 +451,7 @@ extern "C" int asv_draft_step(const asv_draft_args* a, void* workspace, uint64_t
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
   (void)hipGetLastError();
-  if (int rc = record_event(a->k_begin_event, s, "hipEventRecord(k_begin_event)")) return rc;
+  if (int rc = record_event(tu.begin_event, s, "hipEventRecord(begin_event)")) return rc;
   switch (pick_draft_tile(a->B * kTopK)) {
     // <vocab rows, draft rows, waves along vocab, waves along rows, K per stage, ring depth>
     case DraftTile::kRows32: launch_draft<64, 32, 2, 1, 64, 4>(a, L, ws, s); break;
@@ -463,7 +459,7 @@ extern "C" int asv_draft_step(const asv_draft_args* a, void* workspace, uint64_t
     case DraftTile::kRows128: launch_draft<128, 128, 2, 4, 64, 3>(a, L, ws, s); break;
   }
   if (int rc = launch_status("k_draft_partial")) return rc;
-  if (int rc = record_event(a->k_end_event, s, "hipEventRecord(k_end_event)")) return rc;
+  if (int rc = record_event(tu.end_event, s, "hipEventRecord(end_event)")) return rc;
   DraftGrowArgs g;
   g.B = a->B;
   g.S = L.S;
@@ -481,6 +477,11 @@ extern "C" int asv_draft_step(const asv_draft_args* a, void* workspace, uint64_t
   g.draft_conf = a->draft_conf;
   k_draft_grow<<<a->B, kDraftThreads, 0, s>>>(g);
   return launch_status("k_draft_grow");
+}
+
+extern "C" int asv_draft_step(const asv_draft_args* a, void* workspace, uint64_t workspace_bytes,
+                              void* stream) {
+  return asv_draft_step_tuned(a, nullptr, workspace, workspace_bytes, stream);
 }
 
 extern "C" int asv_draft_prune(const asv_draft_tree* tree, int32_t B, const int32_t* root_tok,

@@ -5,8 +5,9 @@
 // K8 k_tree_meta: one workgroup per request. The request's parent links are staged in LDS;
 //   each thread walks one node's chain to the root, which gives its depth and its row of the
 //   ancestor bit mask (words written from the highest down, each exactly once).
-// K9 k_commit: one workgroup per request: its offset among the committed rows (a block sum over
-//   the earlier requests), its tokens and rows, and a copy of the kept rows' data.
+// K9 k_commit: workgroups per request: its offset among the committed rows (a block sum of the
+//   validated counts of the earlier requests), its tokens and rows, and a copy of the kept
+//   rows' data.
 #pragma once
 
 #include "asv.h"
@@ -103,25 +104,41 @@ struct CommitArgs {
   int32_t* status;
 };
 
-// Committed length of request q (well-formed offsets): accepted_len + 1 when accepted_len
-// lies in [0, n - 1] (n = its node count), else 1.
-__device__ __forceinline__ int commit_count(const CommitArgs& a, int q, int* bad) {
-  const int n = a.off[q + 1] - a.off[q];
+// Committed length of request q (well-formed offsets), taken cooperatively by one wave:
+// accepted_len + 1 when accepted_len lies in [0, n - 1] (n = its node count) and every accepted
+// path entry is a non-root node of request q; else 1 (the root row and the bonus), with
+// ASV_RS_BAD_PATH. Every workgroup derives each earlier request's count from the same checks,
+// so the offset one request starts at is where the previous one ends.
+__device__ __forceinline__ int commit_count_wave(const CommitArgs& a, int q, int lane,
+                                                 int* bad) {
+  const int lo = a.off[q], hi = a.off[q + 1];
   const int L = a.acc_len[q];
-  if (L < 0 || L > n - 1) {
-    if (bad) *bad |= ASV_RS_BAD_PATH;
+  if (L < 0 || L > hi - lo - 1) {
+    *bad = ASV_RS_BAD_PATH;
     return 1;
   }
+  bool out = false;
+  for (int j = lane; j < L; j += kWave) {
+    const int p = a.path[lo + j];
+    out |= p <= lo || p >= hi;
+  }
+  if (__any(out)) {
+    *bad = ASV_RS_BAD_PATH;
+    return 1;
+  }
+  *bad = 0;
   return L + 1;
 }
 
 __global__ __launch_bounds__(kCommitThreads)
 void k_commit(CommitArgs a) {
-  __shared__ int s_base, s_bad;
+  __shared__ int s_base, s_cnt, s_bad;
   // Grid (B, G): workgroup (b, g) copies kept rows g, g + G, ... of request b; all G
   // workgroups of a request compute the same offset and checks, and only g = 0 writes the
   // status, the tokens and the row ids.
   const int b = blockIdx.x, g = blockIdx.y, G = gridDim.y, tid = threadIdx.x;
+  const int lane = tid % kWave, wave = tid / kWave;
+  constexpr int kWaves = kCommitThreads / kWave;
   if (!offsets_ok_block(a.off, a.B, a.N, tid, kCommitThreads)) {
     // nothing is committed: empty segments for every request
     if (tid == 0 && g == 0) {
@@ -131,28 +148,24 @@ void k_commit(CommitArgs a) {
     }
     return;
   }
-  if (tid == 0) {
-    s_base = 0;
-    s_bad = 0;
+  if (tid == 0) s_base = 0;
+  __syncthreads();
+  // the earlier requests' validated counts, one wave per request; then this request's own
+  int part = 0, bad = 0;
+  for (int q = wave; q < b; q += kWaves) part += commit_count_wave(a, q, lane, &bad);
+  if (lane == 0 && part) atomicAdd(&s_base, part);
+  if (wave == 0) {
+    const int cnt = commit_count_wave(a, b, lane, &bad);
+    if (lane == 0) {
+      s_cnt = cnt;
+      s_bad = bad;
+    }
   }
   __syncthreads();
-  int part = 0;
-  for (int q = tid; q < b; q += kCommitThreads) part += commit_count(a, q, nullptr);
-  if (part) atomicAdd(&s_base, part);
-  const int lo = a.off[b], hi = a.off[b + 1];
-  int bad = 0;
-  int cnt = commit_count(a, b, &bad);
-  const int L = cnt - 1;
-  // every accepted node must belong to the request
-  for (int j = tid; j < L; j += kCommitThreads) {
-    const int p = a.path[lo + j];
-    if (p <= lo || p >= hi) bad |= ASV_RS_BAD_PATH;
-  }
-  if (bad) atomicOr(&s_bad, bad);
-  __syncthreads();
+  const int lo = a.off[b];
   const int base = s_base;
   const int sbad = s_bad;
-  if (sbad & ASV_RS_BAD_PATH) cnt = cnt > 0 ? 1 : 0;        // root row and bonus only
+  const int cnt = s_cnt;               // 1 (root row and bonus only) under ASV_RS_BAD_PATH
   const int len = cnt - 1;
   if (tid == 0 && g == 0) {
     a.status[b] = sbad;

@@ -36,7 +36,7 @@ def test_exports(lib):
 
 
 def test_version_and_status(lib):
-    assert lib.asv_version() == 150
+    assert lib.asv_version() == 160
     for code in (0, -1, -2, -3, 7):
         assert lib.asv_status_string(code)
 
@@ -44,11 +44,13 @@ def test_version_and_status(lib):
 def test_struct_layouts():
     assert ctypes.sizeof(_abi.AsvReqState) == 112
     assert ctypes.sizeof(_abi.AsvParams) == 60
-    # 4 ints, 18 pointers, params (60 B, padded to 64), 2 event pointers, 2 ints
-    assert ctypes.sizeof(_abi.AsvVerifyArgs) == 16 + 18 * 8 + 64 + 2 * 8 + 2 * 4
+    # 4 ints, 18 pointers, params (60 B), the layout int
+    assert ctypes.sizeof(_abi.AsvVerifyArgs) == 16 + 18 * 8 + 60 + 4
     assert ctypes.sizeof(_abi.AsvDraftTree) == 64 + 3 * 4 * 256
-    # 4 ints, 4 pointers, 3 ints (+4 padding), 8 pointers, 1 int (+4 padding)
-    assert ctypes.sizeof(_abi.AsvDraftArgs) == 16 + 4 * 8 + 16 + 8 * 8 + 8
+    # 4 ints, 4 pointers, 3 ints (+4 padding), 6 pointers, 1 int (+4 padding)
+    assert ctypes.sizeof(_abi.AsvDraftArgs) == 16 + 4 * 8 + 16 + 6 * 8 + 8
+    # 2 event pointers, the tile int (+4 padding)
+    assert ctypes.sizeof(_abi.AsvTuning) == 2 * 8 + 8
     # 2 ints, 10 pointers, an int64, a pointer
     assert ctypes.sizeof(_abi.AsvCommitArgs) == 8 + 10 * 8 + 8 + 8
 
@@ -94,18 +96,20 @@ def test_verify_rejects_on_host(lib):
     assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
     fake = 0x100000
     for f, _ in _abi.AsvVerifyArgs._fields_[4:]:
-        if f not in ("params", "draft_logits", "draft_conf", "state", "k1_begin_event",
-                     "k1_end_event", "k1_tile_rows", "w_lm_layout"):
+        if f not in ("params", "draft_logits", "draft_conf", "state", "w_lm_layout"):
             setattr(a, f, fake)
     a.params = asv.make_params()
     assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EWORKSPACE
-    for rows in (64, 128, 192, 256):                # a forced LM-head tile is accepted
-        a.k1_tile_rows = rows
-        assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EWORKSPACE
+    tu = _abi.AsvTuning()
+    assert lib.asv_verify_tuned(ctypes.byref(a), None, None, 0, None) == asv.ASV_EWORKSPACE
+    for rows in (0, 64, 128, 192, 256):             # a forced LM-head tile is accepted
+        tu.tile_rows = rows
+        assert lib.asv_verify_tuned(ctypes.byref(a), ctypes.byref(tu), None, 0,
+                                    None) == asv.ASV_EWORKSPACE
     for rows in (-1, 1, 100, 512):                  # a value that names no tile is not
-        a.k1_tile_rows = rows
-        assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
-    a.k1_tile_rows = 0
+        tu.tile_rows = rows
+        assert lib.asv_verify_tuned(ctypes.byref(a), ctypes.byref(tu), None, 0,
+                                    None) == asv.ASV_EINVAL
     for layout in (asv.W_ROW_MAJOR, asv.W_PACKED):  # both weight layouts are accepted
         a.w_lm_layout = layout
         assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_EWORKSPACE
@@ -248,6 +252,13 @@ def test_draft_and_tree_entry_points_reject_on_host(lib):
     assert lib.asv_draft_step(ctypes.byref(a), None, 0, None) == asv.ASV_EWORKSPACE
     a.hidden = fake + 2
     assert lib.asv_draft_step(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL   # misaligned
+    a.hidden = fake
+    tu = _abi.AsvTuning()
+    assert lib.asv_draft_step_tuned(ctypes.byref(a), ctypes.byref(tu), None, 0,
+                                    None) == asv.ASV_EWORKSPACE
+    tu.tile_rows = 64                              # the draft LM head takes no forced tile
+    assert lib.asv_draft_step_tuned(ctypes.byref(a), ctypes.byref(tu), None, 0,
+                                    None) == asv.ASV_EINVAL
     a.hidden, a.step = fake, -1
     assert lib.asv_draft_step(ctypes.byref(a), None, 0, None) == asv.ASV_EINVAL
 

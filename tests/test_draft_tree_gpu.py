@@ -472,6 +472,43 @@ def test_commit_bad_path_and_offsets(asv, dev):
     assert list(st.cpu().numpy()) == [asv.RS_BAD_OFFSETS] * 3
 
 
+def test_commit_bad_path_on_first_request(asv, dev):
+    """Request 0's accepted length is in range but its path holds a node of request 1: it
+    commits its root row and bonus only, and requests 1 and 2 start right after it, with their
+    own tokens and rows (the offsets of later requests use the same validated counts)."""
+    import torch
+    parent, off = _random_batch(["eagle60", "eagle60", "tiny"], 6)
+    N = len(parent)
+    rng = np.random.default_rng(9)
+    tok = rng.integers(0, 1000, N).astype(np.int32)
+    path, acc = _accepted_paths(parent, off, np.random.default_rng(10))
+    # request 0: a three-node path whose last entry is a node of request 1
+    deep = next(c for c in range(off[0] + 1, off[1]) if parent[c] != off[0])
+    chain = [int(parent[deep]), int(deep)]
+    path[off[0]:off[0] + 3] = chain + [int(off[1]) + 1]
+    acc[0] = 3
+    acc[1] = max(int(acc[1]), 1)
+    if acc[1] == 1 and path[off[1]] < 0:
+        path[off[1]] = [c for c in range(off[1] + 1, off[2]) if parent[c] == off[1]][0]
+    bonus = np.array([5, 6, 7], dtype=np.int32)
+    rows = rng.integers(-2**31, 2**31, (N, 4)).astype(np.int32)
+    c_off, c_tok, c_row, dst, status = asv.commit(_t(off, dev), _t(tok, dev), _t(acc, dev),
+                                                   _t(path, dev), _t(bonus, dev), _t(rows, dev))
+    torch.cuda.synchronize()
+    st = status.cpu().numpy()
+    assert list(st) == [asv.RS_BAD_PATH, 0, 0], list(st)
+    good_acc = acc.copy()
+    good_acc[0] = 0
+    ref = oracle.commit(path, good_acc, bonus, tok, off)
+    total = int(ref["off"][-1])
+    c_off = c_off.cpu().numpy()
+    assert list(c_off) == list(ref["off"]) and c_off[1] == 1
+    assert list(c_tok.cpu().numpy()[:total]) == list(ref["tok"])
+    assert list(c_row.cpu().numpy()[:total]) == list(ref["row"])
+    assert c_row.cpu().numpy()[1] == off[1] and c_tok.cpu().numpy()[0] == 5
+    assert np.array_equal(dst.cpu().numpy()[:total], rows[ref["row"]])
+
+
 # ----------------------------------------------------------------------------- full size
 
 @pytest.mark.parametrize("name", ["llama31_8b_draft_b1", "llama31_8b_draft_b32"])
