@@ -43,6 +43,8 @@ extern "C" {
 #define ASV_EINVAL     -1        /* bad size, null or misaligned pointer, bad parameter */
 #define ASV_EWORKSPACE -2        /* workspace smaller than asv_workspace_bytes() or misaligned */
 #define ASV_EHIP       -3        /* a HIP runtime call or kernel launch failed */
+#define ASV_ESCRATCH   -4        /* asv_verify_noalloc: the sizes need more workspace than the
+                                    library's static scratch holds */
 
 /* req_status bits, set on the device for request b. A request with any bit set gets
  * accepted_len = 0, bonus_token = -1, draft_conf = NaN and its state left unchanged; its path
@@ -304,15 +306,32 @@ typedef struct asv_commit_args {
  * for bad sizes, null or misaligned pointers, ASV_EHIP if a launch fails. */
 int asv_commit(const asv_commit_args *args, void *stream);
 
+/* ---- For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): asv_verify with its workspace taken from a
+ * scratch array that the library holds in device memory, ASV_STATIC_SCRATCH_BYTES per GPU it
+ * runs on, from its first use on that GPU until the process ends. The caller still passes
+ * every input and output through `args`, as for asv_verify.
+ *
+ * The call allocates nothing and frees nothing. Every call on one GPU shares that GPU's scratch
+ * and leaves its contents behind; nothing in it needs to start at zero (the kernels clear their
+ * own counters). Calls that may overlap on one GPU (several host threads, or several streams
+ * without ordering between them) race on the scratch and give undefined results: order them
+ * on one stream. Returns ASV_ESCRATCH, before anything is enqueued, when
+ * asv_workspace_bytes(B, N, H, V) exceeds ASV_STATIC_SCRATCH_BYTES (for example more than
+ * about 4500 rows at V = 151936); ASV_EHIP if the scratch's device address cannot be obtained
+ * (asv_last_error() names the call); otherwise asv_verify's results and errors. */
+#define ASV_STATIC_SCRATCH_BYTES (32u << 20)
+int asv_verify_noalloc(const asv_verify_args *args, void *stream);
+
 /* ASV_VERSION of the loaded library. */
 int asv_version(void);
 
 /* Static, human-readable text for an ASV_* return code. */
 const char *asv_status_string(int code);
 
-/* Details of the most recent ASV_EHIP failure on the calling host thread (the failing launch
- * or runtime call and the HIP error text); "" if none. Valid until the next failing call on
- * this thread. */
+/* Details of the most recent ASV_EHIP or ASV_ESCRATCH failure on the calling host thread (the
+ * failing launch or runtime call and the HIP error text, or the bytes needed); "" if none.
+ * Valid until the next failing call on this thread. */
 const char *asv_last_error(void);
 
 /* Device workspace that asv_verify needs for these sizes (partial per-vocab-slab records of

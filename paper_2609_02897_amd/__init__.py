@@ -12,10 +12,11 @@ import ctypes
 from typing import NamedTuple, Optional
 
 from ._abi import (  # noqa: F401
-    ASV_EHIP, ASV_EINVAL, ASV_EWORKSPACE, ASV_OK, DS_BAD_SHAPE, DS_OVERFLOW, EXPORTS, LIB_PATH,
-    POOL_MAX, RS_BAD_OFFSETS, RS_BAD_PARENT, RS_BAD_PATH, RS_BAD_ROOT, RS_BAD_TAU,
-    RS_BAD_TOKEN, RS_MASK_SMALL, TOPK_MAX, W_PACKED, W_ROW_MAJOR, AsvCommitArgs, AsvDraftArgs,
-    AsvDraftTree, AsvParams, AsvReqState, AsvTuning, AsvVerifyArgs, LibraryMissing, load)
+    ASV_EHIP, ASV_EINVAL, ASV_ESCRATCH, ASV_EWORKSPACE, ASV_OK, DS_BAD_SHAPE, DS_OVERFLOW,
+    EXPORTS, LIB_PATH, POOL_MAX, RS_BAD_OFFSETS, RS_BAD_PARENT, RS_BAD_PATH, RS_BAD_ROOT,
+    RS_BAD_TAU, RS_BAD_TOKEN, RS_MASK_SMALL, STATIC_SCRATCH_BYTES, TOPK_MAX, W_PACKED,
+    W_ROW_MAJOR, AsvCommitArgs, AsvDraftArgs, AsvDraftTree, AsvParams, AsvReqState, AsvTuning,
+    AsvVerifyArgs, LibraryMissing, load)
 
 STATE_BYTES = ctypes.sizeof(AsvReqState)
 TREE_BYTES = ctypes.sizeof(AsvDraftTree)
@@ -38,7 +39,7 @@ class AsvError(RuntimeError):
     def __init__(self, code: int):
         lib = load()
         msg = lib.asv_status_string(code).decode()
-        detail = lib.asv_last_error().decode() if code == ASV_EHIP else ""
+        detail = lib.asv_last_error().decode() if code in (ASV_EHIP, ASV_ESCRATCH) else ""
         super().__init__(f"libasv returned {code}: {msg}" + (f" [{detail}]" if detail else ""))
         self.code = code
 
@@ -223,7 +224,8 @@ def _weight(w, kind: str, name: str, H: int):
 
 def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None, state=None,
            params: Optional[AsvParams] = None, out: Optional[VerifyOut] = None,
-           workspace=None, k1_events=None, k1_tile: int = 0) -> VerifyOut:
+           workspace=None, k1_events=None, k1_tile: int = 0,
+           noalloc: bool = False) -> VerifyOut:
     """One verification step through ``asv_verify`` on torch's current stream.
 
     hidden bf16 [N, H]; w_lm bf16 [V, H] or its ``PackedLmHead``; draft_tok, parent int32 [N];
@@ -233,8 +235,12 @@ def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None,
     ``k1_events`` is an optional pair of raw hipEvent_t handles recorded around the LM-head
     kernel, and ``k1_tile`` forces the LM-head tile (64, 128, 192 or 256 tree rows); 0 lets the
     library pick it. Without either, the product entry point ``asv_verify`` is called.
+    ``noalloc`` calls ``asv_verify_noalloc`` instead, whose workspace is the library's static
+    device scratch (no workspace tensor; pass ``out`` to allocate nothing at all here either).
     """
     import torch
+    if noalloc and (workspace is not None or k1_events is not None or k1_tile):
+        raise ValueError("noalloc takes no workspace, events or forced tile")
     N, H = hidden.shape
     B = req_offsets.shape[0] - 1
     _need(hidden, "hidden", torch.bfloat16, (N, H))
@@ -252,7 +258,9 @@ def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None,
         out = alloc_outputs(B, N, dev, draft_logits is not None)
     else:
         _need_out(out, _verify_out_spec(B, N, out.draft_conf is not None), dev)
-    if workspace is None:
+    if noalloc:
+        pass
+    elif workspace is None:
         workspace = alloc_workspace(B, N, H, V, dev)
     else:
         _need_workspace(workspace, workspace_bytes(B, N, H, V), dev)
@@ -272,7 +280,9 @@ def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None,
     a.req_status = out.req_status.data_ptr()
     a.params = params or make_params()
     lib = load()
-    if k1_events is None and not k1_tile:
+    if noalloc:
+        _check(lib.asv_verify_noalloc(ctypes.byref(a), _stream_handle(dev)))
+    elif k1_events is None and not k1_tile:
         _check(lib.asv_verify(ctypes.byref(a), workspace.data_ptr(), workspace.numel(),
                               _stream_handle(dev)))
     else:

@@ -8,7 +8,8 @@ import os
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libasv.so")
 
-ASV_OK, ASV_EINVAL, ASV_EWORKSPACE, ASV_EHIP = 0, -1, -2, -3
+ASV_OK, ASV_EINVAL, ASV_EWORKSPACE, ASV_EHIP, ASV_ESCRATCH = 0, -1, -2, -3, -4
+STATIC_SCRATCH_BYTES = 32 << 20   # ASV_STATIC_SCRATCH_BYTES
 W_ROW_MAJOR, W_PACKED = 0, 1     # asv_verify_args.w_lm_layout
 RS_BAD_ROOT, RS_BAD_PARENT, RS_BAD_TOKEN, RS_BAD_OFFSETS, RS_BAD_TAU = 1, 2, 4, 16, 32
 RS_MASK_SMALL, RS_BAD_PATH = 64, 128
@@ -21,7 +22,8 @@ EXPORTS = ("asv_version", "asv_status_string", "asv_last_error", "asv_workspace_
            "asv_tree_policy", "asv_state_init", "asv_verify", "asv_draft_workspace_bytes",
            "asv_draft_step", "asv_draft_prune", "asv_tree_meta", "asv_commit",
            "asv_packed_lm_head_bytes", "asv_pack_lm_head", "asv_packed_draft_head_bytes",
-           "asv_pack_draft_head", "asv_verify_tuned", "asv_draft_step_tuned")
+           "asv_pack_draft_head", "asv_verify_tuned", "asv_draft_step_tuned",
+           "asv_verify_noalloc")
 
 
 class AsvReqState(ctypes.Structure):
@@ -131,6 +133,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
         ctypes.POINTER(ctypes.c_uint64)]
     lib.asv_draft_step.restype = ctypes.c_int
     lib.asv_draft_step.argtypes = [ctypes.POINTER(AsvDraftArgs), _P, ctypes.c_uint64, _P]
+    lib.asv_verify_noalloc.restype = ctypes.c_int
+    lib.asv_verify_noalloc.argtypes = [ctypes.POINTER(AsvVerifyArgs), _P]
     lib.asv_verify_tuned.restype = ctypes.c_int
     lib.asv_verify_tuned.argtypes = [ctypes.POINTER(AsvVerifyArgs), ctypes.POINTER(AsvTuning),
                                      _P, ctypes.c_uint64, _P]

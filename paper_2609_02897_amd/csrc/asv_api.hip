@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <mutex>
 
 #include <cstdio>
 
@@ -264,6 +265,42 @@ void launch_draft(const asv_draft_args* a, const DraftLayout& L, char* ws, hipSt
       reinterpret_cast<float*>(ws + L.off_s), a->w_draft_layout == ASV_W_PACKED ? 1 : 0);
 }
 
+// ---- static scratch of asv_verify_noalloc
+
+// The workspace of asv_verify_noalloc. In host code `scratch` names a host-side stand-in, not
+// the device array: the device address comes from hipGetSymbolAddress, once per device (each
+// GPU holds its own copy at its own address).
+__device__ __align__(256) char scratch[ASV_STATIC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+
+// Device address of `scratch` on the current device, or nullptr (error recorded).
+void* scratch_address() {
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) {
+    set_error("hipGetDevice", e);
+    return nullptr;
+  }
+  if (dev < 0 || dev >= kMaxDevices) {
+    set_error("asv_verify_noalloc: device ordinal out of range", hipErrorInvalidDevice);
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      set_error("hipGetSymbolAddress(scratch)", e != hipSuccess ? e : hipErrorInvalidSymbol);
+      return nullptr;
+    }
+    addr[dev] = p;
+  }
+  return addr[dev];
+}
+
 int record_event(void* ev, hipStream_t s, const char* what) {
   if (!ev) return ASV_OK;
   const hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev), s);
@@ -287,6 +324,8 @@ extern "C" const char* asv_status_string(int code) {
     case ASV_EINVAL: return "invalid argument (size, null or misaligned pointer, parameter)";
     case ASV_EWORKSPACE: return "workspace too small or not 256-byte aligned";
     case ASV_EHIP: return "HIP runtime error or kernel launch failure";
+    case ASV_ESCRATCH:
+      return "the sizes need more workspace than the static scratch of asv_verify_noalloc";
     default: return "unknown asv status code";
   }
 }
@@ -394,6 +433,21 @@ extern "C" int asv_verify_tuned(const asv_verify_args* a, const asv_tuning* tuni
 extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t workspace_bytes,
                           void* stream) {
   return asv_verify_tuned(a, nullptr, workspace, workspace_bytes, stream);
+}
+
+extern "C" int asv_verify_noalloc(const asv_verify_args* a, void* stream) {
+  if (!a || !sizes_ok(a->B, a->N, a->H, a->V)) return ASV_EINVAL;
+  if (a->B == 0) return asv_verify_tuned(a, nullptr, nullptr, 0, stream);
+  const size_t need = layout(a->B, a->N, a->V).bytes;
+  if (need > ASV_STATIC_SCRATCH_BYTES) {
+    snprintf(g_last_error, sizeof(g_last_error),
+             "asv_verify_noalloc: %zu workspace bytes needed, the static scratch holds %u",
+             need, ASV_STATIC_SCRATCH_BYTES);
+    return ASV_ESCRATCH;
+  }
+  void* ws = scratch_address();
+  if (!ws) return ASV_EHIP;
+  return asv_verify_tuned(a, nullptr, ws, ASV_STATIC_SCRATCH_BYTES, stream);
 }
 
 extern "C" int asv_packed_lm_head_bytes(int32_t V, int32_t H, uint64_t* bytes) {

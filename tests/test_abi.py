@@ -37,7 +37,7 @@ def test_exports(lib):
 
 def test_version_and_status(lib):
     assert lib.asv_version() == 160
-    for code in (0, -1, -2, -3, 7):
+    for code in (0, -1, -2, -3, -4, 7):
         assert lib.asv_status_string(code)
 
 
@@ -135,6 +135,23 @@ def test_verify_rejects_on_host(lib):
                           None) == asv.ASV_EWORKSPACE          # too small
     a.B, a.N = 0, 0                              # empty batch: nothing to do
     assert lib.asv_verify(ctypes.byref(a), None, 0, None) == asv.ASV_OK
+
+
+def test_verify_noalloc_rejects_on_host(lib):
+    """asv_verify_noalloc refuses sizes beyond its static scratch (and bad sizes) before any
+    HIP call; an empty batch is a no-op."""
+    a = _abi.AsvVerifyArgs()
+    assert lib.asv_verify_noalloc(None, None) == asv.ASV_EINVAL
+    assert lib.asv_verify_noalloc(ctypes.byref(a), None) == asv.ASV_EINVAL     # H = 0
+    a.B, a.N, a.H, a.V = 1, 8192, 64, 151936
+    need = ctypes.c_uint64(0)
+    assert lib.asv_workspace_bytes(a.B, a.N, a.H, a.V, ctypes.byref(need)) == asv.ASV_OK
+    assert need.value > asv.STATIC_SCRATCH_BYTES
+    assert lib.asv_verify_noalloc(ctypes.byref(a), None) == asv.ASV_ESCRATCH
+    assert b"static scratch" in lib.asv_last_error()
+    assert b"static scratch" in lib.asv_status_string(asv.ASV_ESCRATCH)
+    a.B, a.N = 0, 0
+    assert lib.asv_verify_noalloc(ctypes.byref(a), None) == asv.ASV_OK
 
 
 def test_packed_lm_head_sizes_and_rejections(lib):
