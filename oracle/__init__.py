@@ -25,13 +25,13 @@ from .asv_oracle import (  # noqa: F401
     ReqState,
     accept_flags,
     draft_confidence,
-    drafted_logits,
     logits,
     row_stats,
     row_top8,
     state_init,
     state_update,
     tree_shape,
+    tree_shape_slack,
     verify,
     walk,
     walk_bands,

@@ -90,18 +90,6 @@ def row_top8(z: np.ndarray) -> np.ndarray:
     return out
 
 
-def drafted_logits(z_rows: Dict[int, np.ndarray], parent: np.ndarray,
-                   draft_tok: np.ndarray) -> np.ndarray:
-    """g_c = z_{parent(c)}[d_c]: the target logit of each node's drafted token, read from its
-    parent's row (roots get NaN). ``z_rows`` maps a row id to that row's logits."""
-    g = np.full(len(parent), np.nan)
-    for c in range(len(parent)):
-        p = parent[c]
-        if p >= 0 and p in z_rows:
-            g[c] = z_rows[p][draft_tok[c]]
-    return g
-
-
 # ----------------------------------------------------------------------------- margin rule
 
 def accept_flags(g: np.ndarray, M: np.ndarray, a: np.ndarray, parent: np.ndarray,
@@ -291,20 +279,30 @@ def tree_shape(conf: float, rar: float, breaker: int, p: Params):
     going to the lower one (a reading: the paper selects among pre-captured integer triplets
     without naming the rounding; parity unpinned). A request whose breaker tripped reverts to
     ``shape_start`` (Sec. 3.3; which triplet is "the starting configuration" is a reading,
-    parity unpinned).
-
-    The score decides integers, so it is evaluated in float32, one rounding per operation, as
-    the library does: DCS = min(1, fl(fl(conf * rar) / d)), x = fl(lo + fl((hi - lo) * DCS)).
+    parity unpinned). Evaluated in float64.
     """
-    f = np.float32
-    dcs = min(f(1.0), f(f(f(conf) * f(rar)) / f(p.dcs_divisor)))
+    dcs = min(1.0, float(conf) * float(rar) / float(p.dcs_divisor))
     if breaker:
-        return float(dcs), tuple(int(v) for v in p.shape_start)
+        return dcs, tuple(int(v) for v in p.shape_start)
     shape = []
     for lo, hi in zip(p.shape_lo, p.shape_hi):
-        x = f(f(lo) + f(f(hi - lo) * dcs))
-        shape.append(int(math.ceil(float(x) - 0.5)))
-    return float(dcs), tuple(shape)
+        x = lo + (hi - lo) * dcs
+        shape.append(int(math.ceil(x - 0.5)))
+    return dcs, tuple(shape)
+
+
+def tree_shape_slack(dcs: float, breaker: int, p: Params) -> float:
+    """How far the tree-shape decision of score ``dcs`` is from changing: the smallest distance
+    of any member lo + (hi - lo) * dcs from a half-integer (infinite after a breaker trip, whose
+    shape does not depend on the score). Used to band the integer shape where the library's
+    float32 score and the float64 one may round to different integers."""
+    if breaker:
+        return math.inf
+    out = math.inf
+    for lo, hi in zip(p.shape_lo, p.shape_hi):
+        x = lo + (hi - lo) * float(dcs)
+        out = min(out, abs(x - math.floor(x) - 0.5))
+    return out
 
 
 def _ring_mean(s: ReqState) -> float:

@@ -17,9 +17,8 @@ Readings of points the paper leaves open (listed with their reasons in the desig
     not a number counts as -inf; log-probabilities are taken against the row's log-sum-exp over
     the whole draft vocabulary; an optional map sends draft ids to target ids (EAGLE-3 drafts
     over a reduced vocabulary);
-  * the score of a drafted node is the float32 sum, in path order, of the float32
-    log-probabilities along its path, one rounding per addition; a log-probability that is not a
-    number counts as -inf;
+  * the score of a drafted node is the sum of the log-probabilities along its path (float64
+    here); a log-probability that is not a number counts as -inf;
   * each step appends all frontier x topk children to the pool (frontier slot major, child rank
     minor) and takes the topk best of them as the next frontier, best first, earlier candidate
     on equal scores;
@@ -36,6 +35,7 @@ stated independently, not against numbers the paper prints.
 
 from __future__ import annotations
 
+import math
 from dataclasses import dataclass, field
 from typing import List, Optional, Sequence, Tuple
 
@@ -84,8 +84,8 @@ def draft_topk(x64: np.ndarray, w64: np.ndarray, k: int,
 
 
 def draft_top1_prob(root_logp: float) -> float:
-    """p_draft(top1) of Eq. (2) from the root row's best log-probability (float32 exp)."""
-    return float(np.exp(np.float32(root_logp)))
+    """p_draft(top1) of Eq. (2) from the root row's best log-probability."""
+    return math.exp(float(root_logp))
 
 
 # ----------------------------------------------------------------------------- tree growth
@@ -103,9 +103,9 @@ class DraftTree:
     ndt: int
     tok: List[int] = field(default_factory=list)
     par: List[int] = field(default_factory=list)
-    score: List[np.float32] = field(default_factory=list)
+    score: List[float] = field(default_factory=list)
     front: List[int] = field(default_factory=lambda: [-1])
-    front_score: List[np.float32] = field(default_factory=lambda: [np.float32(0.0)])
+    front_score: List[float] = field(default_factory=lambda: [0.0])
     steps: int = 0
 
 
@@ -115,9 +115,9 @@ def draft_tree_init(shape: Sequence[int]) -> DraftTree:
     return DraftTree(nsteps=nsteps, topk=topk, ndt=ndt)
 
 
-def _f32_logp(v) -> np.float32:
-    x = np.float32(v)
-    return np.float32(-np.inf) if np.isnan(x) else x
+def _logp(v) -> float:
+    x = float(v)
+    return -math.inf if math.isnan(x) else x
 
 
 def draft_tree_step(t: DraftTree, ids: np.ndarray, logp: np.ndarray) -> DraftTree:
@@ -125,7 +125,7 @@ def draft_tree_step(t: DraftTree, ids: np.ndarray, logp: np.ndarray) -> DraftTre
 
     ``ids[j]`` / ``logp[j]`` are the top-k (k >= topk) of frontier slot j's draft row, best first.
     Every frontier node gets its topk children, all of which join the pool; a child's score is
-    its parent's score plus its float32 log-probability. The topk best children become the next
+    its parent's score plus its log-probability. The topk best children become the next
     frontier. A tree that has taken its nsteps steps does not change.
     """
     if t.steps >= t.nsteps:
@@ -133,7 +133,7 @@ def draft_tree_step(t: DraftTree, ids: np.ndarray, logp: np.ndarray) -> DraftTre
     cand = []                                         # (score, parent pool index, token)
     for j, f in enumerate(t.front):
         for c in range(t.topk):
-            s = np.float32(t.front_score[j] + _f32_logp(logp[j][c]))
+            s = t.front_score[j] + _logp(logp[j][c])
             cand.append((s, f, int(ids[j][c])))
     base = len(t.tok)
     tok = t.tok + [c[2] for c in cand]

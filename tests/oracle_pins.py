@@ -322,6 +322,97 @@ def check_promotion_cap(orc):
         assert (k0, b0) == _greedy_by_paths(parent, z, d)
 
 
+def _band_enumeration(parent, z, d, path, kappa, T, band):
+    """The quantities behind every decision of a walk, computed by brute force: at each node of
+    [root] + path, the row's top-2 logit gap (second largest over all other ids, Python
+    loops), the gap between the best child's logit and the best logit among children whose
+    token differs from it, and, when the best child's token is not the row argmax and
+    kappa > 0, |g - M - T ln kappa|. Returns (the first decision index with any of them below
+    ``band``, which one it was), or (-1, None)."""
+    n = len(parent)
+    nodes = [0] + list(path)
+    for i, cur in enumerate(nodes):
+        row = [float(v) for v in z[cur]]
+        top, arg = -math.inf, -1
+        for v, x in enumerate(row):
+            if x > top:
+                top, arg = x, v
+        second = max(x for v, x in enumerate(row) if v != arg)
+        quantities = [(top - second, "row")]
+        kids = [c for c in range(1, n) if parent[c] == cur]
+        if kids:
+            gs = {c: row[d[c]] for c in kids}
+            best = kids[0]
+            for c in kids:
+                if gs[c] > gs[best]:
+                    best = c
+            rivals = [gs[c] for c in kids if d[c] != d[best]]
+            if rivals:
+                quantities.append((gs[best] - max(rivals), "sibling"))
+            if d[best] != arg and kappa > 0.0:
+                quantities.append((abs(gs[best] - top - T * math.log(kappa)), "margin"))
+        for q, kind in quantities:
+            if q < band:
+                return i, kind
+    return -1, None
+
+
+def check_walk_bands(orc):
+    """The band finder against a brute-force enumeration of what each walk decision hangs on:
+    row top-2 gaps, sibling gaps between distinct tokens and the margin's distance to T ln
+    kappa, on trees with planted near-ties (inside and outside 1e-3) and planted near-threshold
+    margins, at several kappa and temperatures."""
+    rng = np.random.default_rng(97)
+    band = 1e-3
+    hits = {"none": 0, "root": 0, "deeper": 0, "row": 0, "sibling": 0, "margin": 0}
+    for trial in range(400):
+        n = int(rng.integers(2, 14))
+        parent, z, d = _tree_and_logits(rng, n, 12, distinct_siblings=False)
+        kappa = float(rng.choice([0.0, 0.05, 0.3, 1.0]))
+        T = float(rng.choice([1.0, 0.5, 2.0]))
+        z = z.copy()
+        for cur in range(n):
+            kids = [c for c in range(1, n) if parent[c] == cur]
+            u = float(rng.choice([0.0, 4e-4, 8e-4, 1.5e-3, 3e-3]))
+            kind = rng.choice(["row", "sibling", "margin", "margin"])
+            best = max(kids, key=lambda c: (z[cur, d[c]], -c)) if kids else None
+            if kind == "row" and rng.random() < 0.5:        # a near-tie at the top of the row
+                a = int(np.argmax(z[cur]))
+                other = (a + 1 + int(rng.integers(11))) % 12
+                z[cur, other] = z[cur, a] - u
+            elif kind == "sibling" and len(kids) >= 2:      # a rival sibling just below
+                # distinct tokens other than the row argmax, so the row's own gap stays wide
+                a = int(np.argmax(z[cur]))
+                toks = rng.permutation([v for v in range(12) if v != a])[:len(kids)]
+                for c, v in zip(kids, toks):
+                    d[c] = int(v)
+                best = max(kids, key=lambda c: (z[cur, d[c]], -c))
+                c2 = [c for c in kids if c != best][int(rng.integers(len(kids) - 1))]
+                z[cur, d[c2]] = z[cur, d[best]] - max(u, 1e-4)
+            elif kind == "margin" and best is not None and kappa > 0.0:
+                # the best child's margin next to the threshold, its token made a mismatch
+                # (another child may then be the best)
+                a = int(np.argmax(z[cur]))
+                if d[best] == a:
+                    d[best] = int((a + 1 + rng.integers(11)) % 12)
+                target = z[cur].max() + T * math.log(kappa) + float(rng.choice([-1, 1])) * u
+                if target < z[cur].max():
+                    z[cur, d[best]] = target
+        M, a, L, gap = orc.row_stats(z)
+        g = np.array([np.nan] + [z[parent[c], d[c]] for c in range(1, n)])
+        acc = orc.accept_flags(g, M, a, parent, d, np.full(n, kappa), T)
+        path, k, bonus = orc.walk(0, n, parent, d, g, acc, a)
+        got = orc.walk_bands(0, n, parent, d, g, M, a, gap, kappa, path, band, T)
+        want, why = _band_enumeration(parent, z, d, path, kappa, T, band)
+        assert got == want, (trial, got, want, why, path, kappa, T)
+        hits["none" if want < 0 else ("root" if want == 0 else "deeper")] += 1
+        if why:
+            hits[why] += 1
+    # the planted cases put decisions on both sides of the band, at the root and deeper, and
+    # each of the three quantities decides some of them
+    assert min(hits.values()) >= 20, hits
+
+
 # ----------------------------------------------------------------------------- Eq. (2) signals
 
 def check_draft_confidence(orc):
@@ -390,9 +481,9 @@ def check_breaker(orc):
 
 
 def _shape_by_fractions(conf, rar, d, lo, hi):
-    """Eq. (2) mapping in exact rationals of the float32 inputs: DCS = min(1, conf * rar / d),
-    each member lo + (hi - lo) * DCS, nearest integer with halves down."""
-    f = lambda v: Fraction(float(np.float32(v)))
+    """Eq. (2) mapping in exact rationals of the inputs: DCS = min(1, conf * rar / d), each
+    member lo + (hi - lo) * DCS, nearest integer with halves down."""
+    f = lambda v: Fraction(float(v))
     dcs = min(Fraction(1), f(conf) * f(rar) / f(d))
     out = []
     for a, b in zip(lo, hi):
@@ -426,8 +517,12 @@ def check_tree_shape(orc):
     for prod in sorted(rng.uniform(0.0, 0.6, 200)):
         conf, rar = float(prod), 1.0
         dcs, shape = orc.tree_shape(conf, rar, 0, p)
-        _, want = _shape_by_fractions(conf, rar, 0.5, (3, 4, 4), (7, 1, 8))
-        assert shape == want, (conf, shape, want)
+        want_dcs, want = _shape_by_fractions(conf, rar, 0.5, (3, 4, 4), (7, 1, 8))
+        assert shape == want and abs(dcs - float(want_dcs)) < 1e-15, (conf, shape, want)
+        # the slack is the distance of the nearest member to a half-integer
+        slack = min(abs(float(a + (b - a) * want_dcs) % 1.0 - 0.5)
+                    for a, b in zip((3, 4, 4), (7, 1, 8)))
+        assert abs(orc.tree_shape_slack(dcs, 0, p) - slack) < 1e-12
         if prev is not None:
             assert shape[0] >= prev[0] and shape[2] >= prev[2] and shape[1] <= prev[1]
         prev = shape
@@ -435,6 +530,9 @@ def check_tree_shape(orc):
     q = orc.Params(dcs_divisor=0.25)
     assert orc.tree_shape(0.25, 1.0, 0, q)[1] == (7, 1, 8)
     assert orc.tree_shape(0.9, 0.9, 1, p)[1] == tuple(p.shape_start)
+    assert orc.tree_shape_slack(0.3, 1, p) == math.inf
+    assert orc.tree_shape_slack(0.125, 0, p) == 0.0           # 3.5, 3.625, 4.5: two halves
+    assert abs(orc.tree_shape_slack(0.1, 0, p) - 0.1) < 1e-12  # 3.4, 3.7, 4.4
     # the state update picks the shape from the latest confidence and the updated RAR
     s = orc.state_init(p)
     s = orc.state_update(s, 2, 9, 0.4, p)
@@ -499,7 +597,7 @@ ALL_CHECKS = [
     check_margin_is_probability_ratio, check_margin_with_temperature,
     check_exact_match_always_accepted,
     check_kappa_one_is_strict, check_kappa_zero_reaches_leaf, check_walk_properties,
-    check_len_monotone_in_kappa, check_promotion_cap, check_draft_confidence,
+    check_len_monotone_in_kappa, check_promotion_cap, check_walk_bands, check_draft_confidence,
     check_ema_closed_form, check_ring_mean, check_breaker, check_tree_shape,
     check_verify_end_to_end,
 ]

@@ -5,9 +5,11 @@ Three decoding steps for a batch of four requests:
   p_draft(top1) enters the state (asv_tree_policy) -> pruning (asv_draft_prune) -> tree metadata
   (asv_tree_meta) -> the target LM head and margin rule (asv_verify, which updates RAR, the
   history and the next shape) -> commit (asv_commit; the bonus becomes the next root).
-Every stage is compared with the oracle on the GPU's own inputs to that stage: floats within
-2e-3, integer decisions bit-exact (float32 tree decisions taken on the GPU's float32 values;
-verification outside its 1e-3 bands).
+The oracle runs the same loop on its own values: its own float64 draft top-4, tree growth,
+confidence, walks and policy state. Every stage must match it: floats within 2e-3 (state
+within 1e-5), integer decisions bit-exact outside the 1e-3 bands of verification, the near-tie
+bands of the draft growth and the 1e-4 band of the tree shape. A banded decision is recorded;
+from there on that request's oracle takes the GPU's outcome (at most one request of the four).
 """
 
 from types import SimpleNamespace
@@ -16,7 +18,7 @@ import numpy as np
 import pytest
 
 import oracle
-from harness import compare, compare_state, to_host
+from harness import BAND, compare, compare_state, follow_gpu_history, log_bands, to_host
 from workloads import bf16_normal, bf16_weights, draft_hidden, draft_vocab_map, root_tokens
 
 pytestmark = pytest.mark.gpu
@@ -63,31 +65,41 @@ def test_decode_loop(asv, dev):
     wdd, wtd, vmd = _bf16(Wd, dev), _bf16(Wt, dev), _t(vmap, dev)
     roots = root_tokens(B, Vt)
     committed = np.zeros(B, dtype=np.int32)                 # tokens committed so far
+    followed = set()                  # requests whose oracle took a banded GPU outcome
     for step in range(3):
         print(f"decode step {step}", flush=True)
-        # ---- draft: shapes come from the state the previous verify wrote
-        shapes = [tuple(s.shape) for s in asv.state_fields(state)]
-        assert shapes == [tuple(s.shape) for s in st_ref], (step, shapes)
+        # ---- draft: shapes come from the state the previous verify wrote; the oracle's own
+        # state chain must select the same ones (outside the shape band)
+        got_states = asv.state_fields(state)
+        shape_banded = compare_state(got_states, st_ref, params=p_ref, tag=f"decode {step}")
+        shapes = [tuple(s.shape) for s in got_states]
+        for e in shape_banded:
+            followed.add(e["request"])
         trees_ref = [oracle.draft_tree_init(sh) for sh in shapes]
-        conf = None
+        conf = conf_ref = None
         for s in range(max(sh[0] for sh in shapes)):
             x = draft_hidden(B, H, s, seed=100 + step)
             out = asv.draft_step(_bf16(x, dev), wdd, trees, s, state=state, vocab_map=vmd,
                                  with_conf=(s == 0))
-            ids, logp = out.topk_id.cpu().numpy(), out.topk_logp.cpu().numpy()
+            ref_s = oracle.draft_topk(oracle.widen_bf16(x), wd64, 4, vmap)
             if s == 0:
                 conf = out.draft_conf.cpu().numpy()
-                ref0 = oracle.draft_topk(oracle.widen_bf16(x), wd64, 4, vmap)
+                conf_ref = [oracle.draft_top1_prob(ref_s["logp"][4 * b, 0]) for b in range(B)]
                 for b in range(B):
-                    assert abs(conf[b] - np.exp(ref0["logp"][4 * b, 0])) < 2e-3 * max(
-                        conf[b], 1e-3), (step, b)
-            trees_ref = [oracle.draft_tree_step(t, ids[4 * b:4 * b + len(t.front)],
-                                                logp[4 * b:4 * b + len(t.front)])
+                    assert abs(conf[b] - conf_ref[b]) < 2e-3 * max(conf_ref[b], 1e-3), (step, b)
+            for b, t in enumerate(trees_ref):
+                if t.steps < t.nsteps:
+                    zs = ref_s["zs"][4 * b:4 * b + len(t.front), :t.topk + 1]
+                    gaps = -np.diff(zs, axis=1)
+                    assert not np.any((gaps > 0) & (gaps < BAND)), \
+                        (step, s, b, "a near-tie decides this draft row: pick another seed")
+            trees_ref = [oracle.draft_tree_step(t, ref_s["ids"][4 * b:4 * b + len(t.front)],
+                                                ref_s["logp"][4 * b:4 * b + len(t.front)])
                          for b, t in enumerate(trees_ref)]
         # the step's fresh draft confidence enters the policy state (Eq. (2) at step t)
         asv.tree_policy(state, _t(conf, dev), params)
         for b in range(B):
-            st_ref[b].draft_conf = float(conf[b])
+            st_ref[b].draft_conf = float(conf_ref[b])
         # ---- prune to the verification layout
         n_cap = sum(sh[2] for sh in shapes)
         parent, tok, off, pst = asv.draft_prune(trees, n_cap, _t(roots, dev))
@@ -120,16 +132,12 @@ def test_decode_loop(asv, dev):
         got = to_host(vout)
         ref = oracle.verify(wt64, hid, tok_ref, par_ref, off_ref, tau, None, st_ref, p_ref)
         w = SimpleNamespace(N=N, B=B, parent=par_ref, draft_tok=tok_ref, req_offsets=off_ref)
-        rep = compare(w, ref, got)
+        rep = compare(w, ref, got, tag=f"decode {step}")
         print(f"  N={N} accepted={list(got['accepted_len'])} banded requests "
-              f"{rep.banded_requests}")
-        banded = {b for b in range(B) if int(ref["band_at"][b]) >= 0}
-        # the oracle's history follows the GPU's accepted lengths (equal outside the bands)
-        for b in range(B):
-            lo, hi = int(off_ref[b]), int(off_ref[b + 1])
-            st_ref[b] = oracle.state_update(st_ref[b], int(got["accepted_len"][b]), hi - lo,
-                                            None, p_ref)
-        compare_state(asv.state_fields(state), st_ref, params=p_ref)
+              f"{rep.requests}")
+        # the oracle's own history; a request whose walk was banded follows the GPU's length
+        st_ref = follow_gpu_history(f"decode {step}", ref, got, st_ref, w, p_ref)
+        followed |= rep.banded_ids
         # ---- commit
         c_off, c_tok, c_row, dst, cst = asv.commit(off, tok_d, vout.accepted_len,
                                                    vout.accepted_path, vout.bonus_token,
@@ -146,5 +154,9 @@ def test_decode_loop(asv, dev):
         # the next step: the bonus is the new root; positions advance by what was committed
         roots = got["bonus_token"].astype(np.int32)
         committed = committed + np.diff(cref["off"]).astype(np.int32)
-        assert not banded or rep.banded_requests == len(banded)
         assert got["accepted_len"][0] >= 1                  # kappa 0 walks to a leaf
+    if followed:
+        log_bands("decode loop", history_follows_gpu=sorted(followed))
+    assert len(followed) <= 1, followed
+    compare_state(asv.state_fields(state), st_ref, banded_requests=followed, params=p_ref,
+                  tag="decode end")

@@ -3,9 +3,13 @@ target forward (asv_tree_meta, asv_commit) with the CPU oracle, through the C AB
 
 Draft top-4: ids bit-exact outside 1e-3 bands around the logit gaps that decide them (banded
 rows must hold a valid top-4 within the band), log-probabilities and log-sum-exp within 2e-3.
-Tree growth and pruning: bit-exact against the oracle fed with the GPU's own float32 top-4
-(both sides take the integer decisions in float32, as the method states them). Tree metadata
-and commit: bit-exact.
+Tree growth and pruning: the oracle grows its own trees from its own float64 top-4 and scores;
+the GPU's trees (tokens, parents, frontier, pruned layout) must match them bit for bit, scores
+within 2e-3 per level. Near-ties (0 < gap < 1e-3) in the oracle's values are handled like the
+verification bands: where one orders a frontier row's topk + 1 best logits, the GPU's ranking,
+checked to lie within the band, is taken for that row (listed); a tree whose best candidate
+scores of a step, or whose pruning cut, sit on a near-tie is listed and no longer compared
+(at most a tenth of the batch). Tree metadata and commit: bit-exact.
 """
 
 import ctypes
@@ -15,7 +19,7 @@ import numpy as np
 import pytest
 
 import oracle
-from harness import BAND, TOL_F
+from harness import BAND, MAX_BANDED_FRACTION, TOL_F, log_bands
 from workloads import (bf16_weights, build_tree, draft_hidden, draft_shapes, draft_vocab_map,
                        root_tokens)
 
@@ -64,6 +68,9 @@ def _check_topk(tag, x_bits, w64, vmap, ids, logp, lse):
     z = np.where(np.isnan(z), -np.inf, z)
     inv = None if vmap is None else {int(t): i for i, t in enumerate(vmap)}
     banded = 0
+    # the oracle's float64 log-probabilities of the ids the GPU ranked, for rows whose ranking
+    # a near-tie decides (the growth then follows the GPU's valid ranking there)
+    ref["gpu_rank_logp"] = np.array(ref["logp"], copy=True)
     for r in range(x64.shape[0]):
         assert abs(lse[r] - ref["lse"][r]) <= TOL_F or lse[r] == ref["lse"][r], (tag, r)
         d_ids = [int(i) if inv is None else inv[int(i)] for i in ids[r]]
@@ -78,6 +85,9 @@ def _check_topk(tag, x_bits, w64, vmap, ids, logp, lse):
             banded += 1
             for j in range(4):
                 assert abs(z[r, d_ids[j]] - zs[j]) <= BAND or z[r, d_ids[j]] == zs[j], (tag, r)
+                with np.errstate(invalid="ignore"):
+                    lp = z[r, d_ids[j]] - ref["lse"][r]
+                ref["gpu_rank_logp"][r, j] = lp if np.isfinite(lp) else -np.inf
         for j in range(4):
             want = z[r, d_ids[j]] - ref["lse"][r]
             if np.isfinite(want):
@@ -202,32 +212,95 @@ def test_draft_packed_weight(asv, dev, B, V, H):
 
 # ----------------------------------------------------------------------------- tree growth
 
-def _oracle_step(trees_ref, ids, logp):
-    """Advance the oracle trees with the GPU's own float32 top-4 of the frontier rows."""
+def _near_tie(values, upto):
+    """True when two of the ``upto`` + 1 largest values (already sorted best first) differ by
+    less than the band without being equal (equal values are ordered the same way on both
+    sides: lowest id, earlier candidate)."""
+    v = [float(x) for x in values[:upto + 1]]
+    return any(0.0 < a - b < BAND for a, b in zip(v, v[1:]) if np.isfinite(a) and np.isfinite(b))
+
+
+def _oracle_step(trees_ref, ref, gpu_ids, banded, adopted, step):
+    """Advance the oracle trees with the oracle's own float64 top-4 of the frontier rows.
+
+    Where a near-tie among a frontier row's topk + 1 best logits decides the ranking of its
+    children, the GPU's ranking (checked to lie within the band) is taken, with the oracle's
+    log-probabilities of those ids, and the row is listed in ``adopted``. A tree whose best
+    candidate scores sit on a near-tie joins ``banded`` (with the reason) and is no longer
+    compared."""
     out = []
     for b, t in enumerate(trees_ref):
-        rows = slice(4 * b, 4 * b + len(t.front))
-        out.append(oracle.draft_tree_step(t, ids[rows], logp[rows].astype(np.float32)))
+        ids = np.array(ref["ids"][4 * b:4 * b + len(t.front)], copy=True)
+        logp = np.array(ref["logp"][4 * b:4 * b + len(t.front)], copy=True)
+        if t.steps < t.nsteps and b not in banded:
+            for j in range(len(t.front)):
+                r = 4 * b + j
+                if _near_tie(ref["zs"][r], t.topk):
+                    ids[j], logp[j] = gpu_ids[r], ref["gpu_rank_logp"][r]
+                    adopted.append(dict(request=b, step=step, row=r))
+            cand = sorted((t.front_score[j] + float(logp[j][c])
+                           for j in range(len(t.front)) for c in range(t.topk)), reverse=True)
+            if _near_tie(cand, t.topk):
+                banded[b] = f"step {step}: near-tie among the best candidate scores"
+        out.append(oracle.draft_tree_step(t, ids, logp))
     return out
 
 
-def _compare_trees(asv, trees, trees_ref, front_tok, grew, tag):
+def _compare_trees(asv, trees, trees_ref, front_tok, grew, banded, tag):
     got = asv.draft_tree_fields(trees)
     for b, (g, t) in enumerate(zip(got, trees_ref)):
         P = len(t.tok)
         assert (g.nsteps, g.topk, g.ndt) == (t.nsteps, t.topk, t.ndt), (tag, b)
         assert g.status == 0 and g.steps == t.steps and g.n_pool == P, (tag, b, g.n_pool, P)
+        nf = len(t.front)
+        assert g.n_front == nf, (tag, b)
+        if b in banded:
+            continue
         assert list(g.tok[:P]) == t.tok, (tag, b)
         assert list(g.par[:P]) == t.par, (tag, b)
-        assert np.array_equal(np.array(g.score[:P], np.float32), np.array(t.score, np.float32))
-        nf = len(t.front)
-        assert g.n_front == nf and list(g.front[:nf]) == t.front, (tag, b)
-        assert np.array_equal(np.array(g.front_score[:nf], np.float32),
-                              np.array(t.front_score, np.float32))
+        tol = TOL_F * max(1, t.steps)
+        assert np.allclose(np.array(g.score[:P], np.float64), np.array(t.score), rtol=0,
+                           atol=tol), (tag, b)
+        assert list(g.front[:nf]) == t.front, (tag, b)
+        assert np.allclose(np.array(g.front_score[:nf], np.float64), np.array(t.front_score),
+                           rtol=0, atol=tol), (tag, b)
         # a tree that grew this step reports its new frontier's tokens, any other -1s
         want_tok = [t.tok[q] for q in t.front] if grew[b] else []
         exp = (want_tok + [-1] * 4)[:4]
         assert list(front_tok[b]) == exp, (tag, b, list(front_tok[b]), exp)
+
+
+def _prune_tie(t):
+    """True when the oracle's pruning cut (the ndt - 1 best pool nodes) separates two nodes
+    whose scores are within the band without being equal. A node and its own descendant are
+    not such a pair: log-probabilities are <= 0 in both precisions, so a descendant never
+    scores above its ancestor and equal scores keep the earlier pool entry, the ancestor, on
+    both sides (a peaked draft row gives a child a log-probability near 0, hence a score
+    within 1e-6 of its parent's)."""
+    P = len(t.tok)
+    m = min(t.ndt - 1, P)
+    if m == 0 or m == P:
+        return False
+    order = sorted(range(P), key=lambda q: (-float(t.score[q]), q))
+    kept, dropped = order[:m], order[m:]
+
+    def ancestors(q):
+        out = set()
+        while q >= 0:
+            q = t.par[q]
+            out.add(q)
+        return out
+
+    lo = float(t.score[kept[-1]])
+    for q in dropped:
+        if lo - float(t.score[q]) >= BAND:
+            break
+        anc = ancestors(q)
+        for p in kept:
+            d = float(t.score[p]) - float(t.score[q])
+            if 0.0 < d < BAND and p not in anc:
+                return True
+    return False
 
 
 def _grow_and_prune(asv, dev, B, V, H, shapes=None, shape=None, steps=None, vmap=None,
@@ -242,32 +315,47 @@ def _grow_and_prune(asv, dev, B, V, H, shapes=None, shape=None, steps=None, vmap
     steps = steps or max(int(s[0]) for s in all_shapes) + 1
     wd = _bf16(W, dev)
     vm = None if vmap is None else _t(vmap, dev)
+    banded, adopted = {}, []
     for s in range(steps):
         x = draft_hidden(B, H, s, seed=7) if hidden is None else hidden(s)
         out = asv.draft_step(_bf16(x, dev), wd, trees, s, state=state, shape=shape,
                              vocab_map=vm, with_conf=True)
         ids, logp, lse, ftok, conf = _draft_host(out)
-        _check_topk(f"{tag}s{s}", x, w64, vmap, ids, logp, lse)
+        ref = _check_topk(f"{tag}s{s}", x, w64, vmap, ids, logp, lse)
         if s == 0:
             for b in range(B):
-                assert conf[b] == np.exp(np.float32(logp[4 * b, 0])) or \
-                    abs(conf[b] - np.exp(np.float64(logp[4 * b, 0]))) < 1e-6
+                want = oracle.draft_top1_prob(ref["logp"][4 * b, 0])
+                assert abs(conf[b] - want) <= 2e-3 * max(want, 1e-3), (b, conf[b], want)
         before = [t.steps for t in trees_ref]
-        trees_ref = _oracle_step(trees_ref, ids, logp)
+        trees_ref = _oracle_step(trees_ref, ref, ids, banded, adopted, s)
         grew = [t.steps > n for t, n in zip(trees_ref, before)]
-        _compare_trees(asv, trees, trees_ref, ftok, grew, f"{tag}s{s}")
+        _compare_trees(asv, trees, trees_ref, ftok, grew, banded, f"{tag}s{s}")
     roots = root_tokens(B, 1000)
     n_cap = sum(t.ndt for t in trees_ref)
     parent, tok, off, status = asv.draft_prune(trees, n_cap, _t(roots, dev))
     torch.cuda.synchronize()
+    for b, t in enumerate(trees_ref):
+        if b not in banded and _prune_tie(t):
+            banded[b] = "near-tie at the pruning cut"
     pruned = [oracle.draft_tree_prune(t, int(r)) for t, r in zip(trees_ref, roots)]
     par_ref, tok_ref, off_ref = oracle.draft_trees_to_batch(pruned)
     off = off.cpu().numpy()
-    assert list(off) == list(off_ref), (tag, list(off), list(off_ref))
-    n = int(off[-1])
-    assert list(parent.cpu().numpy()[:n]) == list(par_ref), tag
-    assert list(tok.cpu().numpy()[:n]) == list(tok_ref), tag
+    assert list(off) == list(off_ref), (tag, list(off), list(off_ref))   # sizes fix the layout
+    par_g, tok_g = parent.cpu().numpy(), tok.cpu().numpy()
+    for b in range(B):
+        lo, hi = int(off[b]), int(off[b + 1])
+        assert par_g[lo] == -1 and all(lo <= par_g[c] < c for c in range(lo + 1, hi)), (tag, b)
+        if b in banded:
+            continue
+        assert list(par_g[lo:hi]) == list(par_ref[lo:hi]), (tag, b)
+        assert list(tok_g[lo:hi]) == list(tok_ref[lo:hi]), (tag, b)
     assert not status.cpu().numpy().any()
+    if banded or adopted:
+        log_bands(tag, draft_trees=[dict(request=b, why=why) for b, why in banded.items()],
+                  draft_rows_ranked_by_gpu=adopted)
+        print(f"[{tag}] banded draft trees: {banded}; rows ranked within the band by the "
+              f"GPU: {len(adopted)}", flush=True)
+    assert len(banded) <= max(1, MAX_BANDED_FRACTION * B), (tag, banded)
     return trees, trees_ref
 
 
@@ -515,7 +603,7 @@ def test_commit_bad_path_on_first_request(asv, dev):
 def test_draft_full_size(asv, dev, name):
     """The bench workloads (H=4096, 32000 draft ids mapped into the 128256-id target vocabulary,
     trees (3,4,4)) in bench.py's launch configuration: every row's top-4 against the oracle, then
-    three growth steps and pruning bit-exact against the oracle fed with the GPU's values."""
+    three growth steps and pruning bit-exact against the oracle's own trees."""
     from workloads import make_draft_workload
     dw = make_draft_workload(name)
     print(f"case {name}", flush=True)

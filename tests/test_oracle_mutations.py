@@ -119,12 +119,11 @@ def _shape_uses_ring_mean(s, acc_len, n, conf, p):
 
 
 def _shape_halves_up(conf, rar, breaker, p):
-    f = np.float32
-    dcs = min(f(1.0), f(f(f(conf) * f(rar)) / f(p.dcs_divisor)))
+    dcs = min(1.0, conf * rar / p.dcs_divisor)
     if breaker:
-        return float(dcs), tuple(p.shape_start)
-    return float(dcs), tuple(int(math.floor(float(f(f(lo) + f(f(hi - lo) * dcs))) + 0.5))
-                             for lo, hi in zip(p.shape_lo, p.shape_hi))
+        return dcs, tuple(p.shape_start)
+    return dcs, tuple(int(math.floor(lo + (hi - lo) * dcs + 0.5))
+                      for lo, hi in zip(p.shape_lo, p.shape_hi))
 
 
 def _shape_ends_swapped(conf, rar, breaker, p):
@@ -135,12 +134,54 @@ def _shape_ends_swapped(conf, rar, breaker, p):
 
 
 def _shape_no_saturation(conf, rar, breaker, p):
-    f = np.float32
-    dcs = f(f(f(conf) * f(rar)) / f(p.dcs_divisor))
+    dcs = conf * rar / p.dcs_divisor
     if breaker:
-        return float(dcs), tuple(p.shape_start)
-    return float(dcs), tuple(int(math.ceil(float(f(f(lo) + f(f(hi - lo) * dcs))) - 0.5))
-                             for lo, hi in zip(p.shape_lo, p.shape_hi))
+        return dcs, tuple(p.shape_start)
+    return dcs, tuple(int(math.ceil(lo + (hi - lo) * dcs - 0.5))
+                      for lo, hi in zip(p.shape_lo, p.shape_hi))
+
+
+def _slack_from_integers(dcs, breaker, p):
+    # distance to the nearest integer instead of the nearest half-integer
+    if breaker:
+        return math.inf
+    return min(abs(x - round(x)) for x in (lo + (hi - lo) * dcs
+                                           for lo, hi in zip(p.shape_lo, p.shape_hi)))
+
+
+def _bands_always_first(root, end, parent, d, g, M, a, gap, kappa, path, band=1e-3,
+                        temperature=1.0):
+    return 0
+
+
+def _bands_never(root, end, parent, d, g, M, a, gap, kappa, path, band=1e-3, temperature=1.0):
+    return -1
+
+
+def _bands_off_by_one(root, end, parent, d, g, M, a, gap, kappa, path, band=1e-3,
+                      temperature=1.0):
+    i = ORIG["walk_bands"](root, end, parent, d, g, M, a, gap, kappa, path, band, temperature)
+    return i + 1 if i >= 0 else -1
+
+
+def _bands_no_sibling_check(root, end, parent, d, g, M, a, gap, kappa, path, band=1e-3,
+                            temperature=1.0):
+    kids = orc._children(parent, root, end)
+    for i, cur in enumerate([root] + list(path)):
+        if gap[cur] < band:
+            return i
+        if not kids[cur]:
+            continue
+        best = max(kids[cur], key=lambda c: (g[c], -c))
+        if d[best] != a[cur] and kappa > 0.0:
+            if abs((g[best] - M[cur]) - temperature * math.log(kappa)) < band:
+                return i
+    return -1
+
+
+def _bands_ignore_temperature(root, end, parent, d, g, M, a, gap, kappa, path, band=1e-3,
+                              temperature=1.0):
+    return ORIG["walk_bands"](root, end, parent, d, g, M, a, gap, kappa, path, band, 1.0)
 
 
 def _widen_truncating(bits):
@@ -148,7 +189,8 @@ def _widen_truncating(bits):
 
 
 ORIG = {name: getattr(orc, name) for name in
-        ("row_stats", "walk", "state_update", "accept_flags", "logits", "tree_shape")}
+        ("row_stats", "walk", "state_update", "accept_flags", "logits", "tree_shape",
+         "walk_bands")}
 
 MUTANTS = {
     "accept_uses_own_row": ("accept_flags", _accept_own_row),
@@ -171,6 +213,12 @@ MUTANTS = {
     "shape_halves_up": ("tree_shape", _shape_halves_up),
     "shape_ends_swapped": ("tree_shape", _shape_ends_swapped),
     "shape_not_saturated": ("tree_shape", _shape_no_saturation),
+    "shape_slack_to_integers": ("tree_shape_slack", _slack_from_integers),
+    "bands_always_first_decision": ("walk_bands", _bands_always_first),
+    "bands_never": ("walk_bands", _bands_never),
+    "bands_off_by_one": ("walk_bands", _bands_off_by_one),
+    "bands_without_sibling_check": ("walk_bands", _bands_no_sibling_check),
+    "bands_ignore_temperature": ("walk_bands", _bands_ignore_temperature),
 }
 
 

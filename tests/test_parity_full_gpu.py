@@ -8,6 +8,7 @@ the raw inputs and compared with both the table and the GPU.
 """
 
 import hashlib
+import json
 import os
 
 import numpy as np
@@ -15,7 +16,7 @@ import pytest
 
 import oracle
 from oracle.asv_oracle import finish
-from harness import TOL_F, compare, compare_state, device_inputs, to_host
+from harness import MAX_BANDED_FRACTION, TOL_F, compare, compare_state, device_inputs, to_host
 from workloads import CONFIGS, make_workload
 
 pytestmark = pytest.mark.gpu
@@ -95,10 +96,16 @@ def _live_rows(w, W, rows):
     return M, a, L, z
 
 
-def _report(name, rep):
+def _report(name, rep, B):
     print(f"[full] {name}: clean requests {rep.clean_requests}, banded requests "
-          f"{rep.banded_requests}, banded rows {rep.banded_rows}, banded nodes "
-          f"{rep.banded_nodes}", flush=True)
+          f"{rep.requests} (request, decision, node), banded rows {rep.banded_rows}, banded "
+          f"nodes {rep.banded_nodes}", flush=True)
+    assert rep.banded_requests <= MAX_BANDED_FRACTION * B, (name, rep.requests)
+
+
+def _band_list(key):
+    with open(os.path.join(GOLDEN, "band_lists.json")) as f:
+        return json.load(f)[key]
 
 
 @pytest.mark.parametrize("tau", [0.1, 0.3])
@@ -107,17 +114,18 @@ def test_full_llama_b1(asv, dev, tau):
     w, W = _workload(1, 0, tab)
     taus = np.full(w.B, tau, dtype=np.float32)
     got = _gpu(asv, w, W, dev, taus)
-    rep = compare(w, _ref(w, tab, 0, taus), got)
-    _report(f"cfg1 tau={tau}", rep)
+    rep = compare(w, _ref(w, tab, 0, taus), got, tag=f"cfg1 tau={tau}")
+    _report(f"cfg1 tau={tau}", rep, w.B)
+    assert rep.requests == _band_list(f"cfg1_tau{tau}")["requests"]
 
 
 def test_full_compute_b32x64(asv, dev):
     tab = _table(3)
     w, W = _workload(3, 0, tab)
     got = _gpu(asv, w, W, dev)
-    rep = compare(w, _ref(w, tab, 0), got)
-    _report("cfg3", rep)
-    assert rep.clean_requests >= 0.8 * w.B
+    rep = compare(w, _ref(w, tab, 0), got, tag="cfg3")
+    _report("cfg3", rep, w.B)
+    assert rep.requests == _band_list("cfg3_tau0.3")["requests"]
 
 
 @pytest.mark.parametrize("tau", [0.05, 0.1, 0.3, 1.0])
@@ -126,30 +134,57 @@ def test_full_sweep_b64(asv, dev, tau):
     w, W = _workload(4, 0, tab)
     taus = np.full(w.B, tau, dtype=np.float32)
     got = _gpu(asv, w, W, dev, taus)
-    rep = compare(w, _ref(w, tab, 0, taus), got)
-    _report(f"cfg4 tau={tau}", rep)
+    rep = compare(w, _ref(w, tab, 0, taus), got, tag=f"cfg4 tau={tau}")
+    _report(f"cfg4 tau={tau}", rep, w.B)
+    assert rep.requests == _band_list(f"cfg4_tau{tau}")["requests"]
 
 
 def test_full_qwen_b8_32_steps(asv, dev):
-    """Adaptive trees with draft logits over 32 steps: the window-16 history wraps twice."""
+    """Adaptive trees with draft logits over 32 steps: the window-16 history wraps twice. The
+    GPU's policy state is compared with the oracle's own state chain (its own walks, its own
+    float64 confidence and score) after every step. After step 16 the state bytes are copied
+    to the host and into a fresh device tensor, and the remaining steps run on both states:
+    the resumed run must give the uninterrupted run's outputs and state bit for bit (the
+    per-request state of Sec. 3.3 is plain bytes that a serving engine may checkpoint)."""
+    import torch
     tab = _table(2)
     p = oracle.Params()
     st_ref = None
     st_gpu = asv.state_init(CONFIGS[2]["B"], asv.make_params(), device=dev)
+    st_resumed = None
     banded = set()
-    for step in range(int(tab["steps"])):
+    banded_steps = 0
+    steps = int(tab["steps"])
+    for step in range(steps):
         w, W = _workload(2, step, tab)
         if st_ref is None:
             st_ref = [oracle.state_init(p) for _ in range(w.B)]
         ref = _ref(w, tab, step, state=st_ref, params=p)
         got = _gpu(asv, w, W, dev, state=st_gpu)
-        rep = compare(w, ref, got)
-        banded |= {b for b in range(w.B) if ref["band_at"][b] >= 0}
+        rep = compare(w, ref, got, tag=f"cfg2 step={step}")
+        assert rep.requests == _band_list(f"cfg2_step{step}")["requests"], step
+        banded_steps += rep.banded_requests
+        banded |= rep.banded_ids
         st_ref = ref["state"]
         # a request whose walk was ever banded may legitimately carry a different history
-        compare_state(asv.state_fields(st_gpu), st_ref, banded_requests=banded)
+        compare_state(asv.state_fields(st_gpu), st_ref, banded_requests=banded, params=p,
+                      tag=f"cfg2 step={step}")
+        if st_resumed is not None:
+            again = _gpu(asv, w, W, dev, state=st_resumed)
+            for k, v in got.items():
+                if v is not None:
+                    sel = w.parent >= 0 if k == "drafted_logit" else slice(None)
+                    assert np.array_equal(again[k][sel], v[sel], equal_nan=True), (step, k)
+            assert torch.equal(st_resumed, st_gpu), step
+        if step == steps // 2 - 1:
+            # checkpoint: the state's bytes through host memory into a fresh device tensor
+            saved = st_gpu.cpu().numpy().tobytes()
+            st_resumed = torch.from_numpy(
+                np.frombuffer(saved, dtype=np.uint8).reshape(w.B, -1).copy()).to(dev)
         print(f"[full] cfg2 step {step}: N={w.N} len={list(got['accepted_len'])} "
-              f"banded={rep.banded_requests}", flush=True)
+              f"banded={rep.requests}", flush=True)
+    assert st_resumed is not None
+    assert banded_steps <= MAX_BANDED_FRACTION * steps * CONFIGS[2]["B"], banded_steps
 
 
 @pytest.mark.parametrize("cfg", [1, 3, 4, 2])
@@ -173,16 +208,18 @@ def test_full_live_sample(asv, dev, cfg):
             assert abs(got["drafted_logit"][c] - z[i, w.draft_tok[c]]) < TOL_F
 
 
-@pytest.mark.parametrize("cfg", [1, 3, 2])
-def test_full_packed_weight(asv, dev, cfg):
-    """The packed LM-head weight at full size: parity with the oracle's tables, and every
-    output bit for bit equal to the row-major weight's."""
+@pytest.mark.parametrize("cfg,tau", [(1, None), (3, None), (2, None), (4, 0.05), (4, 0.1),
+                                     (4, 0.3), (4, 1.0)])
+def test_full_packed_weight(asv, dev, cfg, tau):
+    """The packed LM-head weight at full size, as bench.py times it: parity with the oracle's
+    tables, and every output bit for bit equal to the row-major weight's."""
     tab = _table(cfg)
     w, W = _workload(cfg, 0, tab)
-    got = _gpu(asv, w, W, dev, packed=True)
-    rep = compare(w, _ref(w, tab, 0), got)
-    _report(f"cfg{cfg} packed weight", rep)
-    base = _gpu(asv, w, W, dev)
+    taus = None if tau is None else np.full(w.B, tau, dtype=np.float32)
+    got = _gpu(asv, w, W, dev, taus, packed=True)
+    rep = compare(w, _ref(w, tab, 0, taus), got, tag=f"cfg{cfg} tau={tau} packed")
+    _report(f"cfg{cfg} tau={tau} packed weight", rep, w.B)
+    base = _gpu(asv, w, W, dev, taus)
     nonroot = w.parent >= 0                 # drafted_logit is unspecified at roots
     for k, v in base.items():
         if v is not None:

@@ -11,8 +11,8 @@ import numpy as np
 import pytest
 
 import oracle
-from harness import compare, compare_state, device_inputs, reference, resolve_with_oracle, \
-    to_host
+from harness import SHAPE_BAND, compare, compare_state, device_inputs, follow_gpu_history, \
+    reference, resolve_with_oracle, to_host
 from workloads import build_tree, custom_workload, make_workload
 
 pytestmark = pytest.mark.gpu
@@ -161,7 +161,7 @@ def test_parity_small(asv, dev, name, tau):
     taus = None if tau is None else np.full(w.B, tau, dtype=np.float32)
     ref = reference(w, w64, tau=taus)
     got = _run(asv, w, W, dev, tau=taus, k1_tile=CASE_TILE.get(name, 0))
-    rep = compare(w, ref, got)
+    rep = compare(w, ref, got, tag=f"{name} tau={tau}")
     print(f"  {rep}", flush=True)
     if tau == 0.0:
         assert np.all(got["accept"] == 1)
@@ -398,17 +398,13 @@ def test_history_state_over_steps(asv, dev, n_req):
             w.tau[:] = 1.0
         ref = reference(w, w64, state=st_ref, params=p)
         got = _run(asv, w, W, dev, state=st_gpu)
-        compare(w, ref, got)
+        tag = f"history n_req={n_req} step={step}"
+        compare(w, ref, got, tag=tag)
         # A request whose walk passed a decision inside the float64 tolerance bands may
         # legitimately accept a different length; its expected state is the oracle's update
-        # applied to the length the GPU accepted.
-        new_ref = list(ref["state"])
-        for b in np.flatnonzero(ref["band_at"] >= 0):
-            n_b = int(w.req_offsets[b + 1] - w.req_offsets[b])
-            new_ref[b] = oracle.state_update(st_ref[b], int(got["accepted_len"][b]), n_b,
-                                             float(ref["draft_conf"][b]), p)
-        st_ref = new_ref
-        compare_state(asv.state_fields(st_gpu), st_ref)
+        # applied to the length the GPU accepted (listed, at most a tenth of the batch).
+        st_ref = follow_gpu_history(tag, ref, got, st_ref, w, p, conf=ref["draft_conf"])
+        compare_state(asv.state_fields(st_gpu), st_ref, params=p, tag=tag)
         if step == 10:   # fifth consecutive zero-accept step
             assert all(s.breaker == 1 for s in st_ref)
         if 6 <= step < 10:
@@ -416,9 +412,10 @@ def test_history_state_over_steps(asv, dev, n_req):
 
 
 def test_tree_policy_entry_point(asv, dev):
-    """asv_tree_policy against the oracle's float32 decision (Sec. 3.3, Eq. (2)): fresh
-    confidences including exact half-way points of the shape ranges, the stored confidence when
-    none is given, a non-default divisor and range, and breaker-flagged requests."""
+    """asv_tree_policy against the float64 oracle (Sec. 3.3, Eq. (2)): fresh confidences
+    including exact half-way points of the shape ranges (exact in both precisions, compared
+    without bands), the stored confidence when none is given, a non-default divisor and range,
+    and breaker-flagged requests. Elsewhere a shape within 1e-4 of a half-integer is banded."""
     import ctypes
     import torch
     B = 600
@@ -445,10 +442,16 @@ def test_tree_policy_entry_point(asv, dev):
         asv.tree_policy(st, torch.from_numpy(conf).to(dev), cp)
         torch.cuda.synchronize()
         got = asv.state_fields(st)
+        banded = []
         for b in range(B):
             dcs, shape = oracle.tree_shape(float(conf[b]), float(rar[b]), int(brk[b]), params)
-            assert got[b].draft_conf == conf[b] and got[b].dcs == np.float32(dcs), b
+            assert got[b].draft_conf == conf[b], b
+            assert abs(got[b].dcs - dcs) <= 1e-6 * max(1.0, dcs), (b, got[b].dcs, dcs)
+            if b >= 17 and oracle.tree_shape_slack(dcs, int(brk[b]), params) < SHAPE_BAND:
+                banded.append(b)
+                continue
             assert tuple(got[b].shape) == shape, (b, tuple(got[b].shape), shape)
+        assert len(banded) <= B // 100, banded
         # without a fresh confidence the stored one is used
         asv.tree_policy(st, None, cp)
         torch.cuda.synchronize()

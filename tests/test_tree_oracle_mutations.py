@@ -8,7 +8,8 @@ import oracle.tree_oracle as tor
 from tree_pins import ALL_TREE_CHECKS
 
 ORIG = {name: getattr(tor, name) for name in
-        ("draft_topk", "draft_tree_step", "draft_tree_prune", "tree_meta", "commit")}
+        ("draft_topk", "draft_tree_step", "draft_tree_prune", "tree_meta", "commit",
+         "draft_trees_to_batch")}
 
 
 def _topk_highest_id_on_ties(x64, w64, k, vocab_map=None):
@@ -35,7 +36,7 @@ def _topk_map_before_ranking(x64, w64, k, vocab_map=None):
 def _step_own_logp_only(t, ids, logp):
     zero = tor.DraftTree(nsteps=t.nsteps, topk=t.topk, ndt=t.ndt, tok=t.tok, par=t.par,
                          score=t.score, front=t.front,
-                         front_score=[np.float32(0.0)] * len(t.front), steps=t.steps)
+                         front_score=[0.0] * len(t.front), steps=t.steps)
     return ORIG["draft_tree_step"](zero, ids, logp)
 
 
@@ -112,6 +113,17 @@ def _commit_drops_root_row(path, acc, bonus, tok, off):
     return out
 
 
+def _batch_local_parents(pruned):
+    par, tok, off = ORIG["draft_trees_to_batch"](pruned)
+    lo = np.repeat(off[:-1], np.diff(off))
+    return np.where(par >= 0, par - lo, -1), tok, off      # parents left request-local
+
+
+def _batch_offsets_shifted(pruned):
+    par, tok, off = ORIG["draft_trees_to_batch"](pruned)
+    return par, tok, np.concatenate([off[1:], [off[-1]]])  # offsets one request late
+
+
 MUTANTS = {
     "topk_highest_id_on_ties": ("draft_topk", _topk_highest_id_on_ties),
     "topk_logp_against_max": ("draft_topk", _topk_logp_against_max),
@@ -125,6 +137,8 @@ MUTANTS = {
     "meta_depth_counts_self": ("tree_meta", _meta_depth_counts_self),
     "commit_without_bonus": ("commit", _commit_without_bonus),
     "commit_drops_root_row": ("commit", _commit_drops_root_row),
+    "batch_parents_left_local": ("draft_trees_to_batch", _batch_local_parents),
+    "batch_offsets_shifted": ("draft_trees_to_batch", _batch_offsets_shifted),
 }
 
 

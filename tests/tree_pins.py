@@ -147,14 +147,14 @@ def check_draft_tree_chain(tor):
 
 def _beam_by_levels(logp_of, nsteps, topk, ndt):
     """Independent statement of the growth on the complete topk-ary tree: a node is a tuple of
-    child ranks, its score the float32 sum of the log-probabilities along it; level d + 1
-    holds the children of the topk best nodes of level d; the result is the set of the ndt - 1
-    best nodes of all levels."""
-    level = [((c,), np.float32(logp_of(())[c])) for c in range(topk)]
+    child ranks, its score the sum of the log-probabilities along it; level d + 1 holds the
+    children of the topk best nodes of level d; the result is the set of the ndt - 1 best
+    nodes of all levels."""
+    level = [((c,), float(logp_of(())[c])) for c in range(topk)]
     pool = list(level)
     for _ in range(1, nsteps):
         beam = sorted(level, key=lambda e: -float(e[1]))[:topk]
-        level = [(node + (c,), np.float32(s + np.float32(logp_of(node)[c])))
+        level = [(node + (c,), s + float(logp_of(node)[c]))
                  for node, s in beam for c in range(topk)]
         pool += level
     keep = sorted(pool, key=lambda e: -float(e[1]))[:ndt - 1]
@@ -202,6 +202,33 @@ def check_draft_tree_levels(tor):
                 j = par[j]
             got.add(tuple(reversed(path)))
         assert got == want, (trial, sorted(got), sorted(want))
+
+
+def check_trees_to_batch(tor):
+    """Per-request pruned trees laid out as verification reads them, against hand-built global
+    parent ids: request b's local node i becomes row off[b] + i, roots keep -1."""
+    pruned = [dict(parent=np.array([-1, 0, 0, 1]), tok=np.array([7, 3, 4, 5])),
+              dict(parent=np.array([-1]), tok=np.array([9])),
+              dict(parent=np.array([-1, 0, 1, 1, 0]), tok=np.array([1, 2, 3, 6, 8]))]
+    par, tok, off = tor.draft_trees_to_batch(pruned)
+    assert list(off) == [0, 4, 5, 10]
+    assert list(par) == [-1, 0, 0, 1, -1, -1, 5, 6, 6, 5]
+    assert list(tok) == [7, 3, 4, 5, 9, 1, 2, 3, 6, 8]
+    par, tok, off = tor.draft_trees_to_batch([])
+    assert list(off) == [0] and len(par) == len(tok) == 0
+    # every row's parent lies in its own request, before it
+    rng = np.random.default_rng(3)
+    trees = []
+    for n in rng.integers(1, 9, 12):
+        trees.append(dict(parent=np.array([-1] + [int(rng.integers(c)) for c in range(1, n)]),
+                          tok=rng.integers(0, 100, n)))
+    par, tok, off = tor.draft_trees_to_batch(trees)
+    for b, t in enumerate(trees):
+        lo, hi = int(off[b]), int(off[b + 1])
+        assert hi - lo == len(t["parent"]) and par[lo] == -1
+        assert all(lo <= par[c] < c for c in range(lo + 1, hi))
+        assert list(par[lo + 1:hi] - lo) == list(t["parent"][1:])
+        assert list(tok[lo:hi]) == list(t["tok"])
 
 
 # ----------------------------------------------------------------------------- tree metadata
@@ -293,6 +320,7 @@ def check_commit_is_root_prefix(tor):
 ALL_TREE_CHECKS = [
     check_topk_brute_force, check_topk_ties_and_argmax, check_topk_probabilities,
     check_topk_map_and_nan, check_draft_tree_golden, check_draft_tree_chain,
-    check_draft_tree_levels, check_tree_meta_golden, check_tree_meta_closure,
+    check_draft_tree_levels, check_trees_to_batch, check_tree_meta_golden,
+    check_tree_meta_closure,
     check_commit_golden, check_commit_is_root_prefix,
 ]

@@ -15,6 +15,7 @@ from .synth import (  # noqa: F401
     build_tree,
     custom_workload,
     draft_choices,
+    make_trees,
     make_workload,
     resolve_drafts,
     round_to_bf16_bits,

@@ -319,6 +319,15 @@ def custom_workload(name: str, H: int, V: int, trees, tau, *, seed: int,
                     w_std, w_tag)
 
 
+def make_trees(cfg: int, step: int = 0):
+    """The seeded trees of configuration ``cfg`` at decode step ``step`` alone, as
+    (req_offsets, parent, depth): the same values make_workload draws, without the hidden
+    states and logits."""
+    c = CONFIGS[cfg]
+    trng = np.random.default_rng([BASE_SEED, cfg, step, _S_TREE])
+    return _pack([build_tree(c["trees"], trng, b) for b in range(c["B"])])
+
+
 def make_workload(cfg: int, step: int = 0, tau: Optional[float] = None) -> Workload:
     """The seeded inputs of synthetic configuration ``cfg`` at decode step ``step``."""
     c = CONFIGS[cfg]
