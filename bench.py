@@ -395,27 +395,35 @@ def measured_draft_traffic(name: str):
     return e.get("bytes_per_launch")
 
 
-def cpu_baseline(w, W, budget_s: float = 12.0) -> dict:
-    """The float64 oracle on the same step, repeated until about ``budget_s`` of CPU work."""
+def cpu_baseline(w, W, budget_s: float = 12.0, requests: int = 0) -> dict:
+    """The float64 oracle on the same step, repeated until about ``budget_s`` of CPU work. With
+    ``requests`` > 0 only the first that many requests of the batch (their rows, trees and
+    thresholds) make up the sample, for workloads whose full step takes the oracle longer."""
     import oracle
     try:
         from threadpoolctl import threadpool_info
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     except Exception:  # pragma: no cover
         threads = os.cpu_count() or 1
+    B = w.B if requests <= 0 else min(requests, w.B)
+    n_rows = int(w.req_offsets[B])
+    args = (w.hidden[:n_rows], w.draft_tok[:n_rows], w.parent[:n_rows], w.req_offsets[:B + 1],
+            w.tau[:B], None if w.draft_logits is None else w.draft_logits[:n_rows])
     w64 = oracle.widen_weights(W)
     n, t0 = 0, time.perf_counter()
     while True:
-        oracle.verify(w64, w.hidden, w.draft_tok, w.parent, w.req_offsets, w.tau,
-                      w.draft_logits)
+        oracle.verify(w64, *args)
         n += 1
         if time.perf_counter() - t0 >= budget_s:
             break
     dt = time.perf_counter() - t0
-    return dict(value=round(w.N * n / dt, 2), unit="nodes/s", cores=int(threads), kind="oracle",
-                sample=f"{n} full verify steps of the headline workload ({w.N} rows each; "
-                       f"float64 logits via BLAS, weights pre-widened outside the timing), "
-                       f"{dt:.1f} s")
+    what = (f"{n} full verify steps of the workload ({n_rows} rows each)" if B == w.B else
+            f"{n} verify steps of the first {B} of its {w.B} requests ({n_rows} of "
+            f"{w.N} rows)")
+    return dict(value=round(n_rows * n / dt, 2), unit="nodes/s", cores=int(threads),
+                kind="oracle",
+                sample=f"{what}; float64 logits via BLAS, weights pre-widened outside the "
+                       f"timing; {dt:.1f} s")
 
 
 def measured_ceilings(dev) -> dict:
@@ -502,6 +510,9 @@ def main():
     ap.add_argument("--config", type=int, default=1)
     ap.add_argument("--secondary", default="3")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-row-major", action="store_true",
+                    help="skip the headline step on the row-major [V, H] weight (reported "
+                         "under row_major beside the packed product path)")
     ap.add_argument("--no-draft", action="store_true",
                     help="skip the draft-step measurement (the step before verification)")
     ap.add_argument("--others", default="2,4",
@@ -589,23 +600,37 @@ def main():
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline(w, W)
     del w, W
+    if args.w_layout == "packed" and not args.no_row_major:
+        # the boundary's own input: the same headline step on the row-major [V, H] weight
+        rr, _, _ = measure(args.config, args.steps, args.warmup, dev, hip, layout="row-major")
+        print(f"# cfg{rr['cfg']} row-major weight: {rr['ms_per_step']*1e3:.1f} us/step, "
+              f"K1 {rr['k1_avg_ms']*1e3:.1f} us", file=sys.stderr, flush=True)
+        line["row_major"] = {"workload": rr["name"], "w_layout": "row-major",
+                             "value": round(rr["value"], 1), "unit": "nodes/s",
+                             "ms_per_step": round(rr["ms_per_step"], 4),
+                             "roofline": roofline(rr, ceilings)}
     if args.others != "none":
         from workloads import CONFIGS
         line["other_configs"] = []
         for cfg in (int(x) for x in args.others.split(",")):
-            for tau in (CONFIGS[cfg]["taus"] if cfg == 4 else (None,)):
-                ro, _, _ = measure(cfg, args.steps, args.warmup, dev, hip, tau,
-                                   layout=args.w_layout)
+            for i, tau in enumerate(CONFIGS[cfg]["taus"] if cfg == 4 else (None,)):
+                ro, wo, Wo = measure(cfg, args.steps, args.warmup, dev, hip, tau,
+                                     layout=args.w_layout)
                 print(f"# cfg{cfg} {ro['name']} tau={ro['tau']:.2f}: "
                       f"{ro['ms_per_step']*1e3:.1f} us/step, K1 {ro['k1_avg_ms']*1e3:.1f} us",
                       file=sys.stderr, flush=True)
-                line["other_configs"].append({
+                entry = {
                     "workload": ro["name"], "rows": ro["N"], "requests": ro["B"],
                     "tau": round(ro["tau"], 4), "value": round(ro["value"], 1),
                     "unit": "nodes/s", "ms_per_step": round(ro["ms_per_step"], 4),
                     "mean_accepted_len": round(ro["mean_accepted_len"], 3),
                     "roofline": roofline(ro, ceilings),
-                    "roofline_other_bound": other_bound(ro)})
+                    "roofline_other_bound": other_bound(ro)}
+                if cfg == 4 and i == 0 and not args.no_cpu:
+                    # the largest workload: the oracle on a bounded sample of its requests
+                    entry["cpu_baseline"] = cpu_baseline(wo, Wo, budget_s=10.0, requests=8)
+                del wo, Wo
+                line["other_configs"].append(entry)
     if not args.no_draft:
         line["draft"] = [measure_draft(n, args.steps, args.warmup, dev, hip, not args.no_cpu,
                                        args.w_layout)
