@@ -131,10 +131,11 @@ def _per_call_us(fn, reps: int) -> float:
 
 
 def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents, tau=None,
-            layout: str = "packed"):
+            layout: str = "packed", before_warmup=None):
     """Time asv_verify on configuration `cfg`. With layout "packed" the LM-head weight is
     packed once (asv_pack_lm_head, as at model load; timed alone as pack_ms) and the row-major
-    copy freed before anything is timed; "row-major" passes the [V, H] weight as it is."""
+    copy freed before anything is timed; "row-major" passes the [V, H] weight as it is.
+    ``before_warmup`` runs once the inputs are resident, right before the warm-up steps."""
     import torch
     import paper_2609_02897_amd as asv
     w, c = load_workload(cfg)
@@ -161,6 +162,8 @@ def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents, tau=None,
                    d["tau"], d["draft_logits"], state=state, out=out, workspace=ws,
                    k1_events=k1)
 
+    if before_warmup is not None:
+        before_warmup()
     for _ in range(warmup):
         step()
     # Timed region 1: the throughput. Nothing but the verify calls is enqueued.
@@ -557,7 +560,22 @@ def main():
     asv.load()
     dev = torch.device("cuda:0")
     hip = HipEvents()
-    r, w, W = measure(args.config, args.steps, args.warmup, dev, hip, layout=args.w_layout)
+    # The achievable peaks are measured once the headline's inputs are resident, right before
+    # its warm-up: seconds of streaming reads and MFMA loops, which also leave the GPU's memory
+    # and shader clocks in the working state of a serving loop (the first ~100 steps after an
+    # idle host phase read about 6% slower).
+    ceilings = {}
+
+    def take_ceilings():
+        try:
+            ceilings.update(measured_ceilings(dev))
+            print(f"# measured ceilings: {ceilings}", file=sys.stderr, flush=True)
+        except OSError as e:      # microbenchmark library not built: published peaks only
+            print(f"# measured ceilings unavailable: {e}", file=sys.stderr, flush=True)
+
+    r, w, W = measure(args.config, args.steps, args.warmup, dev, hip, layout=args.w_layout,
+                      before_warmup=take_ceilings)
+    ceilings = ceilings or None
     print(f"# cfg{r['cfg']} {r['name']}: {r['ms_per_step']*1e3:.1f} us/step, "
           f"K1 {r['k1_avg_ms']*1e3:.1f} us, {r['hbm_gbs']:.0f} GB/s, "
           f"{r['mfma_tflops']:.0f} TFLOP/s", file=sys.stderr, flush=True)
@@ -588,12 +606,6 @@ def main():
                              "around_target_forward": r2["around"]}
         w, _ = load_workload(args.config)
         W = w.weights()
-    try:
-        ceilings = measured_ceilings(dev)
-        print(f"# measured ceilings: {ceilings}", file=sys.stderr, flush=True)
-    except OSError as e:      # microbenchmark library not built: published peaks only
-        print(f"# measured ceilings unavailable: {e}", file=sys.stderr, flush=True)
-        ceilings = None
     line["roofline"] = roofline(r, ceilings)
     if "secondary" in line:
         line["secondary"]["roofline"] = roofline(r2, ceilings)
