@@ -532,7 +532,24 @@ def main():
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB five times (the "
                          "reference dispatch for scaling HBM traffic counters) and exit")
+    ap.add_argument("--read-calibration", type=int, default=0, metavar="MIB",
+                    help="only stream-read a buffer of MIB MiB five times back to back (the "
+                         "microbenchmark read; a buffer smaller than the last-level cache is "
+                         "read from it after the first pass) and exit: shows which traffic "
+                         "counters see last-level-cache hits")
     args = ap.parse_args()
+    if args.read_calibration:
+        import torch
+        n = args.read_calibration << 20
+        buf = torch.ones(n // 4, dtype=torch.int32, device="cuda:0")
+        sink = torch.zeros(1 << 16, dtype=torch.int32, device="cuda:0")
+        mb = _microbench_lib()
+        handle = torch.cuda.current_stream().cuda_stream
+        for _ in range(5):
+            assert mb.asvb_stream_read(buf.data_ptr(), n, sink.data_ptr(), 1024, handle) == 0
+        torch.cuda.synchronize()
+        print(json.dumps({"read_calibration_bytes": n, "dispatches": 5}))
+        return
     if args.copy_calibration:
         import torch
         n = args.copy_calibration << 20
