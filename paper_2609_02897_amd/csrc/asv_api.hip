@@ -45,14 +45,25 @@ int launch_status(const char* what) {
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Tile families of K1. Few rows (the weight-streaming regime of small batches) use a 64-row
-// tile so that all rows share one pass over W. Beyond 64 rows the pick minimises an estimate of
-// the launch time: the rounds of workgroups over the CUs times the time of one tile, 62 : 80 :
-// 98 for the 128-, 192- and 256-row tiles (per-round times of the spread loops on MI355X, with
-// the packed weight); ties go to the larger tile. Interleaved comparisons at V = 151936
-// (records bit-identical across the tiles) agree with the estimate at every row count measured
-// from 150 to 3048 rows: e.g. at 540 rows three 192-row tiles beat three 256-row tiles by 17%,
-// at 700 rows three 256-row tiles beat four 192-row tiles by 9%.
+// tile so that all rows share one pass over W. Beyond 64 rows the plan minimises an estimate of
+// the time: the rounds of workgroups over the CUs times the time of one tile, 62 : 80 : 98 for
+// the 128-, 192- and 256-row tiles (per-round times of the spread loops on MI355X, with the
+// packed weight); ties go to the larger tile. Interleaved comparisons at V = 151936 (records
+// bit-identical across the tiles) agree with the single-family estimate at every row count
+// measured from 150 to 3048 rows: e.g. at 540 rows three 192-row tiles beat three 256-row tiles
+// by 17%, at 700 rows three 256-row tiles beat four 192-row tiles by 9%.
+// A plan may split the slabs between two families in two launches: the first n1 slabs on
+// family a, the rest on family b, n1 chosen so that family a fills whole rounds. At 378 rows
+// and V = 151936, for instance, one 192-row family takes 1188 tiles, 4.64 rounds run as 5;
+// 128-row tiles on 85 slabs (255 tiles, one round) and 192-row tiles on the other 509 (1018
+// tiles, four rounds) leave no round a third empty.
 enum class Tile { kRows64, kRows128, kRows192, kRows256 };
+
+struct K1Plan {
+  Tile a, b;       // slabs [0, n1) on tile a, [n1, S) on tile b
+  int n1;          // == S: one launch of tile a
+};
+
 
 // Compute units of the current device, queried once per device.
 int cu_count() {
@@ -69,19 +80,37 @@ int cu_count() {
   return n;
 }
 
-Tile pick_tile(int N, int S, int cus) {
-  if (N <= 64) return Tile::kRows64;
+K1Plan plan_k1(int N, int S, int cus) {
+  if (N <= 64) return K1Plan{Tile::kRows64, Tile::kRows64, S};
   struct Family { Tile tile; int rows; int cost; };
   const Family families[3] = {{Tile::kRows128, 128, 62}, {Tile::kRows192, 192, 80},
                               {Tile::kRows256, 256, 98}};
-  Tile best = Tile::kRows128;
+  auto rounds = [&](int64_t tiles) { return (tiles + cus - 1) / cus; };
+  K1Plan best{Tile::kRows128, Tile::kRows128, S};
   int64_t best_est = INT64_MAX;
   for (const Family& f : families) {
-    const int64_t tiles = (int64_t)((N + f.rows - 1) / f.rows) * S;
-    const int64_t est = (tiles + cus - 1) / cus * f.cost;
+    const int64_t est = rounds((int64_t)((N + f.rows - 1) / f.rows) * S) * f.cost;
     if (est <= best_est) {
       best_est = est;
-      best = f.tile;
+      best = K1Plan{f.tile, f.tile, S};
+    }
+  }
+  // two families: family a fills k whole rounds on its slabs, family b takes the rest; taken
+  // only when strictly better than every single family
+  for (const Family& fa : families) {
+    const int64_t ra = (N + fa.rows - 1) / fa.rows;
+    for (const Family& fb : families) {
+      if (fb.rows == fa.rows) continue;
+      const int64_t rb = (N + fb.rows - 1) / fb.rows;
+      for (int64_t k = 1; k * cus < (int64_t)S * ra; ++k) {
+        const int64_t n1 = k * cus / ra;
+        if (n1 <= 0 || n1 >= S) continue;
+        const int64_t est = rounds(n1 * ra) * fa.cost + rounds((S - n1) * rb) * fb.cost;
+        if (est < best_est) {
+          best_est = est;
+          best = K1Plan{fa.tile, fb.tile, (int)n1};
+        }
+      }
     }
   }
   return best;
@@ -142,15 +171,17 @@ bool params_ok(const asv_params& p) {
   return true;
 }
 
+// K1 over the vocabulary slabs [slab0, slab0 + n_slabs).
 template <int TV, int TR, int WV, int WR, int BK, int NST, int LOOP = 0>
-void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStream_t s) {
+void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStream_t s,
+                   int slab0, int n_slabs) {
   static_assert(TV == kSlab, "tiles span exactly one record slab");
   static_assert(TV == kPackRowsTarget && BK == kPackDepth, "a stage is one packed tile");
   const int RT = (a->N + TR - 1) / TR;
-  const int grid = L.S * RT;
+  const int grid = n_slabs * RT;
   k_lmhead_partial<TV, TR, WV, WR, BK, NST, LOOP><<<grid, WV * WR * kWave, 0, s>>>(
       a->hidden, a->w_lm, a->parent, a->draft_tok, a->req_offsets, a->B, a->N, a->H, a->V,
-      L.S, RT, reinterpret_cast<float*>(ws + L.off_rec_m),
+      L.S, slab0, RT, reinterpret_cast<float*>(ws + L.off_rec_m),
       reinterpret_cast<float*>(ws + L.off_rec_s), reinterpret_cast<int32_t*>(ws + L.off_rec_a),
       a->drafted_logit, reinterpret_cast<int32_t*>(ws + L.off_cnt), a->B + 1,
       a->w_lm_layout == ASV_W_PACKED ? 1 : 0);
@@ -394,20 +425,31 @@ extern "C" int asv_verify_tuned(const asv_verify_args* a, const asv_tuning* tuni
   }
 
   if (int rc = record_event(tu.begin_event, s, "hipEventRecord(begin_event)")) return rc;
-  const Tile tile = tu.tile_rows != 0 ? forced : pick_tile(a->N, L.S, cu_count());
-  switch (tile) {
-    // <vocab rows, tree rows, waves along vocab, waves along rows, K per stage, ring depth,
-    // K loop>, each the fastest of a sweep on MI355X for its row range. The weight-streaming
-    // 64-row tile keeps two workgroups per CU (80 KB of LDS each) with the burst ring; a 3-deep
-    // ring with one workgroup per CU was 0.7% slower in an interleaved comparison over ten
-    // placements of W. The 128-, 192- and 256-row tiles run the spread K loops (copies spaced
-    // between the MFMAs), in interleaved comparisons 28% faster than the burst ring at 378
-    // rows and 20% at 2048 and 3048 rows.
-    case Tile::kRows64: launch_lmhead<256, 64, 4, 1, 64, 2>(a, L, ws, s); break;
-    case Tile::kRows128: launch_lmhead<256, 128, 2, 2, 64, 3, 3>(a, L, ws, s); break;
-    case Tile::kRows192: launch_lmhead<256, 192, 2, 2, 64, 2, 2>(a, L, ws, s); break;
-    case Tile::kRows256: launch_lmhead<256, 256, 2, 2, 64, 2, 2>(a, L, ws, s); break;
-  }
+  const K1Plan plan = tu.tile_rows != 0 ? K1Plan{forced, forced, L.S}
+                                         : plan_k1(a->N, L.S, cu_count());
+  auto launch = [&](Tile tile, int slab0, int n_slabs) {
+    switch (tile) {
+      // <vocab rows, tree rows, waves along vocab, waves along rows, K per stage, ring depth,
+      // K loop>, each the fastest of a sweep on MI355X for its row range. The weight-streaming
+      // 64-row tile keeps two workgroups per CU (80 KB of LDS each) with the burst ring; a
+      // 3-deep ring with one workgroup per CU was 0.7% slower in an interleaved comparison
+      // over ten placements of W. The 128-, 192- and 256-row tiles run the spread K loops
+      // (copies spaced between the MFMAs), in interleaved comparisons 28% faster than the
+      // burst ring at 378 rows and 20% at 2048 and 3048 rows.
+      case Tile::kRows64: launch_lmhead<256, 64, 4, 1, 64, 2>(a, L, ws, s, slab0, n_slabs); break;
+      case Tile::kRows128:
+        launch_lmhead<256, 128, 2, 2, 64, 3, 3>(a, L, ws, s, slab0, n_slabs);
+        break;
+      case Tile::kRows192:
+        launch_lmhead<256, 192, 2, 2, 64, 2, 2>(a, L, ws, s, slab0, n_slabs);
+        break;
+      case Tile::kRows256:
+        launch_lmhead<256, 256, 2, 2, 64, 2, 2>(a, L, ws, s, slab0, n_slabs);
+        break;
+    }
+  };
+  launch(plan.a, 0, plan.n1);
+  if (plan.n1 < L.S) launch(plan.b, plan.n1, L.S - plan.n1);
   if (int rc = launch_status("k_lmhead_partial")) return rc;
   if (int rc = record_event(tu.end_event, s, "hipEventRecord(end_event)")) return rc;
 

@@ -486,15 +486,17 @@ __device__ __forceinline__ void lmhead_tile_spread3(
 }
 
 // LOOP selects the K loop: 0 = the burst ring of lmhead_tile; 2 and 3 = the spread loop of
-// that ring depth (lmhead_tile_spread, lmhead_tile_spread3).
+// that ring depth (lmhead_tile_spread, lmhead_tile_spread3). One launch covers a contiguous
+// range of vocabulary slabs (all of them, or one of two ranges whose tiles differ in height).
 template <int TV, int TR, int WV, int WR, int BK, int NST, int LOOP = 0>
 __global__ __launch_bounds__(WV * WR * kWave, 1)
 void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                       const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
                       const int32_t* __restrict__ req_offsets, int B, int N, int H, int V,
-                      int S, int RT, float* __restrict__ rec_m, float* __restrict__ rec_s,
-                      int32_t* __restrict__ rec_a, float* __restrict__ drafted_logit,
-                      int32_t* __restrict__ done_cnt, int n_cnt, int w_packed) {
+                      int S, int slab0, int RT, float* __restrict__ rec_m,
+                      float* __restrict__ rec_s, int32_t* __restrict__ rec_a,
+                      float* __restrict__ drafted_logit, int32_t* __restrict__ done_cnt,
+                      int n_cnt, int w_packed) {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
   constexpr int T = C::kThreads;
   __shared__ uint4 smem[C::kLds / 16];
@@ -504,9 +506,10 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
   const int wv = wave % WV, wr = wave / WV;
   // clear the per-request completion counters of the finishing kernel that follows
   for (int i = blockIdx.x * T + tid; i < n_cnt; i += gridDim.x * T) done_cnt[i] = 0;
-  // consecutive tiles are the row tiles of one slab, which share the W slab through L2
+  // consecutive tiles are the row tiles of one slab, which share the W slab through L2; this
+  // launch covers slabs slab0 .. slab0 + gridDim.x / RT - 1 of the S slabs
   const int tile = xcd_tile(blockIdx.x, gridDim.x);
-  const int slab = tile / RT;
+  const int slab = slab0 + tile / RT;
   const int rt = tile % RT;
   const int v0 = slab * TV, r0 = rt * TR;
   const int v_end = min(v0 + TV, V);

@@ -201,6 +201,35 @@ def test_every_tile_same_results(asv, dev):
         assert np.allclose(got["row_lse"], base["row_lse"], rtol=1e-6, atol=1e-6), rows
 
 
+@pytest.mark.parametrize("N", [150, 200, 378])
+def test_two_family_plan(asv, dev, N):
+    """At V = 151936 and these row counts the library splits the vocabulary slabs between two
+    LM-head tile families in two launches (on 256 CUs: 128-row tiles on the first slabs, 192-
+    or 256-row tiles on the rest), so that no round of workgroups runs a third empty. Every
+    output equals the single-family runs' bit for bit (the same K order everywhere, and both
+    families merge a slab's record across two waves), and the oracle's."""
+    print(f"[two families] N={N}", flush=True)
+    rng = np.random.default_rng(N)
+    trees, n = [], 0
+    while n < N:
+        t = _rand_tree(rng, min(int(rng.integers(8, 97)), N - n), 8, 4)
+        trees.append(t)
+        n += len(t)
+    w = custom_workload(f"plan{N}", 64, 151936, trees, 0.2, seed=20 + N, w_std=0.16)
+    W = w.weights()
+    w64 = oracle.widen_weights(W)
+    resolve_with_oracle(w, w64)
+    got = _run(asv, w, W, dev, packed=True)
+    compare(w, reference(w, w64), got, tag=f"two families N={N}")
+    nonroot = w.parent >= 0
+    for rows in (128, 192, 256):
+        base = _run(asv, w, W, dev, k1_tile=rows, packed=True)
+        for k, v in base.items():
+            if v is not None:
+                sel = nonroot if k == "drafted_logit" else slice(None)
+                assert np.array_equal(got[k][sel], v[sel], equal_nan=True), (rows, k)
+
+
 @pytest.mark.parametrize("V,H", [(1, 64), (256, 64), (1000, 192), (2 * 256 + 77, 320),
                                  (151936, 4096)])
 def test_pack_layout(asv, dev, V, H):
