@@ -474,13 +474,12 @@ def measured_ceilings(dev) -> dict:
 
 def vendor_reference() -> dict:
     """Context for the roofline fractions: the vendor bf16 GEMM computing only the [N, V]
-    logits of the two bench shapes (no reductions, gather or walk), and the copy bandwidth."""
+    logits of the four verify shapes (no reductions, gather or walk), and the copy bandwidth."""
     import torch
     dev = torch.device("cuda:0")
     g = torch.Generator(device=dev)
     g.manual_seed(0)
-    H, V = 4096, 128256
-    W = (torch.randn(V, H, device=dev, generator=g) * 0.02).to(torch.bfloat16)
+    H = 4096
     out = {}
 
     def timed(fn, reps):
@@ -493,11 +492,14 @@ def vendor_reference() -> dict:
         torch.cuda.synchronize()
         return (time.perf_counter() - t0) / reps
 
-    for N in (60, 2048):
-        X = torch.randn(N, H, device=dev, generator=g).to(torch.bfloat16)
-        sec = timed(lambda: torch.matmul(X, W.t()), 50 if N == 60 else 20)
-        out[f"hipblaslt_logits_n{N}_us"] = round(sec * 1e6, 1)
-        out[f"hipblaslt_logits_n{N}_tflops"] = round(2 * N * V * H / sec / 1e12, 1)
+    for V, rows in ((128256, (60, 2048)), (151936, (378, 3048))):
+        W = (torch.randn(V, H, device=dev, generator=g) * 0.02).to(torch.bfloat16)
+        for N in rows:
+            X = torch.randn(N, H, device=dev, generator=g).to(torch.bfloat16)
+            sec = timed(lambda: torch.matmul(X, W.t()), 50 if N < 1000 else 20)
+            out[f"hipblaslt_logits_n{N}_v{V}_us"] = round(sec * 1e6, 1)
+            out[f"hipblaslt_logits_n{N}_v{V}_tflops"] = round(2 * N * V * H / sec / 1e12, 1)
+        del W
     src = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
     dst = torch.empty_like(src)
     sec = timed(lambda: dst.copy_(src), 20)

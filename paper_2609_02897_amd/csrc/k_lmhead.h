@@ -15,12 +15,14 @@
 // with one barrier per stage; lmhead_tile_spread / lmhead_tile_spread3 place every copy
 // between two MFMAs on a fixed schedule, so the copies never stall a wave's MFMAs (the 128-
 // and 256-row tiles, which are MFMA-bound). 16-byte chunks are XOR-swizzled so that
-// ds_read_b128 in the MFMA operand layout is free of bank conflicts. The MFMA is
-// v_mfma_f32_32x32x16_bf16 with A = W (32 vocabulary rows) and B = X (32 tree rows): each lane
-// then owns one tree row and 16 vocabulary entries of every 32x32 output block, so the
-// per-row reduction is mostly lane-local. Fragments of a later K16 step are read while the
-// current MFMAs run. Every loop accumulates K in increasing order, so all tiles give the same
-// logits bit for bit.
+// ds_read_b128 in the MFMA operand layout is free of bank conflicts. K1 runs
+// v_mfma_f32_16x16x32_bf16 with A = W (16 vocabulary rows) and B = X (16 tree rows): each lane
+// then owns one tree row and 4 vocabulary entries of every 16x16 output block, so the per-row
+// reduction is mostly lane-local, with two cross-lane steps. (The draft LM head, which shares
+// the burst ring, runs v_mfma_f32_32x32x16_bf16: 16 entries of a 32x32 block per lane.) In
+// every comparison made the two shapes gave bit-identical logits; the 16x16x32 form lets the
+// chip hold a higher clock under K1's sustained MFMA load. Fragments of a later K step are read while the current MFMAs run.
+// Every loop accumulates K in increasing order, so all tiles give the same logits bit for bit.
 #pragma once
 
 #include <type_traits>
@@ -31,6 +33,43 @@ namespace asv {
 
 typedef __bf16 bf16x8 __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float f32x16 __attribute__((__vector_size__(16 * sizeof(float))));
+typedef float f32x4 __attribute__((__vector_size__(4 * sizeof(float))));
+
+// The two bf16 MFMA shapes a tile can run on. Both take 8 bf16 of A and of B per lane: lane l
+// holds row (of A) or column (of B) l % kBlock and the 8 consecutive K elements
+// 8 (l / kBlock) .. + 7 of the instruction's K step, so a fragment is one 16-byte LDS read.
+// row_of(lane, e) is the A row (vocabulary entry) of accumulator register e of a lane; its
+// B column (tree row) is lane % kBlock. Within a lane, row_of increases with e.
+// The 16x16x32 form does the same work per K element with a quarter of the accumulator
+// registers per instruction; under sustained load the chip holds a higher shader clock with it.
+struct Mfma32 {   // v_mfma_f32_32x32x16_bf16
+  using Acc = f32x16;
+  static constexpr int kBlock = 32, kK = 16, kRegs = 16;
+  static __device__ __forceinline__ Acc mma(bf16x8 a, bf16x8 b, Acc c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ int row_of(int lane, int e) {
+    return 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+  }
+  // register and lane holding row m (of the block) of tree row p (of the block)
+  static __device__ __forceinline__ int reg_of(int m) { return ((m >> 3) << 2) | (m & 3); }
+  static __device__ __forceinline__ int lane_of(int p, int m) { return p + 32 * ((m >> 2) & 1); }
+};
+struct Mfma16 {   // v_mfma_f32_16x16x32_bf16
+  using Acc = f32x4;
+  static constexpr int kBlock = 16, kK = 32, kRegs = 4;
+  // The empty asm keeps each result in accumulator registers; without it the register
+  // allocator moves the 4-register accumulators between AGPRs and VGPRs on every pass of the
+  // smaller tiles' K loops. It emits no instruction.
+  static __device__ __forceinline__ Acc mma(bf16x8 a, bf16x8 b, Acc c) {
+    Acc d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    asm volatile("" : "+a"(d));
+    return d;
+  }
+  static __device__ __forceinline__ int row_of(int lane, int e) { return 4 * (lane >> 4) + e; }
+  static __device__ __forceinline__ int reg_of(int m) { return m & 3; }
+  static __device__ __forceinline__ int lane_of(int p, int m) { return p + 16 * (m >> 2); }
+};
 
 constexpr int kKAlign = 64;   // H must be a multiple of this (host check)
 
@@ -94,14 +133,15 @@ __device__ __forceinline__ void wait_stage_barrier(int newer) {
   else wait_vm_barrier<0>();
 }
 
-template <int TV, int TR, int WV, int WR, int BK, int NST>
+template <int TV, int TR, int WV, int WR, int BK, int NST, class MF = Mfma32>
 struct LmheadCfg {
   static constexpr int kWaves = WV * WR;
   static constexpr int kThreads = kWaves * kWave;
   static constexpr int kWaveV = TV / WV;        // vocabulary rows per wave
   static constexpr int kWaveR = TR / WR;        // tree rows per wave
-  static constexpr int MV = kWaveV / 32;        // 32x32 blocks per wave, vocab direction
-  static constexpr int MR = kWaveR / 32;        // 32x32 blocks per wave, tree-row direction
+  static constexpr int MV = kWaveV / MF::kBlock;  // MFMA blocks per wave, vocab direction
+  static constexpr int MR = kWaveR / MF::kBlock;  // MFMA blocks per wave, tree-row direction
+  static constexpr int NS = BK / MF::kK;        // MFMA K steps per stage
   static constexpr int CPR = BK / 8;            // 16-byte chunks per staged row
   static constexpr int kRowsPerCopy = 64 / CPR; // rows one 1 KB wave copy fills
   static constexpr int kStageW = TV * BK * 2;   // bytes of W per stage
@@ -112,7 +152,8 @@ struct LmheadCfg {
   static constexpr int kLoads = DW + DX;        // vector-memory ops per lane per stage
   static constexpr int kLds = NST * kStage;
   static constexpr int kCand = 2;               // gather candidates prefetched per thread
-  static_assert(TV % 32 == 0 && TR % 32 == 0, "whole 32x32 MFMA blocks");
+  static_assert(TV % 32 == 0 && TR % 32 == 0 && kWaveV % MF::kBlock == 0 &&
+                kWaveR % MF::kBlock == 0, "whole MFMA blocks");
   static_assert(MV >= 1 && MR >= 1, "tile too small for the wave grid");
   static_assert(BK == 32 || BK == 64, "stage depth");
   static_assert(NST >= 2 && NST <= 5, "ring depth");
@@ -146,13 +187,14 @@ __device__ __forceinline__ int xcd_tile(int bid, int G) {
 // rows are weight-bound or close to it and read W faster with the hint (60 rows: 13% less
 // time), while the larger tiles share each W slab between the row tiles of one XCD through
 // its L2 and keep the default policy (the hint measured within noise there).
-template <int TV, int TR, int WV, int WR, int BK, int NST, bool STREAM_W = (TR <= 128)>
+template <int TV, int TR, int WV, int WR, int BK, int NST, bool STREAM_W = (TR <= 128),
+          class MF = Mfma32>
 struct TileIo {
-  using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
+  using C = LmheadCfg<TV, TR, WV, WR, BK, NST, MF>;
   static constexpr int CPR = C::CPR;
   static constexpr bool kStreamW = STREAM_W;
   const uint4* lds;
-  int lane, wave, wv, wr, lds0, frag_row, frag_half;
+  int lane, wave, wv, wr, lds0, frag_row, frag_grp;
   unsigned w_kstep;             // bytes between the W data of consecutive K stages
   __amdgpu_buffer_rsrc_t w_rsrc, x_rsrc;
   int w_voff[C::DW], x_voff[C::DX];
@@ -164,8 +206,8 @@ struct TileIo {
     wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     wv = wave % WV;
     wr = wave / WV;
-    frag_row = lane & 31;
-    frag_half = lane >> 5;
+    frag_row = lane % MF::kBlock;
+    frag_grp = lane / MF::kBlock;
     lds0 = __builtin_amdgcn_readfirstlane((int)(size_t)smem);
     const int v_end = min(v0 + TV, V);
     const int r_last = min(r0 + TR, N) - 1;
@@ -211,40 +253,46 @@ struct TileIo {
             x_voff[c - C::DW] + ks * BK * 2, x_rsrc);
   }
   // the fragment of W block i (of this wave's vocabulary rows), or of X block j (of its tree
-  // rows), for K16 step s of ring slot `slot`
+  // rows), for MFMA K step s of ring slot `slot`
   __device__ __forceinline__ bf16x8 w_frag(int slot, int s, int i) const {
     const uint4* w = lds + slot * (C::kStage / 16);
     return __builtin_bit_cast(
-        bf16x8, w[swz<CPR>(wv * C::kWaveV + 32 * i + frag_row, 2 * s + frag_half)]);
+        bf16x8, w[swz<CPR>(wv * C::kWaveV + MF::kBlock * i + frag_row,
+                           (MF::kK / 8) * s + frag_grp)]);
   }
   __device__ __forceinline__ bf16x8 x_frag(int slot, int s, int j) const {
     const uint4* x = lds + slot * (C::kStage / 16) + C::kStageW / 16;
     return __builtin_bit_cast(
-        bf16x8, x[swz<CPR>(wr * C::kWaveR + 32 * j + frag_row, 2 * s + frag_half)]);
+        bf16x8, x[swz<CPR>(wr * C::kWaveR + MF::kBlock * j + frag_row,
+                           (MF::kK / 8) * s + frag_grp)]);
   }
 };
 
-template <int MV, int MR>
-__device__ __forceinline__ void zero_acc(f32x16 (&acc)[MV][MR]) {
+template <class Acc, int MV, int MR>
+__device__ __forceinline__ void zero_acc(Acc (&acc)[MV][MR]) {
+  constexpr int kRegs = sizeof(Acc) / sizeof(float);
 #pragma unroll
   for (int i = 0; i < MV; ++i)
 #pragma unroll
     for (int j = 0; j < MR; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+      for (int e = 0; e < kRegs; ++e) acc[i][j][e] = 0.f;
 }
 
-// The logits of one tile, left in the MFMA accumulators: acc[i][j] holds the 32x32 block of
-// vocabulary rows v0 + wv * kWaveV + 32 i .. and tree rows r0 + wr * kWaveR + 32 j .. of this
-// wave, summed over all of H. Rows past V or past N read as zeros. On return every stage copy
-// has landed and the workgroup has passed a barrier, so the caller may reuse the LDS ring.
-template <int TV, int TR, int WV, int WR, int BK, int NST, bool STREAM_W = (TR <= 128)>
+// The logits of one tile, left in the MFMA accumulators: acc[i][j] holds the block of
+// vocabulary rows v0 + wv * kWaveV + kBlock i .. and tree rows r0 + wr * kWaveR + kBlock j ..
+// of this wave, summed over all of H. Rows past V or past N read as zeros. On return every
+// stage copy has landed and the workgroup has passed a barrier, so the caller may reuse the
+// LDS ring.
+template <int TV, int TR, int WV, int WR, int BK, int NST, bool STREAM_W = (TR <= 128),
+          class MF = Mfma32>
 __device__ __forceinline__ void lmhead_tile(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int N, int H, int V,
     int v0, int r0, uint4* smem, int w_packed,
-    f32x16 (&acc)[LmheadCfg<TV, TR, WV, WR, BK, NST>::MV][LmheadCfg<TV, TR, WV, WR, BK, NST>::MR]) {
-  using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
-  const TileIo<TV, TR, WV, WR, BK, NST, STREAM_W> io(X, W, N, H, V, v0, r0, smem, w_packed);
+    typename MF::Acc (&acc)[LmheadCfg<TV, TR, WV, WR, BK, NST, MF>::MV]
+                           [LmheadCfg<TV, TR, WV, WR, BK, NST, MF>::MR]) {
+  using C = LmheadCfg<TV, TR, WV, WR, BK, NST, MF>;
+  const TileIo<TV, TR, WV, WR, BK, NST, STREAM_W, MF> io(X, W, N, H, V, v0, r0, smem, w_packed);
   const int KT = H / BK;
   auto issue_stage = [&](int ks) {
     static_for<C::kLoads>([&](auto cc) { io.template copy<decltype(cc)::value>(ks % NST, ks); });
@@ -252,19 +300,18 @@ __device__ __forceinline__ void lmhead_tile(
   zero_acc(acc);
 
   bf16x8 a0[C::MV], b0[C::MR], a1[C::MV], b1[C::MR];
-  // Fragments of K16 step `half` (0 or 1) of the stage in ring slot `slot`.
-  auto load_frags = [&](int slot, int half, bf16x8* a, bf16x8* b) {   // half: K16 step
+  // Fragments of MFMA K step `step` of the stage in ring slot `slot`.
+  auto load_frags = [&](int slot, int step, bf16x8* a, bf16x8* b) {
 #pragma unroll
-    for (int i = 0; i < C::MV; ++i) a[i] = io.w_frag(slot, half, i);
+    for (int i = 0; i < C::MV; ++i) a[i] = io.w_frag(slot, step, i);
 #pragma unroll
-    for (int j = 0; j < C::MR; ++j) b[j] = io.x_frag(slot, half, j);
+    for (int j = 0; j < C::MR; ++j) b[j] = io.x_frag(slot, step, j);
   };
   auto mfmas = [&](const bf16x8* a, const bf16x8* b) {
 #pragma unroll
     for (int i = 0; i < C::MV; ++i)
 #pragma unroll
-      for (int j = 0; j < C::MR; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      for (int j = 0; j < C::MR; ++j) acc[i][j] = MF::mma(a[i], b[j], acc[i][j]);
   };
 
   // Prologue: fill the whole ring, then wait for stage 0.
@@ -273,20 +320,20 @@ __device__ __forceinline__ void lmhead_tile(
   wait_stage_barrier<C::kLoads>(pro - 1);
   load_frags(0, 0, a0, b0);
 
-  // Per stage k with K16 steps s = 0 .. BK/16 - 1: read the fragments of step s + 1 while the
+  // Per stage k with MFMA K steps s = 0 .. NS - 1: read the fragments of step s + 1 while the
   // MFMAs of step s run. Before the last step's MFMAs (all reads of slot k done), wait for
   // stage k+1 and pass the barrier while the previous MFMAs drain, refill slot k with stage
   // k + NST, and read the first fragments of k+1 under the last step's MFMAs.
-  constexpr int NS16 = BK / 16;
+  constexpr int NS = C::NS;
   for (int k = 0; k < KT; ++k) {
     const int slot = k % NST;
 #pragma unroll
-    for (int s = 0; s < NS16; ++s) {
+    for (int s = 0; s < NS; ++s) {
       bf16x8* ca = (s & 1) ? a1 : a0;
       bf16x8* cb = (s & 1) ? b1 : b0;
       bf16x8* na = (s & 1) ? a0 : a1;
       bf16x8* nb = (s & 1) ? b0 : b1;
-      if (s + 1 < NS16) {
+      if (s + 1 < NS) {
         load_frags(slot, s + 1, na, nb);
       } else if (k + 1 < KT) {
         // stage k+1 must have landed; the copies of the newer stages may stay in flight
@@ -297,7 +344,7 @@ __device__ __forceinline__ void lmhead_tile(
       mfmas(ca, cb);
     }
   }
-  static_assert(NS16 % 2 == 0, "fragment double buffer alternates within a stage");
+  static_assert(NS % 2 == 0, "fragment double buffer alternates within a stage");
   // every copy was waited for by the last stage's predecessor
   __syncthreads();
 }
@@ -308,38 +355,44 @@ __device__ __forceinline__ void wait_lds_barrier() {
 }
 
 // The same logits as lmhead_tile for 64-deep stages in a two-slot ring, with a fixed
-// instruction schedule that spreads each stage's copies over the MFMAs. A stage has four K16
-// steps F0..F3 of NF = MV + MR fragments and MV * MR MFMAs each (NM MFMAs in all). Per stage
-// k, in issue order (one MFMA per position m, the other work attached after it):
-//   m < 2 NF        read F2 and F3 of slot k, one fragment per MFMA;
+// instruction schedule that spreads each stage's copies over the MFMAs. A stage has NS MFMA K
+// steps (four K16 steps of 32x32x16, or two K32 steps of 16x16x32) of NF = MV + MR fragments
+// and MV * MR MFMAs each (NM MFMAs in all); its first half is steps 0 .. NS/2 - 1, its second
+// half the rest. Per stage k, in issue order (one MFMA per position m, the other work
+// attached after it):
+//   m < NS/2 NF     read the second half's fragments of slot k, one per MFMA;
 //   m = Q1 - 1      LDS reads done + barrier: no wave reads slot k any more;
 //   Q1 <= m < NM    the copies of stage k + 2 into slot k, evenly spaced;
 //   m = Q2 - 1      wait until stage k + 1 has landed (only copies of stage k + 2 may be
 //                   outstanding) + barrier;
-//   m >= Q2         read F0 and F1 of stage k + 1, one fragment per MFMA.
+//   m >= Q2         read the first half's fragments of stage k + 1, one per MFMA.
 // Each wave's vector-memory queue thus never holds a whole stage of copies (issued in one
 // burst, they block the wave's in-order instruction stream, and with it its MFMAs, until the
 // CU's address unit has taken them); the stage copy has about 1.5 stages to land. MFMAs
 // accumulate in the same K order as lmhead_tile, so the logits are bit-identical. The
 // schedule is branch-free: past the last stage the copies repeat the last stage into the slot
 // just freed (never read again) and the reads of the stage after the last are discarded.
-template <int TV, int TR, int WV, int WR>
+template <int TV, int TR, int WV, int WR, class MF = Mfma32>
 __device__ __forceinline__ void lmhead_tile_spread(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int N, int H, int V,
     int v0, int r0, uint4* smem, int w_packed,
-    f32x16 (&acc)[LmheadCfg<TV, TR, WV, WR, 64, 2>::MV][LmheadCfg<TV, TR, WV, WR, 64, 2>::MR]) {
+    typename MF::Acc (&acc)[LmheadCfg<TV, TR, WV, WR, 64, 2, MF>::MV]
+                           [LmheadCfg<TV, TR, WV, WR, 64, 2, MF>::MR]) {
   constexpr int BK = 64, NST = 2;
-  using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
-  constexpr int MV = C::MV, MR = C::MR;
-  constexpr int NF = MV + MR;                 // fragments per K16 step
-  constexpr int NM = 4 * MV * MR;             // MFMAs per stage
+  using C = LmheadCfg<TV, TR, WV, WR, BK, NST, MF>;
+  constexpr int MV = C::MV, MR = C::MR, NS = C::NS, HS = NS / 2;
+  constexpr int NF = MV + MR;                 // fragments per K step
+  constexpr int NM = NS * MV * MR;            // MFMAs per stage
   constexpr int kCopies = C::kLoads;          // copies per wave per stage
-  constexpr int Q1 = 2 * NF + 2;              // slot-free barrier after MFMA Q1 - 1
-  constexpr int Q2 = NM - 2 * NF - 4;         // next-stage barrier after MFMA Q2 - 1
-  static_assert(2 * NF <= 2 * MV * MR, "F2 and F3 are read within steps 0 and 1");
-  static_assert(Q1 < Q2 && Q2 + 2 * NF <= NM, "schedule points inside the stage");
-  static_assert(Q2 >= 2 * MV * MR, "F0 and F1 of the next stage overwrite registers steps 0 "
-                "and 1 of this stage have finished with");
+  constexpr int RS = MF::kK / 16;             // MFMAs per fragment read (one per 32 cycles)
+  constexpr int NR = RS * HS * NF;            // MFMA positions the reads of a half span
+  constexpr int Q1 = NR + 2;                  // slot-free barrier after MFMA Q1 - 1
+  constexpr int Q2 = NM - NR - 4;             // next-stage barrier after MFMA Q2 - 1
+  static_assert(NS % 2 == 0, "two halves of K steps");
+  static_assert(NR <= HS * MV * MR, "the second half is read within the first half");
+  static_assert(Q1 < Q2 && Q2 + NR <= NM, "schedule points inside the stage");
+  static_assert(Q2 >= HS * MV * MR, "the first half of the next stage overwrites registers "
+                "this stage's first half has finished with");
   // position of copy c, and how many copies precede the next-stage barrier
   constexpr auto copy_pos = [](int c) { return Q1 + c * (NM - Q1) / kCopies; };
   constexpr int kBeforeQ2 = [&] {
@@ -348,21 +401,30 @@ __device__ __forceinline__ void lmhead_tile_spread(
     return n;
   }();
 
-  const TileIo<TV, TR, WV, WR, BK, NST> io(X, W, N, H, V, v0, r0, smem, w_packed);
+  const TileIo<TV, TR, WV, WR, BK, NST, (TR <= 128), MF> io(X, W, N, H, V, v0, r0, smem,
+                                                           w_packed);
   const int KT = H / BK;
   auto issue_copy = [&](int slot, int ks, auto cc) {
     io.template copy<decltype(cc)::value>(slot, ks);
   };
   zero_acc(acc);
 
-  bf16x8 fa[4][MV], fb[4][MR];
-  // fragment f (W for f < MV, else X) of K16 step s of ring slot `slot`
+  bf16x8 fa[NS][MV], fb[NS][MR];
+  // fragment f of MFMA K step s of ring slot `slot`. The 32x32x16 loop reads W before X;
+  // the 16x16x32 loop reads in the order the step's MFMAs first use them (W 0, every X, then
+  // the other W), since its reads come closer to their use.
   auto read_frag = [&](int slot, int s, int f) {
-    if (f < MV) fa[s][f] = io.w_frag(slot, s, f);
-    else fb[s][f - MV] = io.x_frag(slot, s, f - MV);
+    if constexpr (RS == 1) {
+      if (f < MV) fa[s][f] = io.w_frag(slot, s, f);
+      else fb[s][f - MV] = io.x_frag(slot, s, f - MV);
+    } else {
+      if (f == 0) fa[s][0] = io.w_frag(slot, s, 0);
+      else if (f <= MR) fb[s][f - 1] = io.x_frag(slot, s, f - 1);
+      else fa[s][f - MR] = io.w_frag(slot, s, f - MR);
+    }
   };
 
-  // Prologue: stages 0 and 1, wait for stage 0, read its F0 and F1.
+  // Prologue: stages 0 and 1, wait for stage 0, read its first half.
   static_for<kCopies>([&](auto cc) { issue_copy(0, 0, cc); });
   if (KT > 1) {
     static_for<kCopies>([&](auto cc) { issue_copy(1, 1, cc); });
@@ -371,9 +433,9 @@ __device__ __forceinline__ void lmhead_tile_spread(
     wait_vm_barrier<0>();
   }
 #pragma unroll
-  for (int f = 0; f < NF; ++f) read_frag(0, 0, f);
+  for (int s = 0; s < HS; ++s)
 #pragma unroll
-  for (int f = 0; f < NF; ++f) read_frag(0, 1, f);
+    for (int f = 0; f < NF; ++f) read_frag(0, s, f);
 
   for (int k = 0; k < KT; ++k) {
     const int slot = k & 1;
@@ -381,15 +443,15 @@ __device__ __forceinline__ void lmhead_tile_spread(
     static_for<NM>([&](auto mc) {
       constexpr int m = decltype(mc)::value;
       constexpr int s = m / (MV * MR), q = m % (MV * MR), i = q / MR, j = q % MR;
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
-      if constexpr (m < 2 * NF) read_frag(slot, 2 + m / NF, m % NF);
+      acc[i][j] = MF::mma(fa[s][i], fb[s][j], acc[i][j]);
+      if constexpr (m < NR && m % RS == 0) read_frag(slot, HS + m / RS / NF, m / RS % NF);
       if constexpr (m == Q1 - 1) wait_lds_barrier();
       static_for<kCopies>([&](auto cc) {
         if constexpr (copy_pos(decltype(cc)::value) == m) issue_copy(slot, ks_copy, cc);
       });
       if constexpr (m == Q2 - 1) wait_vm_barrier<kBeforeQ2>();
-      if constexpr (m >= Q2 && m < Q2 + 2 * NF)
-        read_frag(slot ^ 1, (m - Q2) / NF, (m - Q2) % NF);
+      if constexpr (m >= Q2 && m < Q2 + NR && (m - Q2) % RS == 0)
+        read_frag(slot ^ 1, (m - Q2) / RS / NF, (m - Q2) / RS % NF);
       __builtin_amdgcn_sched_barrier(0);
     });
   }
@@ -401,28 +463,32 @@ __device__ __forceinline__ void lmhead_tile_spread(
 // The spread K loop for a three-slot ring: one barrier per stage. Stage j's copies go to slot
 // j % 3 and are spread evenly over the window from the barrier of stage j - 3 (after which no
 // wave reads that slot) to the barrier of stage j - 2 (which waits for stage j - 1); each copy
-// thus has at least one stage to land. Per stage k, one MFMA per position m:
-//   m < 2 NF        read F2 and F3 of slot k, one fragment per MFMA;
+// thus has at least one stage to land. Per stage k (halves of K steps as in
+// lmhead_tile_spread), one MFMA per position m:
+//   m < NS/2 NF     read the second half's fragments of slot k, one per MFMA;
 //   m < Q2          the remaining copies of stage k + 2;
 //   m = Q2 - 1      wait until stage k + 1 has landed (only copies of stage k + 2 may be
 //                   outstanding) + barrier;
-//   m >= Q2         read F0 and F1 of stage k + 1; the first copies of stage k + 3.
+//   m >= Q2         read the first half's fragments of stage k + 1; the first copies of
+//                   stage k + 3.
 // Past the last stage the copies repeat the last stage into slots no later stage reads.
-template <int TV, int TR, int WV, int WR>
+template <int TV, int TR, int WV, int WR, class MF = Mfma32>
 __device__ __forceinline__ void lmhead_tile_spread3(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int N, int H, int V,
     int v0, int r0, uint4* smem, int w_packed,
-    f32x16 (&acc)[LmheadCfg<TV, TR, WV, WR, 64, 3>::MV][LmheadCfg<TV, TR, WV, WR, 64, 3>::MR]) {
+    typename MF::Acc (&acc)[LmheadCfg<TV, TR, WV, WR, 64, 3, MF>::MV]
+                           [LmheadCfg<TV, TR, WV, WR, 64, 3, MF>::MR]) {
   constexpr int BK = 64, NST = 3;
-  using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
-  constexpr int MV = C::MV, MR = C::MR;
-  constexpr int NF = MV + MR;                 // fragments per K16 step
-  constexpr int NM = 4 * MV * MR;             // MFMAs per stage
+  using C = LmheadCfg<TV, TR, WV, WR, BK, NST, MF>;
+  constexpr int MV = C::MV, MR = C::MR, NS = C::NS, HS = NS / 2;
+  constexpr int NF = MV + MR;                 // fragments per K step
+  constexpr int NM = NS * MV * MR;            // MFMAs per stage
   constexpr int G = C::kLoads;                // copies per wave per stage
-  constexpr int Q2 = NM - 2 * NF;             // the barrier after MFMA Q2 - 1
-  static_assert(Q2 >= 2 * NF + 2, "F2 and F3 reads land before the barrier");
-  static_assert(Q2 >= 2 * MV * MR, "F0 and F1 of the next stage overwrite registers steps 0 "
-                "and 1 of this stage have finished with");
+  constexpr int Q2 = NM - HS * NF;            // the barrier after MFMA Q2 - 1
+  static_assert(NS % 2 == 0, "two halves of K steps");
+  static_assert(Q2 >= HS * NF + 2, "the second half's reads land before the barrier");
+  static_assert(Q2 >= HS * MV * MR, "the first half of the next stage overwrites registers "
+                "this stage's first half has finished with");
   static_assert(2 * G <= 63, "vmcnt range");
   // copy c of a group sits c * NM / G MFMAs after the barrier that opens its window; the
   // first n1 of them fall in the same stage as that barrier
@@ -433,7 +499,8 @@ __device__ __forceinline__ void lmhead_tile_spread3(
     return n;
   }();
 
-  const TileIo<TV, TR, WV, WR, BK, NST> io(X, W, N, H, V, v0, r0, smem, w_packed);
+  const TileIo<TV, TR, WV, WR, BK, NST, (TR <= 128), MF> io(X, W, N, H, V, v0, r0, smem,
+                                                           w_packed);
   const int KT = H / BK;
   // copy c of stage j into slot j % 3, from K stage min(j, KT - 1)
   auto issue_copy = [&](int j, auto cc) {
@@ -441,14 +508,14 @@ __device__ __forceinline__ void lmhead_tile_spread3(
   };
   zero_acc(acc);
 
-  bf16x8 fa[4][MV], fb[4][MR];
+  bf16x8 fa[NS][MV], fb[NS][MR];
   auto read_frag = [&](int slot, int s, int f) {
     if (f < MV) fa[s][f] = io.w_frag(slot, s, f);
     else fb[s][f - MV] = io.x_frag(slot, s, f - MV);
   };
 
   // Prologue: stages 0 and 1 and the first n1 copies of stage 2 (what the window of a stage
-  // -1 would have issued); wait for stage 0; read its F0 and F1.
+  // -1 would have issued); wait for stage 0; read its first half.
   static_for<G>([&](auto cc) { issue_copy(0, cc); });
   static_for<G>([&](auto cc) { issue_copy(1, cc); });
   static_for<G>([&](auto cc) {
@@ -456,9 +523,9 @@ __device__ __forceinline__ void lmhead_tile_spread3(
   });
   wait_vm_barrier<G + n1>();
 #pragma unroll
-  for (int f = 0; f < NF; ++f) read_frag(0, 0, f);
+  for (int s = 0; s < HS; ++s)
 #pragma unroll
-  for (int f = 0; f < NF; ++f) read_frag(0, 1, f);
+    for (int f = 0; f < NF; ++f) read_frag(0, s, f);
 
   int slot = 0;
   for (int k = 0; k < KT; ++k) {
@@ -466,15 +533,15 @@ __device__ __forceinline__ void lmhead_tile_spread3(
     static_for<NM>([&](auto mc) {
       constexpr int m = decltype(mc)::value;
       constexpr int s = m / (MV * MR), q = m % (MV * MR), i = q / MR, j = q % MR;
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[s][i], fb[s][j], acc[i][j], 0, 0, 0);
-      if constexpr (m < 2 * NF) read_frag(slot, 2 + m / NF, m % NF);
+      acc[i][j] = MF::mma(fa[s][i], fb[s][j], acc[i][j]);
+      if constexpr (m < HS * NF) read_frag(slot, HS + m / NF, m % NF);
       static_for<G>([&](auto cc) {
         constexpr int c = decltype(cc)::value;
         if constexpr (c >= n1 && Q2 + rel(c) - NM == m) issue_copy(k + 2, cc);
         if constexpr (c < n1 && Q2 + rel(c) == m) issue_copy(k + 3, cc);
       });
       if constexpr (m == Q2 - 1) wait_vm_barrier<G>();
-      if constexpr (m >= Q2 && m < Q2 + 2 * NF)
+      if constexpr (m >= Q2 && m < Q2 + HS * NF)
         read_frag(nslot, (m - Q2) / NF, (m - Q2) % NF);
       __builtin_amdgcn_sched_barrier(0);
     });
@@ -486,9 +553,11 @@ __device__ __forceinline__ void lmhead_tile_spread3(
 }
 
 // LOOP selects the K loop: 0 = the burst ring of lmhead_tile; 2 and 3 = the spread loop of
-// that ring depth (lmhead_tile_spread, lmhead_tile_spread3). One launch covers a contiguous
-// range of vocabulary slabs (all of them, or one of two ranges whose tiles differ in height).
-template <int TV, int TR, int WV, int WR, int BK, int NST, int LOOP = 0>
+// that ring depth (lmhead_tile_spread, lmhead_tile_spread3). MF is the MFMA shape; every tile
+// family of K1 runs the same one, so that all of them sum each logit's products in the same
+// order and give the same logits bit for bit. One launch covers a contiguous range of
+// vocabulary slabs (all of them, or one of two ranges whose tiles differ in height).
+template <int TV, int TR, int WV, int WR, int BK, int NST, int LOOP = 0, class MF = Mfma16>
 __global__ __launch_bounds__(WV * WR * kWave, 1)
 void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                       const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
@@ -497,8 +566,9 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
                       float* __restrict__ rec_s, int32_t* __restrict__ rec_a,
                       float* __restrict__ drafted_logit, int32_t* __restrict__ done_cnt,
                       int n_cnt, int w_packed) {
-  using C = LmheadCfg<TV, TR, WV, WR, BK, NST>;
+  using C = LmheadCfg<TV, TR, WV, WR, BK, NST, MF>;
   constexpr int T = C::kThreads;
+  constexpr int kBlock = MF::kBlock, kRegs = MF::kRegs;
   __shared__ uint4 smem[C::kLds / 16];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -536,22 +606,21 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
   }
 
   // ---- the tile's logits
-  f32x16 acc[C::MV][C::MR];
+  typename MF::Acc acc[C::MV][C::MR];
   if constexpr (LOOP == 2) {
     static_assert(BK == 64 && NST == 2, "two-slot spread loop: 64-deep stages");
-    lmhead_tile_spread<TV, TR, WV, WR>(X, W, N, H, V, v0, r0, smem, w_packed, acc);
+    lmhead_tile_spread<TV, TR, WV, WR, MF>(X, W, N, H, V, v0, r0, smem, w_packed, acc);
   } else if constexpr (LOOP == 3) {
     static_assert(BK == 64 && NST == 3, "three-slot spread loop: 64-deep stages");
-    lmhead_tile_spread3<TV, TR, WV, WR>(X, W, N, H, V, v0, r0, smem, w_packed, acc);
+    lmhead_tile_spread3<TV, TR, WV, WR, MF>(X, W, N, H, V, v0, r0, smem, w_packed, acc);
   } else {
     static_assert(LOOP == 0, "K loop");
-    lmhead_tile<TV, TR, WV, WR, BK, NST>(X, W, N, H, V, v0, r0, smem, w_packed, acc);
+    lmhead_tile<TV, TR, WV, WR, BK, NST, (TR <= 128), MF>(X, W, N, H, V, v0, r0, smem,
+                                                          w_packed, acc);
   }
-  const int frag_half = lane >> 5;
 
-  // Output block (i, j), register e of a lane holds vocab row
-  //   32*i + 8*(e/4) + 4*(lane/32) + e%4   (of the wave's vocab range) and
-  // tree row 32*j + lane%32 (of the wave's row range).
+  // Output block (i, j), register e of a lane holds vocab row kBlock i + MF::row_of(lane, e)
+  // (of the wave's vocab range) and tree row kBlock j + lane % kBlock (of the wave's rows).
 
   // Epilogue scratch reuses the ring: the gather list (kCap entries of 16 bytes), one
   // 64 x 16-float extraction area per wave, the row-reduction exchange and two counters.
@@ -615,10 +684,10 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
       for (int i = 0; i < C::MV; ++i)
 #pragma unroll
         for (int j = 0; j < C::MR; ++j) asm volatile("" : "+a"(acc[i][j]));
-      const int jj = pr >> 5, ii = dv >> 5, mm = dv & 31;
-      const int ee = ((mm >> 3) << 2) | (mm & 3);
-      const int owner = (pr & 31) + 32 * ((mm >> 2) & 1);
-      // The block index is wave-uniform: branch to it, park its 16 registers in this wave's
+      const int jj = pr / kBlock, ii = dv / kBlock, mm = dv % kBlock;
+      const int ee = MF::reg_of(mm);
+      const int owner = MF::lane_of(pr % kBlock, mm);
+      // The block index is wave-uniform: branch to it, park its registers in this wave's
       // LDS scratch and let the owner lane read its element back (LDS operations of one wave
       // complete in order).
 #pragma unroll
@@ -627,7 +696,7 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
         for (int j = 0; j < C::MR; ++j)
           if (i == ii && j == jj) {
 #pragma unroll
-            for (int e2 = 0; e2 < 16; ++e2) wscr[e2 * kWave + lane] = acc[i][j][e2];
+            for (int e2 = 0; e2 < kRegs; ++e2) wscr[e2 * kWave + lane] = acc[i][j][e2];
           }
       __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
       if (lane == owner) drafted_logit[m.x] = wscr[ee * kWave + owner];
@@ -636,15 +705,18 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
     __syncthreads();
   }
 
-  // ---- per-row slab record: lane-local pass, then the two lane halves, then the waves
-  // that share the same tree rows (through LDS). Within a lane the entries of a tree row are
-  // visited in increasing vocabulary order, so "strictly greater" keeps the lowest argmax;
-  // the argmax is tracked as the entry ordinal k = 16 i + e and turned into a vocabulary id
-  // afterwards. Only the last slab needs the v < V mask. One row block at a time keeps the
-  // accumulator reads short-lived (sched_barrier stops the scheduler from hoisting them).
+  // ---- per-row slab record: lane-local pass, then the lane groups that hold the same tree
+  // rows (64 / kBlock of them), then the waves that share the same tree rows (through LDS).
+  // Within a lane the entries of a tree row are visited in increasing vocabulary order, so
+  // "strictly greater" keeps the lowest argmax; the argmax is tracked as the entry ordinal
+  // k = kRegs i + e and turned into a vocabulary id afterwards, and merges keep the lowest id
+  // among equal maxima. Only the last slab needs the v < V mask. One row block at a time keeps
+  // the accumulator reads short-lived (sched_barrier stops the scheduler from hoisting them).
   const bool full_slab = v0 + TV <= V;
-  const int vlane = v0 + wv * C::kWaveV + 4 * frag_half;
-  auto entry_v = [&](int k) { return vlane + 32 * (k >> 4) + 8 * ((k & 15) >> 2) + (k & 3); };
+  const int vwave = v0 + wv * C::kWaveV;
+  auto entry_v = [&](int k) {
+    return vwave + kBlock * (k / kRegs) + MF::row_of(lane, k % kRegs);
+  };
   // Branch-free lane-local record of row block j; MASK drops entries past V (last slab).
   auto row_record = [&](int j, auto mask_tag) -> Rec {
     constexpr bool MASK = decltype(mask_tag)::value;
@@ -653,8 +725,8 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
 #pragma unroll
     for (int i = 0; i < C::MV; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int k = 16 * i + e;
+      for (int e = 0; e < kRegs; ++e) {
+        const int k = kRegs * i + e;
         float z = acc[i][j][e];
         if constexpr (MASK) z = entry_v(k) < V ? z : kNegInf;
         kbest = z > m ? k : kbest;
@@ -665,9 +737,9 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
 #pragma unroll
     for (int i = 0; i < C::MV; ++i)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
+      for (int e = 0; e < kRegs; ++e) {
         const float t = exp2_rel(fmaf(acc[i][j][e], kLog2e, -mb));
-        if constexpr (MASK) sum += entry_v(16 * i + e) < V ? t : 0.f;
+        if constexpr (MASK) sum += entry_v(kRegs * i + e) < V ? t : 0.f;
         else sum += t;
       }
     return Rec{m, m == kNegInf ? 0.f : sum, m == kNegInf ? kNoIndex : entry_v(kbest)};
@@ -675,9 +747,10 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
 #pragma unroll
   for (int j = 0; j < C::MR; ++j) {
     Rec r = full_slab ? row_record(j, std::false_type{}) : row_record(j, std::true_type{});
-    r = rec_merge(r, rec_shfl_xor(r, 32));
-    if (lane < 32) {
-      const int row = wr * C::kWaveR + 32 * j + lane;
+#pragma unroll
+    for (int mask = kBlock; mask < kWave; mask <<= 1) r = rec_merge(r, rec_shfl_xor(r, mask));
+    if (lane < kBlock) {
+      const int row = wr * C::kWaveR + kBlock * j + lane;
       red_m[wv * TR + row] = r.m;
       red_s[wv * TR + row] = r.s;
       red_a[wv * TR + row] = r.a;
