@@ -92,25 +92,31 @@ __device__ __forceinline__ int swz(int row, int chunk) {
   return row * CPR + (chunk ^ swz_phase<CPR>(row));
 }
 
-// Direct global->LDS copy of 16 bytes per lane: lane t's 16 bytes land at LDS byte address
-// lds + 16 t. Out-of-range offsets of the buffer resource write zeros.
+// Direct global->LDS copy of 16 bytes per lane from byte voff + soff of the buffer: lane t's
+// 16 bytes land at LDS byte address lds + 16 t. A lane whose offset lies past the buffer
+// resource's range writes zeros. The K loops keep each lane's offset within its row in voff
+// (fixed for the whole loop) and put the K stage's offset, the same for every lane, in the
+// scalar soff: the per-copy address needs no vector instruction, and the range check still
+// turns every row past the valid ones into zeros (their voff alone is out of range) whether or
+// not soff takes part in it.
 // M0 is reserved: the compiler sets it right before each instruction that reads it and never
 // keeps a value in it across other code on gfx9-family GPUs, so overwriting it here is safe;
 // the clobber is declared anyway.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void dma16(int lds, int voff, __amdgpu_buffer_rsrc_t r) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+__device__ __forceinline__ void dma16(int lds, int voff, int soff, __amdgpu_buffer_rsrc_t r) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
                :
-               : "s"(lds), "v"(voff), "s"(r)
+               : "s"(lds), "v"(voff), "s"(r), "s"(soff)
                : "memory", "m0");
 }
 // The same copy with the non-temporal hint (nt): for data read once and streamed, which the
 // caches should not try to keep.
-__device__ __forceinline__ void dma16_stream(int lds, int voff, __amdgpu_buffer_rsrc_t r) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen nt lds"
+__device__ __forceinline__ void dma16_stream(int lds, int voff, int soff,
+                                             __amdgpu_buffer_rsrc_t r) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen nt lds"
                :
-               : "s"(lds), "v"(voff), "s"(r)
+               : "s"(lds), "v"(voff), "s"(r), "s"(soff)
                : "memory", "m0");
 }
 #pragma clang diagnostic pop
@@ -243,14 +249,14 @@ struct TileIo {
     const int base = lds0 + slot * C::kStage;
     if constexpr (c < C::DW) {
       const int lds_at = base + (c * C::kWaves + wave) * 1024;
-      const int at = (int)((unsigned)w_voff[c] + (unsigned)ks * w_kstep);
+      const int so = __builtin_amdgcn_readfirstlane((int)((unsigned)ks * w_kstep));
       if constexpr (kStreamW)
-        dma16_stream(lds_at, at, w_rsrc);
+        dma16_stream(lds_at, w_voff[c], so, w_rsrc);
       else
-        dma16(lds_at, at, w_rsrc);
+        dma16(lds_at, w_voff[c], so, w_rsrc);
     } else
-      dma16(base + C::kStageW + ((c - C::DW) * C::kWaves + wave) * 1024,
-            x_voff[c - C::DW] + ks * BK * 2, x_rsrc);
+      dma16(base + C::kStageW + ((c - C::DW) * C::kWaves + wave) * 1024, x_voff[c - C::DW],
+            __builtin_amdgcn_readfirstlane(ks * BK * 2), x_rsrc);
   }
   // the fragment of W block i (of this wave's vocabulary rows), or of X block j (of its tree
   // rows), for MFMA K step s of ring slot `slot`
