@@ -11,7 +11,7 @@ import numpy as np
 import pytest
 
 import oracle
-from harness import SHAPE_BAND, compare, compare_state, device_inputs, follow_gpu_history, \
+from harness import TOL_F, SHAPE_BAND, compare, compare_state, device_inputs, follow_gpu_history, \
     reference, resolve_with_oracle, to_host
 from workloads import build_tree, custom_workload, make_workload
 
@@ -396,6 +396,41 @@ def test_exact_ties_lowest_index(asv, dev):
     assert got["drafted_logit"][1] == got["drafted_logit"][2]
     assert list(got["accepted_path"]) == list(ref["accepted_path"])
     assert got["bonus_token"][0] == ref["bonus_token"][0]
+
+
+def test_exact_ties_lane_groups(asv, dev):
+    """Exact ties laid across the accumulator layout of the 16x16 MFMA blocks: ids 558 (block
+    34, lane group 3), 566 and 570 (block 35, groups 1 and 2), 582 (block 36), 694 (the other
+    128-id half of slab 2, another wave) and 822 (slab 3) carry the same doubled weight row, so
+    their logits are equal and the largest of row 0. Every LM-head tile family must report the
+    lowest id, 558, as the oracle does, on the row-major and on the packed weight; the lowest id
+    sits in the highest lane group of its block, so the lane-group merges decide it."""
+    print("[ties across lane groups]", flush=True)
+    w = custom_workload("ties16", 128, 2000, [[-1, 0, 0]], 1.0, seed=19, w_std=0.11)
+    W = np.array(w.weights())
+    x64 = oracle.widen_bf16(w.hidden)
+    z = oracle.logits(x64, oracle.widen_weights(W))
+    a0 = int(np.argmax(z[0]))
+    assert z[0, a0] > 0
+    doubled = (W[a0].astype(np.uint32) << 16).view(np.float32) * 2     # exact in bf16
+    doubled = (doubled.view(np.uint32) >> 16).astype(np.uint16)
+    ties = [558, 566, 570, 582, 694, 822]
+    for v in ties:
+        W[v] = doubled
+    w64 = oracle.widen_weights(W)
+    z = oracle.logits(x64, w64)
+    assert list(np.flatnonzero(z[0] == z[0].max())) == ties
+    w.with_drafts(oracle.row_top8(z))
+    ref = reference(w, w64)
+    assert ref["row_argmax"][0] == 558
+    row_max = set()
+    for packed in (False, True):
+        for rows in (64, 128, 192, 256):
+            got = _run(asv, w, W, dev, k1_tile=rows, packed=packed)
+            assert got["row_argmax"][0] == 558, (rows, packed, int(got["row_argmax"][0]))
+            row_max.add(float(got["row_max"][0]))
+    assert len(row_max) == 1
+    assert abs(row_max.pop() - ref["row_max"][0]) < TOL_F
 
 
 @pytest.mark.parametrize("n_req", [3, 1030])
