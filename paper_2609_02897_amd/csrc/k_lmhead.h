@@ -77,15 +77,19 @@ constexpr int kKAlign = 64;   // H must be a multiple of this (host check)
 constexpr int kRsrcWord3 = 0x00020000;
 
 // A staged row of BK bf16 is CPR = BK / 8 chunks of 16 bytes. Logical chunk c of row r is
-// stored at position c ^ f(r) (16-byte units from the region start). ds_read_b128 serves 16
-// lanes per pass from 64 four-byte banks; in the MFMA operand layout 16 consecutive lanes read
-// the same logical chunk of 16 consecutive rows, so f is chosen to put every aligned group of
-// 16 rows (and of 8 rows, for 8-lane passes) on distinct 16-byte bank groups:
-//   128-byte rows: f(r) = (r & 7) ^ ((r >> 3) & 1);  64-byte rows: f(r) = ((r >> 2) ^ (r >> 1)) & 3.
+// stored at position c ^ f(r) (16-byte units from the region start). The LDS serves a wave's
+// ds_read_b128 in four passes of 16 lanes over 64 four-byte banks, 16 bank groups of 16 bytes;
+// a pass takes the lanes with equal lane bit 5 and equal parity of lane bits 2, 3 and 4
+// (measured: this grouping reproduces the bank-conflict counts of every probe pattern), and a
+// pass takes as many cycles as it has lanes on its busiest bank group. With 128-byte rows a read
+// lands in group 8 (r & 1) + (c ^ f(r)) mod 8, and f(r) = (r >> 1) & 7 gives every pass 16
+// distinct groups in both fragment layouts: 32x32x16 (lane l reads row l % 32, chunk
+// 2 s + l / 32) and 16x16x32 (row l % 16, chunk 4 s + l / 16). 64-byte rows (32x32x16 only)
+// take f(r) = ((r >> 2) ^ (r >> 1)) & 3.
 template <int CPR>
 __device__ __forceinline__ int swz_phase(int row) {
   static_assert(CPR == 4 || CPR == 8, "64- or 128-byte staged rows");
-  return CPR == 8 ? ((row & 7) ^ ((row >> 3) & 1)) : (((row >> 2) ^ (row >> 1)) & 3);
+  return CPR == 8 ? ((row >> 1) & 7) : (((row >> 2) ^ (row >> 1)) & 3);
 }
 template <int CPR>
 __device__ __forceinline__ int swz(int row, int chunk) {
