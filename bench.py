@@ -472,6 +472,31 @@ def measured_ceilings(dev) -> dict:
     return {"stream_read_gbps": round(best, 1), "mfma_bf16_tflops": round(tflops, 1)}
 
 
+def lds_probe_patterns() -> list:
+    """Lane patterns for the LDS read probe (asvb_lds_read): the 16-byte LDS unit each lane of a
+    wave reads with one ds_read_b128. Bit-selection patterns put lane l on bank group
+    (four lane bits of l) at a distinct address; the fragment patterns are the LM-head tiles'
+    staged operand reads (128-byte rows, logical chunk c of row r at c ^ f(r)) for both MFMA
+    shapes, with the current swizzle f(r) = (r >> 1) & 7 and the earlier
+    f(r) = (r & 7) ^ ((r >> 3) & 1)."""
+    import itertools
+    pats = [("linear", list(range(64))), ("one_bank_group", [16 * l for l in range(64)])]
+    for bits in itertools.combinations(range(6), 4):
+        g = [sum(((l >> b) & 1) << i for i, b in enumerate(bits)) for l in range(64)]
+        pats.append(("group_from_lane_bits_" + "".join(map(str, bits)),
+                     [16 * l + g[l] for l in range(64)]))
+    swz = {"current": lambda r: (r >> 1) & 7, "earlier": lambda r: (r & 7) ^ ((r >> 3) & 1)}
+    for name, f in swz.items():
+        for s in range(2):       # 16x16x32: lane l reads row l % 16, chunk 4 s + l / 16
+            pats.append((f"mfma16x16x32_{name}_swizzle_step{s}",
+                         [(l % 16) * 8 + ((4 * s + l // 16) ^ f(l % 16)) for l in range(64)]))
+        for s in range(4):       # 32x32x16: lane l reads row l % 32, chunk 2 s + l / 32
+            pats.append((f"mfma32x32x16_{name}_swizzle_step{s}",
+                         [(l % 32) * 8 + ((2 * s + l // 32) ^ f(l % 32)) for l in range(64)]))
+    assert all(len(u) == 64 and 0 <= min(u) and max(u) < 1024 for _, u in pats)
+    return pats
+
+
 def vendor_reference() -> dict:
     """Context for the roofline fractions: the vendor bf16 GEMM computing only the [N, V]
     logits of the four verify shapes (no reductions, gather or walk), and the copy bandwidth."""
@@ -539,7 +564,33 @@ def main():
                          "microbenchmark read; a buffer smaller than the last-level cache is "
                          "read from it after the first pass) and exit: shows which traffic "
                          "counters see last-level-cache hits")
+    ap.add_argument("--lds-probe", action="store_true",
+                    help="only run the LDS read-pattern probe (one asvb_lds_read dispatch per "
+                         "lane pattern, in the printed order, for SQ_LDS_BANK_CONFLICT counters) "
+                         "and exit")
     args = ap.parse_args()
+    if args.lds_probe:
+        import torch
+        mb = _microbench_lib()
+        mb.asvb_lds_read.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                     ctypes.c_int32, ctypes.c_void_p]
+        stream = torch.cuda.current_stream()
+        handle = stream.cuda_stream
+        grid, iters = 1024, 4096
+        sink = torch.zeros(grid * 256, dtype=torch.int32, device="cuda:0")
+        rows = []
+        for name, units in lds_probe_patterns():
+            u = torch.tensor(units, dtype=torch.int32, device="cuda:0")
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            assert mb.asvb_lds_read(u.data_ptr(), iters, sink.data_ptr(), grid, handle) == 0
+            b.record(stream)
+            b.synchronize()
+            rows.append({"pattern": name, "us": round(a.elapsed_time(b) * 1e3, 1)})
+        print(json.dumps({"lds_probe": rows, "grid": grid, "iters": iters,
+                          "reads_per_dispatch": grid * 4 * iters}))
+        return
     if args.read_calibration:
         import torch
         n = args.read_calibration << 20

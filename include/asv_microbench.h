@@ -34,6 +34,15 @@ int asvb_stream_read_nt(const void *buf, uint64_t bytes, uint32_t *sink, int32_t
  * sink: [grid * 256] device floats. FLOPs: grid * 4 * iters * 8 * 32768. */
 int asvb_mfma_loop(float *sink, int32_t iters, int32_t grid, void *stream);
 
+/* LDS read-pattern probe: `grid` workgroups of 256 threads fill a 16 KB LDS buffer of 1024
+ * 16-byte units, then every wave reads unit unit_of_lane[lane] % 1024 (unit_of_lane: 64 device
+ * ints) with ds_read_b128, `iters` times, and each thread writes one word to
+ * sink[(workgroup * 256) + thread]. The dispatch's hardware counters (SQ_INSTS_LDS,
+ * SQ_LDS_BANK_CONFLICT) then give the bank-conflict cycles of that lane pattern.
+ * sink: [grid * 256] device words. */
+int asvb_lds_read(const int32_t *unit_of_lane, int32_t iters, uint32_t *sink, int32_t grid,
+                  void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -79,6 +79,26 @@ __global__ __launch_bounds__(kThreads) void k_mfma_loop(float* __restrict__ sink
   sink[blockIdx.x * kThreads + t] = s;
 }
 
+constexpr int kLdsUnits = 1024;   // 16 KB of 16-byte units
+
+// Each wave reads one 16-byte unit per lane, the same every iteration; `mask` is zero at run
+// time, so the address is fixed, but the compiler cannot hoist the read out of the loop.
+__global__ __launch_bounds__(kThreads) void k_lds_read(const int32_t* __restrict__ unit_of_lane,
+                                                        int iters, int mask,
+                                                        uint32_t* __restrict__ sink) {
+  __shared__ uint4 buf[kLdsUnits];
+  for (int i = threadIdx.x; i < kLdsUnits; i += kThreads)
+    buf[i] = make_uint4(i, i + 1, i + 2, i + 3);
+  __syncthreads();
+  const int u = unit_of_lane[threadIdx.x & 63] & (kLdsUnits - 1);
+  uint32_t acc = 0;
+  for (int it = 0; it < iters; ++it) {
+    const uint4 v = buf[u ^ (it & mask)];
+    acc += v.x ^ v.y ^ v.z ^ v.w;
+  }
+  sink[blockIdx.x * kThreads + threadIdx.x] = acc;
+}
+
 }  // namespace
 
 extern "C" int asvb_stream_read(const void* buf, uint64_t bytes, uint32_t* sink, int32_t grid,
@@ -108,5 +128,14 @@ extern "C" int asvb_mfma_loop(float* sink, int32_t iters, int32_t grid, void* st
   if (!sink || iters < 1 || grid < 1) return -1;
   (void)hipGetLastError();
   k_mfma_loop<<<grid, kThreads, 0, reinterpret_cast<hipStream_t>(stream)>>>(sink, iters);
+  return hipGetLastError() == hipSuccess ? 0 : -3;
+}
+
+extern "C" int asvb_lds_read(const int32_t* unit_of_lane, int32_t iters, uint32_t* sink,
+                             int32_t grid, void* stream) {
+  if (!unit_of_lane || !sink || iters < 1 || grid < 1) return -1;
+  (void)hipGetLastError();
+  k_lds_read<<<grid, kThreads, 0, reinterpret_cast<hipStream_t>(stream)>>>(unit_of_lane, iters,
+                                                                          0, sink);
   return hipGetLastError() == hipSuccess ? 0 : -3;
 }

@@ -226,7 +226,8 @@ def test_microbench_library_exports_and_checks():
     src = open(os.path.join(ROOT, "include", "asv_microbench.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
     names = sorted(set(re.findall(r"\b(asvb_[a-z_]+)\s*\(", src)))
-    assert names == ["asvb_mfma_loop", "asvb_stream_read", "asvb_stream_read_nt"]
+    assert names == ["asvb_lds_read", "asvb_mfma_loop", "asvb_stream_read",
+                     "asvb_stream_read_nt"]
     for n in names:
         assert hasattr(mb, n), n
     for f in (mb.asvb_stream_read, mb.asvb_stream_read_nt):
@@ -244,6 +245,10 @@ def test_microbench_library_exports_and_checks():
         assert mb.asvb_stream_read_nt(*bad, None) == -1
     assert mb.asvb_mfma_loop(None, 4, 4, None) == -1
     assert mb.asvb_mfma_loop(p, 0, 4, None) == -1
+    mb.asvb_lds_read.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
+                                 ctypes.c_int32, ctypes.c_void_p]
+    for bad in ((None, 4, p, 4), (p, 0, p, 4), (p, 4, None, 4), (p, 4, p, 0)):
+        assert mb.asvb_lds_read(*bad, None) == -1
 
 
 def test_draft_and_tree_entry_points_reject_on_host(lib):
