@@ -13,10 +13,11 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of ``b
 import it. It shares no code with the HIP path (``paper_2609_02897_amd``); both read inputs from
 ``workloads`` only.
 
-Parity pins live in ``tests/oracle_pins.py`` and ``tests/tree_pins.py``. Functions whose result the paper does not fix
-are marked "parity unpinned" in their docstrings (the walk's sibling choice, the promotion
-count, the acceptance observation, the history reset on a breaker trip, the rounding of the
-tree shape and the starting configuration).
+Parity pins live in ``tests/oracle_pins.py`` and ``tests/tree_pins.py``. Every function has a pin. Where the paper does
+not fix a result (the walk's sibling choice, the promotion count, the acceptance observation,
+the history reset on a breaker trip, the rounding of the tree shape and the starting
+configuration), the docstring names the reading taken, and the pins check the code against
+that reading stated independently.
 """
 
 from .asv_oracle import (  # noqa: F401

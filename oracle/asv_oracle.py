@@ -10,7 +10,7 @@ Readings of points the paper leaves open (each one is listed with its reason in 
   * the rule is applied at every mismatch along the walk, not only the first one, unless
     ``max_promotions`` caps it (Sec. 3.2 speaks of "the first mismatch position");
   * among siblings the walk takes the child with the highest target logit, lowest node id on
-    ties (parity unpinned);
+    ties (reading R3: the paper does not fix the choice);
   * an exact match is always accepted (redundant in exact arithmetic: margin = 1 >= kappa);
   * kappa = 0 accepts everything; kappa must lie in [0, 1] (margin lies in [0, 1], Eq. (1));
   * argmax ties break to the lowest vocabulary id; the bonus token is the argmax of the last
@@ -136,7 +136,8 @@ def walk(root: int, end: int, parent: np.ndarray, draft_tok: np.ndarray, g: np.n
     "promotes drafted tokens at the first mismatch position"); with ``max_promotions >= 0`` the
     walk stops instead of exceeding that many promotions. The bonus token is the target argmax
     at the last accepted node (greedy decoding, Sec. 4.1). The child choice and the repeated
-    promotion are readings of the paper (parity unpinned).
+    promotion are readings the paper does not fix (R3, R2); the pins check the walk against
+    them stated independently.
 
     Returns (path as global node ids, accepted_len, bonus_token).
     """
@@ -234,11 +235,11 @@ def state_update(s: ReqState, accepted_len: int, n_nodes: int, conf: Optional[fl
     """Per-request acceptance history after one step (Sec. 3.3).
 
     RAR is an exponential moving average (alpha = 0.3) of the fraction of drafted tokens the
-    target accepted, here x = accepted_len / (n_nodes - 1) (parity unpinned: the paper names
+    target accepted, here x = accepted_len / (n_nodes - 1) (reading R10: the paper names
     the fraction, not its denominator). A 16-slot ring keeps the last observations and their
     mean. A request with ``breaker_n`` consecutive zero-accept steps trips the circuit breaker:
-    the flag is raised and RAR, the ring and the streak restart (the reset itself is a reading,
-    parity unpinned). A root-only tree drafts nothing and only advances ``steps``.
+    the flag is raised and RAR, the ring and the streak restart (the reset itself is reading R13,
+    not fixed by the paper). A root-only tree drafts nothing and only advances ``steps``.
     Finally the next step's tree shape is chosen from the latest draft confidence (this step's
     when draft logits were given, else the last one stored) and the updated RAR (Eq. (2),
     :func:`tree_shape`).
@@ -277,9 +278,9 @@ def tree_shape(conf: float, rar: float, breaker: int, p: Params):
     (nsteps, topk, ndt) moves linearly from ``shape_lo`` at DCS = 0 to ``shape_hi`` at DCS = 1
     (depth grows with DCS, branching with 1 - DCS), rounded to the nearest integer with halves
     going to the lower one (a reading: the paper selects among pre-captured integer triplets
-    without naming the rounding; parity unpinned). A request whose breaker tripped reverts to
-    ``shape_start`` (Sec. 3.3; which triplet is "the starting configuration" is a reading,
-    parity unpinned). Evaluated in float64.
+    without naming the rounding; reading R23). A request whose breaker tripped reverts to
+    ``shape_start`` (Sec. 3.3; which triplet is "the starting configuration" is reading R24,
+    not fixed by the paper). Evaluated in float64.
     """
     dcs = min(1.0, float(conf) * float(rar) / float(p.dcs_divisor))
     if breaker:

@@ -28,8 +28,8 @@ Readings of points the paper leaves open (listed with their reasons in the desig
   * committed tokens are the accepted drafted tokens followed by the bonus token; the rows kept
     for the next step are the root's and those of the accepted nodes.
 
-Parity unpinned: the growth rule itself (scores, frontier choice, pruning) is the EAGLE-2 reading
-above; the paper names only its three parameters. The pins check the code against that reading
+Not fixed by the paper: the growth rule itself (scores, frontier choice, pruning) is the EAGLE-2
+reading above; the paper names only its three parameters. The pins check the code against that reading
 stated independently, not against numbers the paper prints.
 """
 
