@@ -3,6 +3,7 @@
 // tree-attention metadata and the commit. Every entry point is declared in include/asv.h.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <atomic>
 #include <mutex>
 
@@ -116,6 +117,24 @@ K1Plan plan_k1(int N, int S, int cus) {
   return best;
 }
 
+// Order of a K1 launch's tiles. The blocks are dealt to the 8 XCDs in contiguous runs, and the
+// concurrent tiles of an XCD (cus / 8 of them) share what they read through its L2: in the
+// slab-major order about c / RT W slabs and all RT X row tiles per round of c tiles, blocked
+// into groups of 4 row tiles, c / 4 slabs and 4 row tiles. Per round an XCD then reads about
+// c / RT + RT or c / 4 + 4 slabs' and row tiles' worth of data from beyond its L2; the blocked
+// order is taken where it reads less (at 256 CUs: more than 8 row tiles). Measured at 3048
+// rows (12 row tiles): K1 1.3-1.6% faster, with blocks of 8 slabs x 4 row tiles.
+void tile_blocking(int RT, int cus, int* blk_slabs, int* blk_rows) {
+  constexpr int kRows = 4;
+  const int c = std::max(1, cus / 8);
+  *blk_slabs = 0;
+  *blk_rows = 0;
+  if (RT > kRows && (double)c / RT + RT > (double)c / kRows + kRows) {
+    *blk_slabs = std::max(1, c / kRows);
+    *blk_rows = kRows;
+  }
+}
+
 // The tile asv_verify_args.k1_tile_rows asks for; false for a value that names no tile.
 bool forced_tile(int rows, Tile* t) {
   switch (rows) {
@@ -179,12 +198,14 @@ void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStrea
   static_assert(TV == kPackRowsTarget && BK == kPackDepth, "a stage is one packed tile");
   const int RT = (a->N + TR - 1) / TR;
   const int grid = n_slabs * RT;
+  int blk_slabs = 0, blk_rows = 0;
+  tile_blocking(RT, cu_count(), &blk_slabs, &blk_rows);
   k_lmhead_partial<TV, TR, WV, WR, BK, NST, LOOP><<<grid, WV * WR * kWave, 0, s>>>(
       a->hidden, a->w_lm, a->parent, a->draft_tok, a->req_offsets, a->B, a->N, a->H, a->V,
       L.S, slab0, RT, reinterpret_cast<float*>(ws + L.off_rec_m),
       reinterpret_cast<float*>(ws + L.off_rec_s), reinterpret_cast<int32_t*>(ws + L.off_rec_a),
       a->drafted_logit, reinterpret_cast<int32_t*>(ws + L.off_cnt), a->B + 1,
-      a->w_lm_layout == ASV_W_PACKED ? 1 : 0);
+      a->w_lm_layout == ASV_W_PACKED ? 1 : 0, blk_slabs, blk_rows);
 }
 
 // Total bytes of the packed copy of a [V][H] weight whose K blocks hold V rounded up to

@@ -181,6 +181,35 @@ __device__ __forceinline__ int xcd_tile(int bid, int G) {
   return xcd * q + min(xcd, rem) + loc;
 }
 
+// Tile t of a launch over n_slabs vocabulary slabs x RT row tiles -> (slab within the launch,
+// row tile). With blk_rows = 0 the order is slab-major (the row tiles of one slab are
+// consecutive). Otherwise the slabs go in blocks of blk_slabs, each block's tiles in groups of
+// blk_rows row tiles (the last group takes the rest), slab-major within a group: a run of
+// blk_slabs * blk_rows consecutive tiles, which xcd_tile keeps on one XCD, then reads
+// blk_slabs W slabs and blk_rows X row tiles through that XCD's L2 instead of about
+// blk_slabs * blk_rows / RT slabs and all RT row tiles. Every (slab, row tile) pair is taken
+// once; the order changes no result.
+__device__ __forceinline__ void tile_coords(int t, int n_slabs, int RT, int blk_slabs,
+                                            int blk_rows, int& slab, int& rt) {
+  if (blk_rows <= 0 || blk_rows >= RT) {
+    slab = t / RT;
+    rt = t % RT;
+    return;
+  }
+  const int blk = t / (blk_slabs * RT), rem = t % (blk_slabs * RT);
+  const int sb = min(blk_slabs, n_slabs - blk * blk_slabs);  // slabs in this block
+  const int group = sb * blk_rows, full_groups = RT / blk_rows;
+  if (rem < full_groups * group) {
+    const int g = rem / group, in = rem % group;
+    slab = blk * blk_slabs + in / blk_rows;
+    rt = g * blk_rows + in % blk_rows;
+  } else {
+    const int rest = RT - full_groups * blk_rows, in = rem - full_groups * group;
+    slab = blk * blk_slabs + in / rest;
+    rt = full_groups * blk_rows + in % rest;
+  }
+}
+
 // What every K loop of a tile shares: this wave's place in the tile; one buffer resource per
 // operand covering only the tile's valid rows (rows past V in the last slab or past N in the
 // last row tile read as zeros and never touch memory outside the arrays; their results are
@@ -575,7 +604,7 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
                       int S, int slab0, int RT, float* __restrict__ rec_m,
                       float* __restrict__ rec_s, int32_t* __restrict__ rec_a,
                       float* __restrict__ drafted_logit, int32_t* __restrict__ done_cnt,
-                      int n_cnt, int w_packed) {
+                      int n_cnt, int w_packed, int blk_slabs, int blk_rows) {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST, MF>;
   constexpr int T = C::kThreads;
   constexpr int kBlock = MF::kBlock, kRegs = MF::kRegs;
@@ -586,11 +615,12 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
   const int wv = wave % WV, wr = wave / WV;
   // clear the per-request completion counters of the finishing kernel that follows
   for (int i = blockIdx.x * T + tid; i < n_cnt; i += gridDim.x * T) done_cnt[i] = 0;
-  // consecutive tiles are the row tiles of one slab, which share the W slab through L2; this
-  // launch covers slabs slab0 .. slab0 + gridDim.x / RT - 1 of the S slabs
+  // consecutive tiles share W slabs and X row tiles through one XCD's L2; this launch covers
+  // slabs slab0 .. slab0 + gridDim.x / RT - 1 of the S slabs
   const int tile = xcd_tile(blockIdx.x, gridDim.x);
-  const int slab = slab0 + tile / RT;
-  const int rt = tile % RT;
+  int slab, rt;
+  tile_coords(tile, gridDim.x / RT, RT, blk_slabs, blk_rows, slab, rt);
+  slab += slab0;
   const int v0 = slab * TV, r0 = rt * TR;
   const int v_end = min(v0 + TV, V);
   const int r_last = min(r0 + TR, N) - 1;

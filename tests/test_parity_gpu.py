@@ -132,6 +132,17 @@ def _case(name):
         # one ragged 192-row tile over H = 192 (three K stages)
         trees = [_rand_tree(rng, int(rng.integers(36, 48)), 6, 4) for _ in range(4)]
         return custom_workload(name, 192, 1300, trees, 0.3, seed=15, w_std=0.09)
+    if name == "blocked_tile_order":
+        # about 2600 rows: 11 row tiles of 256 (more than 8, so on 256 CUs the tiles run in
+        # blocks of 8 slabs x 4 row tiles: row groups of 4, 4 and 3) over 11 slabs, the last
+        # block of 3 slabs and a ragged last slab of 77 entries
+        trees, n = [], 0
+        while n < 2600:
+            t = _rand_tree(rng, min(int(rng.integers(16, 120)), 2600 - n), 9, 4)
+            trees.append(t)
+            n += len(t)
+        return custom_workload(name, 128, 10 * 256 + 77, trees, 0.2, seed=16, w_std=0.11,
+                               draft_logits=True)
     raise KeyError(name)
 
 
@@ -191,6 +202,31 @@ def test_every_tile_same_results(asv, dev):
     W = w.weights()
     resolve_with_oracle(w, oracle.widen_weights(W))
     runs = {rows: _run(asv, w, W, dev, k1_tile=rows) for rows in (64, 128, 192, 256)}
+    base = runs[64]
+    nonroot = w.parent >= 0
+    for rows, got in runs.items():
+        for k in ("row_max", "row_argmax", "accept", "accepted_len", "accepted_path",
+                  "bonus_token", "draft_conf"):
+            assert np.array_equal(got[k], base[k], equal_nan=True), (rows, k)
+        assert np.array_equal(got["drafted_logit"][nonroot], base["drafted_logit"][nonroot]), rows
+        assert np.allclose(got["row_lse"], base["row_lse"], rtol=1e-6, atol=1e-6), rows
+
+
+def test_blocked_tile_order(asv, dev):
+    """Launches of many row tiles take their tiles in blocks of slabs x row tiles (ragged row
+    groups and a ragged last block here, on every tile family: 11 to 41 row tiles). Every
+    (slab, row tile) pair must run once: the records match the oracle's, and all four tile
+    families agree bit for bit as in test_every_tile_same_results."""
+    print("[blocked order] case=blocked_tile_order", flush=True)
+    w = _case("blocked_tile_order")
+    W = w.weights()
+    w64 = oracle.widen_weights(W)
+    resolve_with_oracle(w, w64)
+    ref = reference(w, w64)
+    runs = {}
+    for rows in (256, 192, 128, 64):
+        runs[rows] = _run(asv, w, W, dev, k1_tile=rows, packed=rows == 256)
+        compare(w, ref, runs[rows], tag=f"blocked order tile={rows}")
     base = runs[64]
     nonroot = w.parent >= 0
     for rows, got in runs.items():
