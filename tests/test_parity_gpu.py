@@ -237,6 +237,29 @@ def test_blocked_tile_order(asv, dev):
         assert np.allclose(got["row_lse"], base["row_lse"], rtol=1e-6, atol=1e-6), rows
 
 
+def test_long_hidden_16384(asv, dev):
+    """H = 16384 (256 K stages, the hidden size of the largest Llama-3.1 model): every K loop
+    (the burst ring of the 64-row tile, the three-slot loop of the 128-row tile and the two-slot
+    loop of the 256-row tile) wraps its ring 128 times or more, on both weight layouts; the
+    records, drafted logits and walks match the oracle."""
+    print("[long hidden] H=16384", flush=True)
+    rng = np.random.default_rng(16384)
+    trees, n = [], 0
+    while n < 300:
+        t = _rand_tree(rng, min(int(rng.integers(10, 70)), 300 - n), 8, 4)
+        trees.append(t)
+        n += len(t)
+    w = custom_workload("long_hidden", 16384, 6000 + 77, trees, 0.2, seed=17, w_std=0.02,
+                        draft_logits=True)
+    W = w.weights()
+    w64 = oracle.widen_weights(W)
+    resolve_with_oracle(w, w64)
+    ref = reference(w, w64)
+    for rows, packed in ((64, False), (128, True), (256, False), (256, True)):
+        got = _run(asv, w, W, dev, k1_tile=rows, packed=packed)
+        compare(w, ref, got, tag=f"long hidden tile={rows} packed={packed}")
+
+
 @pytest.mark.parametrize("N", [150, 200, 378])
 def test_two_family_plan(asv, dev, N):
     """At V = 151936 and these row counts the library splits the vocabulary slabs between two
