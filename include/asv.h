@@ -360,10 +360,13 @@ int asv_state_init(asv_req_state *state, int32_t B, const asv_params *p, void *s
  * (asv_verify, asv_draft_step) are these calls with a NULL asv_tuning. */
 
 typedef struct asv_tuning {
-  void   *begin_event;            /* optional hipEvent_t recorded on `stream` just before the
-                                     LM-head kernel (K1 of asv_verify, the draft LM head of
-                                     asv_draft_step), or NULL */
-  void   *end_event;              /* optional hipEvent_t recorded just after it, or NULL */
+  void   *begin_event;            /* optional hipEvent_t (created by the caller) set to the
+                                     start time of the LM-head kernel's first launch (K1 of
+                                     asv_verify, the draft LM head of asv_draft_step), taken from
+                                     the dispatch itself (hipExtLaunchKernel), or NULL */
+  void   *end_event;              /* optional hipEvent_t set to the end time of its last
+                                     launch, or NULL; hipEventElapsedTime(begin, end) is then
+                                     the kernel's own time, without event-record packets */
   int32_t tile_rows;              /* asv_verify only: tree rows per LM-head tile. 0 lets the
                                      library pick it from N, V and the device's compute-unit
                                      count; 64, 128, 192 or 256 force that tile (every tile

@@ -1,6 +1,7 @@
 // Host side of libasv: argument checks, workspace layouts, tile selection and the launch
 // sequences of one verification step, one draft step, the pruning of the draft trees, the
 // tree-attention metadata and the commit. Every entry point is declared in include/asv.h.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -191,17 +192,28 @@ bool params_ok(const asv_params& p) {
 }
 
 // K1 over the vocabulary slabs [slab0, slab0 + n_slabs).
+// Launches `kernel` on `s`; with a start or stop event (measurement only) through
+// hipExtLaunchKernelGGL, which sets the events to the dispatch's own start and end times.
+template <typename F, typename... Args>
+void launch_timed(F kernel, int grid, int threads, hipStream_t s, hipEvent_t start,
+                  hipEvent_t stop, Args... args) {
+  if (start || stop)
+    hipExtLaunchKernelGGL(kernel, dim3(grid), dim3(threads), 0, s, start, stop, 0, args...);
+  else
+    kernel<<<grid, threads, 0, s>>>(args...);
+}
+
 template <int TV, int TR, int WV, int WR, int BK, int NST, int LOOP = 0>
 void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStream_t s,
-                   int slab0, int n_slabs) {
+                   int slab0, int n_slabs, hipEvent_t start, hipEvent_t stop) {
   static_assert(TV == kSlab, "tiles span exactly one record slab");
   static_assert(TV == kPackRowsTarget && BK == kPackDepth, "a stage is one packed tile");
   const int RT = (a->N + TR - 1) / TR;
   const int grid = n_slabs * RT;
   int blk_slabs = 0, blk_rows = 0;
   tile_blocking(RT, cu_count(), &blk_slabs, &blk_rows);
-  k_lmhead_partial<TV, TR, WV, WR, BK, NST, LOOP><<<grid, WV * WR * kWave, 0, s>>>(
-      a->hidden, a->w_lm, a->parent, a->draft_tok, a->req_offsets, a->B, a->N, a->H, a->V,
+  launch_timed(k_lmhead_partial<TV, TR, WV, WR, BK, NST, LOOP>, grid, WV * WR * kWave, s, start,
+               stop, a->hidden, a->w_lm, a->parent, a->draft_tok, a->req_offsets, a->B, a->N, a->H, a->V,
       L.S, slab0, RT, reinterpret_cast<float*>(ws + L.off_rec_m),
       reinterpret_cast<float*>(ws + L.off_rec_s), reinterpret_cast<int32_t*>(ws + L.off_rec_a),
       a->drafted_logit, reinterpret_cast<int32_t*>(ws + L.off_cnt), a->B + 1,
@@ -307,12 +319,13 @@ bool draft_sizes_ok(int B, int H, int V) {
 }
 
 template <int TV, int TR, int WV, int WR, int BK, int NST>
-void launch_draft(const asv_draft_args* a, const DraftLayout& L, char* ws, hipStream_t s) {
+void launch_draft(const asv_draft_args* a, const DraftLayout& L, char* ws, hipStream_t s,
+                  hipEvent_t start, hipEvent_t stop) {
   static_assert(BK == kPackDepth && TV % kPackRowsDraft == 0 && 128 % TV == 0,
                 "a stage is one or two consecutive packed draft tiles");
   const int R = a->B * kTopK;
   const int RT = (R + TR - 1) / TR;
-  k_draft_partial<TV, TR, WV, WR, BK, NST><<<L.S * RT, WV * WR * kWave, 0, s>>>(
+  launch_timed(k_draft_partial<TV, TR, WV, WR, BK, NST>, L.S * RT, WV * WR * kWave, s, start, stop,
       a->hidden, a->w_draft, R, a->H, a->V, L.S, RT, reinterpret_cast<uint64_t*>(ws + L.off_k),
       reinterpret_cast<float*>(ws + L.off_s), a->w_draft_layout == ASV_W_PACKED ? 1 : 0);
 }
@@ -351,14 +364,6 @@ void* scratch_address() {
     addr[dev] = p;
   }
   return addr[dev];
-}
-
-int record_event(void* ev, hipStream_t s, const char* what) {
-  if (!ev) return ASV_OK;
-  const hipError_t e = hipEventRecord(reinterpret_cast<hipEvent_t>(ev), s);
-  if (e == hipSuccess) return ASV_OK;
-  set_error(what, e);
-  return ASV_EHIP;
 }
 
 }  // namespace
@@ -445,10 +450,12 @@ extern "C" int asv_verify_tuned(const asv_verify_args* a, const asv_tuning* tuni
     if (int rc = launch_status("k_draft_conf_partial")) return rc;
   }
 
-  if (int rc = record_event(tu.begin_event, s, "hipEventRecord(begin_event)")) return rc;
   const K1Plan plan = tu.tile_rows != 0 ? K1Plan{forced, forced, L.S}
                                          : plan_k1(a->N, L.S, cu_count());
-  auto launch = [&](Tile tile, int slab0, int n_slabs) {
+  // timing events (measurement only): the start of the first launch, the end of the last
+  const hipEvent_t ev_begin = reinterpret_cast<hipEvent_t>(tu.begin_event);
+  const hipEvent_t ev_end = reinterpret_cast<hipEvent_t>(tu.end_event);
+  auto launch = [&](Tile tile, int slab0, int n_slabs, hipEvent_t start, hipEvent_t stop) {
     switch (tile) {
       // <vocab rows, tree rows, waves along vocab, waves along rows, K per stage, ring depth,
       // K loop>, each the fastest of a sweep on MI355X for its row range. The weight-streaming
@@ -457,22 +464,22 @@ extern "C" int asv_verify_tuned(const asv_verify_args* a, const asv_tuning* tuni
       // over ten placements of W. The 128-, 192- and 256-row tiles run the spread K loops
       // (copies spaced between the MFMAs), in interleaved comparisons 28% faster than the
       // burst ring at 378 rows and 20% at 2048 and 3048 rows.
-      case Tile::kRows64: launch_lmhead<256, 64, 4, 1, 64, 2>(a, L, ws, s, slab0, n_slabs); break;
+      case Tile::kRows64: launch_lmhead<256, 64, 4, 1, 64, 2>(a, L, ws, s, slab0, n_slabs, start, stop); break;
       case Tile::kRows128:
-        launch_lmhead<256, 128, 2, 2, 64, 3, 3>(a, L, ws, s, slab0, n_slabs);
+        launch_lmhead<256, 128, 2, 2, 64, 3, 3>(a, L, ws, s, slab0, n_slabs, start, stop);
         break;
       case Tile::kRows192:
-        launch_lmhead<256, 192, 2, 2, 64, 2, 2>(a, L, ws, s, slab0, n_slabs);
+        launch_lmhead<256, 192, 2, 2, 64, 2, 2>(a, L, ws, s, slab0, n_slabs, start, stop);
         break;
       case Tile::kRows256:
-        launch_lmhead<256, 256, 2, 2, 64, 2, 2>(a, L, ws, s, slab0, n_slabs);
+        launch_lmhead<256, 256, 2, 2, 64, 2, 2>(a, L, ws, s, slab0, n_slabs, start, stop);
         break;
     }
   };
-  launch(plan.a, 0, plan.n1);
-  if (plan.n1 < L.S) launch(plan.b, plan.n1, L.S - plan.n1);
+  const bool two = plan.n1 < L.S;
+  launch(plan.a, 0, plan.n1, ev_begin, two ? nullptr : ev_end);
+  if (two) launch(plan.b, plan.n1, L.S - plan.n1, nullptr, ev_end);
   if (int rc = launch_status("k_lmhead_partial")) return rc;
-  if (int rc = record_event(tu.end_event, s, "hipEventRecord(end_event)")) return rc;
 
   const AcceptArgs acc = accept_args(a, L, ws, conf);
   const float* rec_m = reinterpret_cast<const float*>(ws + L.off_rec_m);
@@ -568,15 +575,18 @@ extern "C" int asv_draft_step_tuned(const asv_draft_args* a, const asv_tuning* t
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
   (void)hipGetLastError();
-  if (int rc = record_event(tu.begin_event, s, "hipEventRecord(begin_event)")) return rc;
+  // timing events (measurement only): the start and the end of the draft LM head's launch
+  const hipEvent_t ev_begin = reinterpret_cast<hipEvent_t>(tu.begin_event);
+  const hipEvent_t ev_end = reinterpret_cast<hipEvent_t>(tu.end_event);
   switch (pick_draft_tile(a->B * kTopK)) {
     // <vocab rows, draft rows, waves along vocab, waves along rows, K per stage, ring depth>
-    case DraftTile::kRows32: launch_draft<64, 32, 2, 1, 64, 4>(a, L, ws, s); break;
-    case DraftTile::kRows64: launch_draft<64, 64, 2, 2, 64, 4>(a, L, ws, s); break;
-    case DraftTile::kRows128: launch_draft<128, 128, 2, 4, 64, 3>(a, L, ws, s); break;
+    case DraftTile::kRows32: launch_draft<64, 32, 2, 1, 64, 4>(a, L, ws, s, ev_begin, ev_end); break;
+    case DraftTile::kRows64: launch_draft<64, 64, 2, 2, 64, 4>(a, L, ws, s, ev_begin, ev_end); break;
+    case DraftTile::kRows128:
+      launch_draft<128, 128, 2, 4, 64, 3>(a, L, ws, s, ev_begin, ev_end);
+      break;
   }
   if (int rc = launch_status("k_draft_partial")) return rc;
-  if (int rc = record_event(tu.end_event, s, "hipEventRecord(end_event)")) return rc;
   DraftGrowArgs g;
   g.B = a->B;
   g.S = L.S;
