@@ -10,7 +10,8 @@ seeded synthetic inputs already resident in HBM. The headline workload is the Ll
 shaped batch-1 verify (H=4096, V=128256, one 60-node EAGLE-style tree, kappa=0.3); the
 32x64-node batch (2048 rows) is measured after it as the MFMA-bound point. Prints one JSON
 line: verified tree nodes per second, the LM-head kernel's roofline fraction (its duration
-from HIP events recorded around it in every timed step) and the CPU oracle's throughput on a
+from HIP events that carry its dispatches' start and end times, in a second timed pass) and
+the CPU oracle's throughput on a
 bounded sample of the same workload. The JSON line also carries the draft step that precedes
 verification (``draft``: the draft LM head reduced to each row's top-4, and one tree-growth
 step) on the EAGLE-3-shaped draft head at batch 1 and 32, with its kernel's roofline.
@@ -173,9 +174,9 @@ def measure(cfg: int, steps: int, warmup: int, dev, hip: HipEvents, tau=None,
         step()
     torch.cuda.synchronize()
     dt = time.perf_counter() - t0
-    # Timed region 2: the same steps with HIP events recorded just before and after the
-    # LM-head kernel on the stream it runs on (each record costs the GPU a few microseconds,
-    # so this region is kept out of the throughput).
+    # Timed region 2: the same steps with HIP events set to the start of the LM-head kernel's
+    # first launch and the end of its last, on the stream it runs on (the library passes them
+    # to hipExtLaunchKernelGGL; this region is kept out of the throughput).
     torch.cuda.synchronize()
     for i in range(steps):
         step(evs[i])

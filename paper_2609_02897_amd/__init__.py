@@ -232,8 +232,8 @@ def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None,
     req_offsets int32 [B+1]; tau float32 [B]; draft_logits float32 [N, V] or None; state u8
     [B, 112] (in/out) or None. ``out`` and ``workspace`` may be passed to reuse buffers
     (checked against these sizes). Measurement and tuning go through ``asv_verify_tuned``:
-    ``k1_events`` is an optional pair of raw hipEvent_t handles recorded around the LM-head
-    kernel, and ``k1_tile`` forces the LM-head tile (64, 128, 192 or 256 tree rows); 0 lets the
+    ``k1_events`` is an optional pair of raw hipEvent_t handles set to the start and end of
+    the LM-head kernel's launches, and ``k1_tile`` forces the LM-head tile (64, 128, 192 or 256 tree rows); 0 lets the
     library pick it. Without either, the product entry point ``asv_verify`` is called.
     ``noalloc`` calls ``asv_verify_noalloc`` instead, whose workspace is the library's static
     device scratch (no workspace tensor; pass ``out`` to allocate nothing at all here either).
