@@ -203,6 +203,13 @@ void launch_timed(F kernel, int grid, int threads, hipStream_t s, hipEvent_t sta
     kernel<<<grid, threads, 0, s>>>(args...);
 }
 
+// Launches of at most this many row tiles copy W with the non-temporal hint (the one or two
+// tiles of a slab read it about once); more row tiles share each W slab through an XCD's L2
+// and keep the default policy. Against the earlier rule (the hint for tiles of up to 128 rows)
+// in same-box A/Bs: 260, 300, 378 and 450 rows 3% faster, 150 rows 1.4%, 500 rows 1%; 128,
+// 200 and 600 to 3048 rows level.
+constexpr int kStreamWMaxRowTiles = 2;
+
 template <int TV, int TR, int WV, int WR, int BK, int NST, int LOOP = 0>
 void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStream_t s,
                    int slab0, int n_slabs, hipEvent_t start, hipEvent_t stop) {
@@ -212,12 +219,19 @@ void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStrea
   const int grid = n_slabs * RT;
   int blk_slabs = 0, blk_rows = 0;
   tile_blocking(RT, cu_count(), &blk_slabs, &blk_rows);
-  launch_timed(k_lmhead_partial<TV, TR, WV, WR, BK, NST, LOOP>, grid, WV * WR * kWave, s, start,
-               stop, a->hidden, a->w_lm, a->parent, a->draft_tok, a->req_offsets, a->B, a->N, a->H, a->V,
-      L.S, slab0, RT, reinterpret_cast<float*>(ws + L.off_rec_m),
-      reinterpret_cast<float*>(ws + L.off_rec_s), reinterpret_cast<int32_t*>(ws + L.off_rec_a),
-      a->drafted_logit, reinterpret_cast<int32_t*>(ws + L.off_cnt), a->B + 1,
-      a->w_lm_layout == ASV_W_PACKED ? 1 : 0, blk_slabs, blk_rows);
+  auto go = [&](auto kernel) {
+    launch_timed(kernel, grid, WV * WR * kWave, s, start, stop, a->hidden, a->w_lm, a->parent,
+                 a->draft_tok, a->req_offsets, a->B, a->N, a->H, a->V, L.S, slab0, RT,
+                 reinterpret_cast<float*>(ws + L.off_rec_m),
+                 reinterpret_cast<float*>(ws + L.off_rec_s),
+                 reinterpret_cast<int32_t*>(ws + L.off_rec_a), a->drafted_logit,
+                 reinterpret_cast<int32_t*>(ws + L.off_cnt), a->B + 1,
+                 a->w_lm_layout == ASV_W_PACKED ? 1 : 0, blk_slabs, blk_rows);
+  };
+  if (RT <= kStreamWMaxRowTiles)
+    go(k_lmhead_partial<TV, TR, WV, WR, BK, NST, LOOP, true>);
+  else
+    go(k_lmhead_partial<TV, TR, WV, WR, BK, NST, LOOP, false>);
 }
 
 // Total bytes of the packed copy of a [V][H] weight whose K blocks hold V rounded up to
@@ -464,7 +478,9 @@ extern "C" int asv_verify_tuned(const asv_verify_args* a, const asv_tuning* tuni
       // over ten placements of W. The 128-, 192- and 256-row tiles run the spread K loops
       // (copies spaced between the MFMAs), in interleaved comparisons 28% faster than the
       // burst ring at 378 rows and 20% at 2048 and 3048 rows.
-      case Tile::kRows64: launch_lmhead<256, 64, 4, 1, 64, 2>(a, L, ws, s, slab0, n_slabs, start, stop); break;
+      case Tile::kRows64:
+        launch_lmhead<256, 64, 4, 1, 64, 2>(a, L, ws, s, slab0, n_slabs, start, stop);
+        break;
       case Tile::kRows128:
         launch_lmhead<256, 128, 2, 2, 64, 3, 3>(a, L, ws, s, slab0, n_slabs, start, stop);
         break;
@@ -580,8 +596,12 @@ extern "C" int asv_draft_step_tuned(const asv_draft_args* a, const asv_tuning* t
   const hipEvent_t ev_end = reinterpret_cast<hipEvent_t>(tu.end_event);
   switch (pick_draft_tile(a->B * kTopK)) {
     // <vocab rows, draft rows, waves along vocab, waves along rows, K per stage, ring depth>
-    case DraftTile::kRows32: launch_draft<64, 32, 2, 1, 64, 4>(a, L, ws, s, ev_begin, ev_end); break;
-    case DraftTile::kRows64: launch_draft<64, 64, 2, 2, 64, 4>(a, L, ws, s, ev_begin, ev_end); break;
+    case DraftTile::kRows32:
+      launch_draft<64, 32, 2, 1, 64, 4>(a, L, ws, s, ev_begin, ev_end);
+      break;
+    case DraftTile::kRows64:
+      launch_draft<64, 64, 2, 2, 64, 4>(a, L, ws, s, ev_begin, ev_end);
+      break;
     case DraftTile::kRows128:
       launch_draft<128, 128, 2, 4, 64, 3>(a, L, ws, s, ev_begin, ev_end);
       break;

@@ -222,10 +222,10 @@ __device__ __forceinline__ void tile_coords(int t, int n_slabs, int RT, int blk_
 // consecutive [BK]-wide row segments, so the TV rows of slab s at K block k are one contiguous
 // run starting at element k Vp BK + v0 BK. Offsets within the packed buffer are 32-bit
 // unsigned (the host keeps it under 4 GiB).
-// STREAM_W: copy W with the non-temporal hint. The default suits K1: its tiles of up to 128
-// rows are weight-bound or close to it and read W faster with the hint (60 rows: 13% less
-// time), while the larger tiles share each W slab between the row tiles of one XCD through
-// its L2 and keep the default policy (the hint measured within noise there).
+// STREAM_W: copy W with the non-temporal hint. K1 takes it for launches of one or two row
+// tiles, which read each W slab about once (60 rows: 13% less time), and the default policy
+// for more row tiles, which share each W slab through an XCD's L2 (with the hint: 378 rows'
+// three 128-row tiles a slab about 2% slower, 2048 and 3048 rows 1.5% and 4.5%).
 template <int TV, int TR, int WV, int WR, int BK, int NST, bool STREAM_W = (TR <= 128),
           class MF = Mfma32>
 struct TileIo {
@@ -411,7 +411,7 @@ __device__ __forceinline__ void wait_lds_barrier() {
 // accumulate in the same K order as lmhead_tile, so the logits are bit-identical. The
 // schedule is branch-free: past the last stage the copies repeat the last stage into the slot
 // just freed (never read again) and the reads of the stage after the last are discarded.
-template <int TV, int TR, int WV, int WR, class MF = Mfma32>
+template <int TV, int TR, int WV, int WR, bool STREAM_W, class MF = Mfma32>
 __device__ __forceinline__ void lmhead_tile_spread(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int N, int H, int V,
     int v0, int r0, uint4* smem, int w_packed,
@@ -440,8 +440,8 @@ __device__ __forceinline__ void lmhead_tile_spread(
     return n;
   }();
 
-  const TileIo<TV, TR, WV, WR, BK, NST, (TR <= 128), MF> io(X, W, N, H, V, v0, r0, smem,
-                                                           w_packed);
+  const TileIo<TV, TR, WV, WR, BK, NST, STREAM_W, MF> io(X, W, N, H, V, v0, r0, smem,
+                                                        w_packed);
   const int KT = H / BK;
   auto issue_copy = [&](int slot, int ks, auto cc) {
     io.template copy<decltype(cc)::value>(slot, ks);
@@ -511,7 +511,7 @@ __device__ __forceinline__ void lmhead_tile_spread(
 //   m >= Q2         read the first half's fragments of stage k + 1; the first copies of
 //                   stage k + 3.
 // Past the last stage the copies repeat the last stage into slots no later stage reads.
-template <int TV, int TR, int WV, int WR, class MF = Mfma32>
+template <int TV, int TR, int WV, int WR, bool STREAM_W, class MF = Mfma32>
 __device__ __forceinline__ void lmhead_tile_spread3(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int N, int H, int V,
     int v0, int r0, uint4* smem, int w_packed,
@@ -538,8 +538,8 @@ __device__ __forceinline__ void lmhead_tile_spread3(
     return n;
   }();
 
-  const TileIo<TV, TR, WV, WR, BK, NST, (TR <= 128), MF> io(X, W, N, H, V, v0, r0, smem,
-                                                           w_packed);
+  const TileIo<TV, TR, WV, WR, BK, NST, STREAM_W, MF> io(X, W, N, H, V, v0, r0, smem,
+                                                        w_packed);
   const int KT = H / BK;
   // copy c of stage j into slot j % 3, from K stage min(j, KT - 1)
   auto issue_copy = [&](int j, auto cc) {
@@ -592,11 +592,13 @@ __device__ __forceinline__ void lmhead_tile_spread3(
 }
 
 // LOOP selects the K loop: 0 = the burst ring of lmhead_tile; 2 and 3 = the spread loop of
-// that ring depth (lmhead_tile_spread, lmhead_tile_spread3). MF is the MFMA shape; every tile
+// that ring depth (lmhead_tile_spread, lmhead_tile_spread3). STREAM_W: the W copies' cache
+// policy (see TileIo); it changes no result. MF is the MFMA shape; every tile
 // family of K1 runs the same one, so that all of them sum each logit's products in the same
 // order and give the same logits bit for bit. One launch covers a contiguous range of
 // vocabulary slabs (all of them, or one of two ranges whose tiles differ in height).
-template <int TV, int TR, int WV, int WR, int BK, int NST, int LOOP = 0, class MF = Mfma16>
+template <int TV, int TR, int WV, int WR, int BK, int NST, int LOOP, bool STREAM_W,
+          class MF = Mfma16>
 __global__ __launch_bounds__(WV * WR * kWave, 1)
 void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                       const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
@@ -649,14 +651,16 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
   typename MF::Acc acc[C::MV][C::MR];
   if constexpr (LOOP == 2) {
     static_assert(BK == 64 && NST == 2, "two-slot spread loop: 64-deep stages");
-    lmhead_tile_spread<TV, TR, WV, WR, MF>(X, W, N, H, V, v0, r0, smem, w_packed, acc);
+    lmhead_tile_spread<TV, TR, WV, WR, STREAM_W, MF>(X, W, N, H, V, v0, r0, smem, w_packed,
+                                                     acc);
   } else if constexpr (LOOP == 3) {
     static_assert(BK == 64 && NST == 3, "three-slot spread loop: 64-deep stages");
-    lmhead_tile_spread3<TV, TR, WV, WR, MF>(X, W, N, H, V, v0, r0, smem, w_packed, acc);
+    lmhead_tile_spread3<TV, TR, WV, WR, STREAM_W, MF>(X, W, N, H, V, v0, r0, smem, w_packed,
+                                                      acc);
   } else {
     static_assert(LOOP == 0, "K loop");
-    lmhead_tile<TV, TR, WV, WR, BK, NST, (TR <= 128), MF>(X, W, N, H, V, v0, r0, smem,
-                                                          w_packed, acc);
+    lmhead_tile<TV, TR, WV, WR, BK, NST, STREAM_W, MF>(X, W, N, H, V, v0, r0, smem,
+                                                       w_packed, acc);
   }
 
   // Output block (i, j), register e of a lane holds vocab row kBlock i + MF::row_of(lane, e)
