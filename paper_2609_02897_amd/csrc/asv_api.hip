@@ -136,6 +136,12 @@ void tile_blocking(int RT, int cus, int* blk_slabs, int* blk_rows) {
   }
 }
 
+// Whether a launch of `tiles` 64-row tiles runs the one-slot ring: its workgroups fit three
+// per CU but not two. Same-box A/Bs (K1, up to 64 rows): at V = 151936 (594 tiles on 256
+// CUs) 5.3% faster at 60 rows and 2.2% at 30; outside this range it was slower (V = 64000,
+// 250 tiles: +7%; V = 200000, 782 tiles: +6%) or level (V = 128256, 501 tiles).
+bool one_slot_64(int tiles, int cus) { return tiles > 2 * cus && tiles <= 3 * cus; }
+
 // The tile asv_verify_args.k1_tile_rows asks for; false for a value that names no tile.
 bool forced_tile(int rows, Tile* t) {
   switch (rows) {
@@ -479,7 +485,13 @@ extern "C" int asv_verify_tuned(const asv_verify_args* a, const asv_tuning* tuni
       // (copies spaced between the MFMAs), in interleaved comparisons 28% faster than the
       // burst ring at 378 rows and 20% at 2048 and 3048 rows.
       case Tile::kRows64:
-        launch_lmhead<256, 64, 4, 1, 64, 2>(a, L, ws, s, slab0, n_slabs, start, stop);
+        // the one-slot ring (three workgroups per CU) when the two-slot ring (two per CU)
+        // would leave a second, partial round of workgroups and three per CU take them all at
+        // once (at 256 CUs and up to 64 rows: 513 to 768 slabs, e.g. V = 151936)
+        if (one_slot_64(n_slabs * ((a->N + 63) / 64), cu_count()))
+          launch_lmhead<256, 64, 4, 1, 64, 1, 1>(a, L, ws, s, slab0, n_slabs, start, stop);
+        else
+          launch_lmhead<256, 64, 4, 1, 64, 2>(a, L, ws, s, slab0, n_slabs, start, stop);
         break;
       case Tile::kRows128:
         launch_lmhead<256, 128, 2, 2, 64, 3, 3>(a, L, ws, s, slab0, n_slabs, start, stop);

@@ -166,10 +166,10 @@ struct LmheadCfg {
                 kWaveR % MF::kBlock == 0, "whole MFMA blocks");
   static_assert(MV >= 1 && MR >= 1, "tile too small for the wave grid");
   static_assert(BK == 32 || BK == 64, "stage depth");
-  static_assert(NST >= 2 && NST <= 5, "ring depth");
+  static_assert(NST >= 1 && NST <= 5, "ring depth");
   static_assert(DW >= 1 && DX >= 1 && DW * kWaves * 1024 == kStageW &&
                 DX * kWaves * 1024 == kStageX, "each wave copies whole 1 KB groups");
-  static_assert((NST - 2) * kLoads <= 63, "vmcnt range");
+  static_assert(NST < 2 || (NST - 2) * kLoads <= 63, "vmcnt range");
   static_assert(kLds <= 160 * 1024, "LDS per workgroup");
 };
 
@@ -393,6 +393,48 @@ __device__ __forceinline__ void wait_lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" : : : "memory");
 }
 
+// The same logits as lmhead_tile with a one-slot ring, for weight-streaming tiles that run
+// three workgroups per CU: each wave reads a whole stage's fragments into registers, the
+// workgroup frees the slot and refills it with the next stage while this stage's MFMAs run.
+// A stage's copy latency is exposed per workgroup and hidden by the other workgroups of the
+// CU. MFMAs accumulate in lmhead_tile's K order, so the logits are bit-identical.
+template <int TV, int TR, int WV, int WR, int BK, bool STREAM_W, class MF>
+__device__ __forceinline__ void lmhead_tile_1slot(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, int N, int H, int V,
+    int v0, int r0, uint4* smem, int w_packed,
+    typename MF::Acc (&acc)[LmheadCfg<TV, TR, WV, WR, BK, 1, MF>::MV]
+                           [LmheadCfg<TV, TR, WV, WR, BK, 1, MF>::MR]) {
+  using C = LmheadCfg<TV, TR, WV, WR, BK, 1, MF>;
+  const TileIo<TV, TR, WV, WR, BK, 1, STREAM_W, MF> io(X, W, N, H, V, v0, r0, smem, w_packed);
+  const int KT = H / BK;
+  auto issue_stage = [&](int ks) {
+    static_for<C::kLoads>([&](auto cc) { io.template copy<decltype(cc)::value>(0, ks); });
+  };
+  zero_acc(acc);
+  constexpr int NS = C::NS;
+  bf16x8 fa[NS][C::MV], fb[NS][C::MR];
+  issue_stage(0);
+  for (int k = 0; k < KT; ++k) {
+    wait_vm_barrier<0>();                 // stage k has landed in the slot
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+#pragma unroll
+      for (int i = 0; i < C::MV; ++i) fa[s][i] = io.w_frag(0, s, i);
+#pragma unroll
+      for (int j = 0; j < C::MR; ++j) fb[s][j] = io.x_frag(0, s, j);
+    }
+    wait_lds_barrier();                   // every wave holds its fragments: the slot is free
+    if (k + 1 < KT) issue_stage(k + 1);
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+#pragma unroll
+      for (int i = 0; i < C::MV; ++i)
+#pragma unroll
+        for (int j = 0; j < C::MR; ++j) acc[i][j] = MF::mma(fa[s][i], fb[s][j], acc[i][j]);
+  }
+  __syncthreads();
+}
+
 // The same logits as lmhead_tile for 64-deep stages in a two-slot ring, with a fixed
 // instruction schedule that spreads each stage's copies over the MFMAs. A stage has NS MFMA K
 // steps (four K16 steps of 32x32x16, or two K32 steps of 16x16x32) of NF = MV + MR fragments
@@ -591,15 +633,16 @@ __device__ __forceinline__ void lmhead_tile_spread3(
   __syncthreads();
 }
 
-// LOOP selects the K loop: 0 = the burst ring of lmhead_tile; 2 and 3 = the spread loop of
-// that ring depth (lmhead_tile_spread, lmhead_tile_spread3). STREAM_W: the W copies' cache
+// LOOP selects the K loop: 0 = the burst ring of lmhead_tile; 1 = the one-slot ring of
+// lmhead_tile_1slot (three workgroups per CU); 2 and 3 = the spread loop of that ring depth
+// (lmhead_tile_spread, lmhead_tile_spread3). STREAM_W: the W copies' cache
 // policy (see TileIo); it changes no result. MF is the MFMA shape; every tile
 // family of K1 runs the same one, so that all of them sum each logit's products in the same
 // order and give the same logits bit for bit. One launch covers a contiguous range of
 // vocabulary slabs (all of them, or one of two ranges whose tiles differ in height).
 template <int TV, int TR, int WV, int WR, int BK, int NST, int LOOP, bool STREAM_W,
           class MF = Mfma16>
-__global__ __launch_bounds__(WV * WR * kWave, 1)
+__global__ __launch_bounds__(WV * WR * kWave, LOOP == 1 ? 3 : 1)
 void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
                       const int32_t* __restrict__ parent, const int32_t* __restrict__ draft_tok,
                       const int32_t* __restrict__ req_offsets, int B, int N, int H, int V,
@@ -649,7 +692,11 @@ void k_lmhead_partial(const uint16_t* __restrict__ X, const uint16_t* __restrict
 
   // ---- the tile's logits
   typename MF::Acc acc[C::MV][C::MR];
-  if constexpr (LOOP == 2) {
+  if constexpr (LOOP == 1) {
+    static_assert(NST == 1, "one-slot ring");
+    lmhead_tile_1slot<TV, TR, WV, WR, BK, STREAM_W, MF>(X, W, N, H, V, v0, r0, smem, w_packed,
+                                                        acc);
+  } else if constexpr (LOOP == 2) {
     static_assert(BK == 64 && NST == 2, "two-slot spread loop: 64-deep stages");
     lmhead_tile_spread<TV, TR, WV, WR, STREAM_W, MF>(X, W, N, H, V, v0, r0, smem, w_packed,
                                                      acc);

@@ -237,6 +237,33 @@ def test_blocked_tile_order(asv, dev):
         assert np.allclose(got["row_lse"], base["row_lse"], rtol=1e-6, atol=1e-6), rows
 
 
+def test_one_slot_weight_stream(asv, dev):
+    """Up to 64 rows over 513-768 vocabulary slabs (V = 140000: 547 slabs) the 64-row tile runs
+    its one-slot ring at three workgroups per CU (on a 256-CU GPU). Its records, drafted logits
+    and walks match the oracle, and every other tile family bit for bit."""
+    print("[one-slot ring] V=140000 N<=64", flush=True)
+    rng = np.random.default_rng(140000)
+    trees = [_rand_tree(rng, 30, 6, 4), _rand_tree(rng, 21, 5, 3), [-1, 0, 0, 1]]
+    w = custom_workload("one_slot", 256, 140000, trees, 0.2, seed=18, w_std=0.1,
+                        draft_logits=True)
+    W = w.weights()
+    w64 = oracle.widen_weights(W)
+    resolve_with_oracle(w, w64)
+    ref = reference(w, w64)
+    runs = {}
+    for rows, packed in ((0, True), (0, False), (128, True), (256, True)):
+        runs[(rows, packed)] = _run(asv, w, W, dev, k1_tile=rows, packed=packed)
+        compare(w, ref, runs[(rows, packed)], tag=f"one-slot tile={rows} packed={packed}")
+    base = runs[(0, True)]
+    nonroot = w.parent >= 0
+    for key, got in runs.items():
+        for k in ("row_max", "row_argmax", "accept", "accepted_len", "accepted_path",
+                  "bonus_token", "draft_conf"):
+            assert np.array_equal(got[k], base[k], equal_nan=True), (key, k)
+        assert np.array_equal(got["drafted_logit"][nonroot], base["drafted_logit"][nonroot]), key
+        assert np.allclose(got["row_lse"], base["row_lse"], rtol=1e-6, atol=1e-6), key
+
+
 def test_long_hidden_16384(asv, dev):
     """H = 16384 (256 K stages, the hidden size of the largest Llama-3.1 model): every K loop
     (the burst ring of the 64-row tile, the three-slot loop of the 128-row tile and the two-slot
