@@ -379,6 +379,27 @@ typedef struct asv_tuning {
  * returns ASV_EHIP. */
 int asv_verify_tuned(const asv_verify_args *args, const asv_tuning *tuning, void *workspace,
                      uint64_t workspace_bytes, void *stream);
+
+/* One launch of the LM-head kernel of asv_verify (see asv_k1_plan). */
+typedef struct asv_k1_launch {
+  int32_t tile_rows;              /* tree rows per workgroup tile: 64, 128, 192 or 256 */
+  int32_t slab0;                  /* first vocabulary slab (256 ids each) of the launch */
+  int32_t n_slabs;                /* slabs it covers */
+  int32_t row_tiles;              /* tiles along the tree rows: ceil(N / tile_rows) */
+  int32_t k_loop;                 /* 0 burst ring, 1 one-slot ring, 2 two-slot spread loop,
+                                     3 three-slot spread loop */
+  int32_t stream_w;               /* 1: the weight is copied with the non-temporal hint */
+  int32_t blk_slabs, blk_rows;    /* tile order: blocks of blk_slabs slabs x blk_rows row
+                                     tiles, or 0 and 0 for the slab-major order */
+} asv_k1_launch;
+
+/* The LM-head launches asv_verify (asv_verify_tuned with tile_rows forced, 0 = the library's
+ * choice) enqueues for N tree rows and V vocabulary ids on a GPU with `cus` compute units:
+ * fills launches[0 .. *n_launches), at most two, in launch order. Host computation only; no
+ * GPU call. ASV_EINVAL for N < 1, V < 1, cus < 1, a tile_rows asv_tuning rejects or null
+ * pointers. */
+int asv_k1_plan(int32_t N, int32_t V, int32_t cus, int32_t tile_rows, asv_k1_launch *launches,
+                int32_t *n_launches);
 int asv_draft_step_tuned(const asv_draft_args *args, const asv_tuning *tuning, void *workspace,
                          uint64_t workspace_bytes, void *stream);
 

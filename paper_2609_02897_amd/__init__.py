@@ -292,6 +292,18 @@ def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None,
     return out
 
 
+def k1_plan(N: int, V: int, cus: int, tile_rows: int = 0) -> list:
+    """The LM-head launches ``verify`` enqueues for N tree rows and V vocabulary ids on a GPU
+    with ``cus`` compute units (``k1_tile`` = tile_rows; 0 = the library's choice), as dicts
+    in launch order. Host computation only (``asv_k1_plan``)."""
+    lib = load()
+    out = (_abi.AsvK1Launch * 2)()
+    n = ctypes.c_int32(0)
+    _check(lib.asv_k1_plan(N, V, cus, tile_rows, out, ctypes.byref(n)))
+    return [{f: getattr(out[i], f) for f, _ in _abi.AsvK1Launch._fields_}
+            for i in range(n.value)]
+
+
 def _tuning(events=None, tile_rows: int = 0) -> AsvTuning:
     tu = AsvTuning()
     if events is not None:

@@ -61,6 +61,13 @@ class AsvTuning(ctypes.Structure):
     _fields_ = [("begin_event", _P), ("end_event", _P), ("tile_rows", ctypes.c_int32)]
 
 
+class AsvK1Launch(ctypes.Structure):
+    _fields_ = [("tile_rows", ctypes.c_int32), ("slab0", ctypes.c_int32),
+                ("n_slabs", ctypes.c_int32), ("row_tiles", ctypes.c_int32),
+                ("k_loop", ctypes.c_int32), ("stream_w", ctypes.c_int32),
+                ("blk_slabs", ctypes.c_int32), ("blk_rows", ctypes.c_int32)]
+
+
 class AsvDraftTree(ctypes.Structure):
     _fields_ = [("nsteps", ctypes.c_int32), ("topk", ctypes.c_int32), ("ndt", ctypes.c_int32),
                 ("steps", ctypes.c_int32), ("n_pool", ctypes.c_int32),
@@ -138,6 +145,9 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.asv_verify_tuned.restype = ctypes.c_int
     lib.asv_verify_tuned.argtypes = [ctypes.POINTER(AsvVerifyArgs), ctypes.POINTER(AsvTuning),
                                      _P, ctypes.c_uint64, _P]
+    lib.asv_k1_plan.restype = ctypes.c_int
+    lib.asv_k1_plan.argtypes = [ctypes.c_int32] * 4 + [ctypes.POINTER(AsvK1Launch),
+                                                       ctypes.POINTER(ctypes.c_int32)]
     lib.asv_draft_step_tuned.restype = ctypes.c_int
     lib.asv_draft_step_tuned.argtypes = [ctypes.POINTER(AsvDraftArgs),
                                          ctypes.POINTER(AsvTuning), _P, ctypes.c_uint64, _P]

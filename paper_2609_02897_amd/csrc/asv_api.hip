@@ -142,6 +142,46 @@ void tile_blocking(int RT, int cus, int* blk_slabs, int* blk_rows) {
 // 250 tiles: +7%; V = 200000, 782 tiles: +6%) or level (V = 128256, 501 tiles).
 bool one_slot_64(int tiles, int cus) { return tiles > 2 * cus && tiles <= 3 * cus; }
 
+// Launches of at most this many row tiles copy W with the non-temporal hint (the one or two
+// tiles of a slab read it about once); more row tiles share each W slab through an XCD's L2
+// and keep the default policy. Against the earlier rule (the hint for tiles of up to 128 rows)
+// in same-box A/Bs: 260, 300, 378 and 450 rows 3% faster, 150 rows 1.4%, 500 rows 1%; 128,
+// 200 and 600 to 3048 rows level.
+constexpr int kStreamWMaxRowTiles = 2;
+
+int tile_rows_of(Tile t) {
+  switch (t) {
+    case Tile::kRows64: return 64;
+    case Tile::kRows128: return 128;
+    case Tile::kRows192: return 192;
+    default: return 256;
+  }
+}
+
+// The K1 launches of a verification step over N rows and S slabs on `cus` CUs: the plan's one
+// or two launches, each with its K loop, W copy policy and tile order. Returns the count.
+int k1_launches(int N, int S, int cus, const K1Plan& plan, asv_k1_launch out[2]) {
+  int n = 0;
+  auto add = [&](Tile t, int slab0, int n_slabs) {
+    asv_k1_launch& k = out[n++];
+    k.tile_rows = tile_rows_of(t);
+    k.slab0 = slab0;
+    k.n_slabs = n_slabs;
+    k.row_tiles = (N + k.tile_rows - 1) / k.tile_rows;
+    const int tiles = n_slabs * k.row_tiles;
+    switch (t) {
+      case Tile::kRows64: k.k_loop = one_slot_64(tiles, cus) ? 1 : 0; break;
+      case Tile::kRows128: k.k_loop = 3; break;
+      default: k.k_loop = 2; break;
+    }
+    k.stream_w = k.row_tiles <= kStreamWMaxRowTiles ? 1 : 0;
+    tile_blocking(k.row_tiles, cus, &k.blk_slabs, &k.blk_rows);
+  };
+  add(plan.a, 0, plan.n1);
+  if (plan.n1 < S) add(plan.b, plan.n1, S - plan.n1);
+  return n;
+}
+
 // The tile asv_verify_args.k1_tile_rows asks for; false for a value that names no tile.
 bool forced_tile(int rows, Tile* t) {
   switch (rows) {
@@ -209,32 +249,22 @@ void launch_timed(F kernel, int grid, int threads, hipStream_t s, hipEvent_t sta
     kernel<<<grid, threads, 0, s>>>(args...);
 }
 
-// Launches of at most this many row tiles copy W with the non-temporal hint (the one or two
-// tiles of a slab read it about once); more row tiles share each W slab through an XCD's L2
-// and keep the default policy. Against the earlier rule (the hint for tiles of up to 128 rows)
-// in same-box A/Bs: 260, 300, 378 and 450 rows 3% faster, 150 rows 1.4%, 500 rows 1%; 128,
-// 200 and 600 to 3048 rows level.
-constexpr int kStreamWMaxRowTiles = 2;
-
-template <int TV, int TR, int WV, int WR, int BK, int NST, int LOOP = 0>
+template <int TV, int TR, int WV, int WR, int BK, int NST, int LOOP>
 void launch_lmhead(const asv_verify_args* a, const Layout& L, char* ws, hipStream_t s,
-                   int slab0, int n_slabs, hipEvent_t start, hipEvent_t stop) {
+                   const asv_k1_launch& k, hipEvent_t start, hipEvent_t stop) {
   static_assert(TV == kSlab, "tiles span exactly one record slab");
   static_assert(TV == kPackRowsTarget && BK == kPackDepth, "a stage is one packed tile");
-  const int RT = (a->N + TR - 1) / TR;
-  const int grid = n_slabs * RT;
-  int blk_slabs = 0, blk_rows = 0;
-  tile_blocking(RT, cu_count(), &blk_slabs, &blk_rows);
+  const int grid = k.n_slabs * k.row_tiles;
   auto go = [&](auto kernel) {
     launch_timed(kernel, grid, WV * WR * kWave, s, start, stop, a->hidden, a->w_lm, a->parent,
-                 a->draft_tok, a->req_offsets, a->B, a->N, a->H, a->V, L.S, slab0, RT,
-                 reinterpret_cast<float*>(ws + L.off_rec_m),
+                 a->draft_tok, a->req_offsets, a->B, a->N, a->H, a->V, L.S, k.slab0,
+                 k.row_tiles, reinterpret_cast<float*>(ws + L.off_rec_m),
                  reinterpret_cast<float*>(ws + L.off_rec_s),
                  reinterpret_cast<int32_t*>(ws + L.off_rec_a), a->drafted_logit,
                  reinterpret_cast<int32_t*>(ws + L.off_cnt), a->B + 1,
-                 a->w_lm_layout == ASV_W_PACKED ? 1 : 0, blk_slabs, blk_rows);
+                 a->w_lm_layout == ASV_W_PACKED ? 1 : 0, k.blk_slabs, k.blk_rows);
   };
-  if (RT <= kStreamWMaxRowTiles)
+  if (k.stream_w)
     go(k_lmhead_partial<TV, TR, WV, WR, BK, NST, LOOP, true>);
   else
     go(k_lmhead_partial<TV, TR, WV, WR, BK, NST, LOOP, false>);
@@ -472,41 +502,35 @@ extern "C" int asv_verify_tuned(const asv_verify_args* a, const asv_tuning* tuni
 
   const K1Plan plan = tu.tile_rows != 0 ? K1Plan{forced, forced, L.S}
                                          : plan_k1(a->N, L.S, cu_count());
+  asv_k1_launch k1[2];
+  const int n_k1 = k1_launches(a->N, L.S, cu_count(), plan, k1);
   // timing events (measurement only): the start of the first launch, the end of the last
   const hipEvent_t ev_begin = reinterpret_cast<hipEvent_t>(tu.begin_event);
   const hipEvent_t ev_end = reinterpret_cast<hipEvent_t>(tu.end_event);
-  auto launch = [&](Tile tile, int slab0, int n_slabs, hipEvent_t start, hipEvent_t stop) {
-    switch (tile) {
-      // <vocab rows, tree rows, waves along vocab, waves along rows, K per stage, ring depth,
-      // K loop>, each the fastest of a sweep on MI355X for its row range. The weight-streaming
-      // 64-row tile keeps two workgroups per CU (80 KB of LDS each) with the burst ring; a
-      // 3-deep ring with one workgroup per CU was 0.7% slower in an interleaved comparison
-      // over ten placements of W. The 128-, 192- and 256-row tiles run the spread K loops
-      // (copies spaced between the MFMAs), in interleaved comparisons 28% faster than the
-      // burst ring at 378 rows and 20% at 2048 and 3048 rows.
-      case Tile::kRows64:
-        // the one-slot ring (three workgroups per CU) when the two-slot ring (two per CU)
-        // would leave a second, partial round of workgroups and three per CU take them all at
-        // once (at 256 CUs and up to 64 rows: 513 to 768 slabs, e.g. V = 151936)
-        if (one_slot_64(n_slabs * ((a->N + 63) / 64), cu_count()))
-          launch_lmhead<256, 64, 4, 1, 64, 1, 1>(a, L, ws, s, slab0, n_slabs, start, stop);
+  for (int q = 0; q < n_k1; ++q) {
+    const asv_k1_launch& k = k1[q];
+    const hipEvent_t start = q == 0 ? ev_begin : nullptr;
+    const hipEvent_t stop = q == n_k1 - 1 ? ev_end : nullptr;
+    // <vocab rows, tree rows, waves along vocab, waves along rows, K per stage, ring depth,
+    // K loop>, each the fastest of a sweep on MI355X for its row range. The weight-streaming
+    // 64-row tile keeps two workgroups per CU (80 KB of LDS each) with the burst ring, or
+    // three (40 KB each) with the one-slot ring when that takes every tile at once; a 3-deep
+    // ring with one workgroup per CU was 0.7% slower in an interleaved comparison over ten
+    // placements of W. The 128-, 192- and 256-row tiles run the spread K loops (copies spaced
+    // between the MFMAs), in interleaved comparisons 28% faster than the burst ring at 378
+    // rows and 20% at 2048 and 3048 rows.
+    switch (k.tile_rows) {
+      case 64:
+        if (k.k_loop == 1)
+          launch_lmhead<256, 64, 4, 1, 64, 1, 1>(a, L, ws, s, k, start, stop);
         else
-          launch_lmhead<256, 64, 4, 1, 64, 2>(a, L, ws, s, slab0, n_slabs, start, stop);
+          launch_lmhead<256, 64, 4, 1, 64, 2, 0>(a, L, ws, s, k, start, stop);
         break;
-      case Tile::kRows128:
-        launch_lmhead<256, 128, 2, 2, 64, 3, 3>(a, L, ws, s, slab0, n_slabs, start, stop);
-        break;
-      case Tile::kRows192:
-        launch_lmhead<256, 192, 2, 2, 64, 2, 2>(a, L, ws, s, slab0, n_slabs, start, stop);
-        break;
-      case Tile::kRows256:
-        launch_lmhead<256, 256, 2, 2, 64, 2, 2>(a, L, ws, s, slab0, n_slabs, start, stop);
-        break;
+      case 128: launch_lmhead<256, 128, 2, 2, 64, 3, 3>(a, L, ws, s, k, start, stop); break;
+      case 192: launch_lmhead<256, 192, 2, 2, 64, 2, 2>(a, L, ws, s, k, start, stop); break;
+      default: launch_lmhead<256, 256, 2, 2, 64, 2, 2>(a, L, ws, s, k, start, stop); break;
     }
-  };
-  const bool two = plan.n1 < L.S;
-  launch(plan.a, 0, plan.n1, ev_begin, two ? nullptr : ev_end);
-  if (two) launch(plan.b, plan.n1, L.S - plan.n1, nullptr, ev_end);
+  }
   if (int rc = launch_status("k_lmhead_partial")) return rc;
 
   const AcceptArgs acc = accept_args(a, L, ws, conf);
@@ -526,6 +550,17 @@ extern "C" int asv_verify_tuned(const asv_verify_args* a, const asv_tuning* tuni
   if (int rc = launch_status("k_slab_merge")) return rc;
   k_tree_accept<<<a->B, kWave, 0, s>>>(cnt + a->B, acc);
   return launch_status("k_tree_accept");
+}
+
+extern "C" int asv_k1_plan(int32_t N, int32_t V, int32_t cus, int32_t tile_rows,
+                           asv_k1_launch* launches, int32_t* n_launches) {
+  if (N < 1 || V < 1 || cus < 1 || !launches || !n_launches) return ASV_EINVAL;
+  Tile forced = Tile::kRows64;
+  if (tile_rows != 0 && !forced_tile(tile_rows, &forced)) return ASV_EINVAL;
+  const int S = (V + kSlab - 1) / kSlab;
+  const K1Plan plan = tile_rows != 0 ? K1Plan{forced, forced, S} : plan_k1(N, S, cus);
+  *n_launches = k1_launches(N, S, cus, plan, launches);
+  return ASV_OK;
 }
 
 extern "C" int asv_verify(const asv_verify_args* a, void* workspace, uint64_t workspace_bytes,
