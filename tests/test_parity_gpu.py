@@ -237,24 +237,29 @@ def test_blocked_tile_order(asv, dev):
         assert np.allclose(got["row_lse"], base["row_lse"], rtol=1e-6, atol=1e-6), rows
 
 
-def test_one_slot_weight_stream(asv, dev):
-    """Up to 64 rows over 513-768 vocabulary slabs (V = 140000: 547 slabs) the 64-row tile runs
-    its one-slot ring at three workgroups per CU (on a 256-CU GPU). Its records, drafted logits
-    and walks match the oracle, and every other tile family bit for bit."""
-    print("[one-slot ring] V=140000 N<=64", flush=True)
-    rng = np.random.default_rng(140000)
-    trees = [_rand_tree(rng, 30, 6, 4), _rand_tree(rng, 21, 5, 3), [-1, 0, 0, 1]]
-    w = custom_workload("one_slot", 256, 140000, trees, 0.2, seed=18, w_std=0.1,
+@pytest.mark.parametrize("V,sizes,tile", [(140000, (30, 21, 4), 0),
+                                          (80000, (40, 33, 27), 64)])
+def test_one_slot_weight_stream(asv, dev, V, sizes, tile):
+    """When a launch's 64-row tiles fit three per CU but not two (on a 256-CU GPU: 513-768
+    tiles) the 64-row tile runs its one-slot ring: V = 140000 (547 slabs, one row tile) with
+    the library's pick, and V = 80000 (313 slabs, two row tiles at 100 rows) with the 64-row
+    tile forced. The records, drafted logits and walks match the oracle, and the other tile
+    families bit for bit."""
+    assert asv.k1_plan(sum(sizes), V, 256, tile)[0]["k_loop"] == 1
+    print(f"[one-slot ring] V={V} N={sum(sizes)} tile={tile}", flush=True)
+    rng = np.random.default_rng(V)
+    trees = [_rand_tree(rng, n, 6, 4) for n in sizes]
+    w = custom_workload(f"one_slot{V}", 256, V, trees, 0.2, seed=18, w_std=0.1,
                         draft_logits=True)
     W = w.weights()
     w64 = oracle.widen_weights(W)
     resolve_with_oracle(w, w64)
     ref = reference(w, w64)
     runs = {}
-    for rows, packed in ((0, True), (0, False), (128, True), (256, True)):
+    for rows, packed in ((tile, True), (tile, False), (128, True), (256, True)):
         runs[(rows, packed)] = _run(asv, w, W, dev, k1_tile=rows, packed=packed)
         compare(w, ref, runs[(rows, packed)], tag=f"one-slot tile={rows} packed={packed}")
-    base = runs[(0, True)]
+    base = runs[(tile, True)]
     nonroot = w.parent >= 0
     for key, got in runs.items():
         for k in ("row_max", "row_argmax", "accept", "accepted_len", "accepted_path",
