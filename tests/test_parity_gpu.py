@@ -219,6 +219,8 @@ def test_blocked_tile_order(asv, dev):
     families agree bit for bit as in test_every_tile_same_results."""
     print("[blocked order] case=blocked_tile_order", flush=True)
     w = _case("blocked_tile_order")
+    for rows in (256, 192, 128, 64):     # on a 256-CU GPU every family takes the blocked order
+        assert asv.k1_plan(w.N, w.V, 256, rows)[0]["blk_rows"] == 4, rows
     W = w.weights()
     w64 = oracle.widen_weights(W)
     resolve_with_oracle(w, w64)
