@@ -106,7 +106,9 @@ typedef struct asv_params {
  * draft_tok[c] is judged by the target distribution predicted at its parent's row. */
 typedef struct asv_verify_args {
   int32_t B, N, H, V;             /* host ints: B >= 0, N >= B (N == 0 iff B == 0),
-                                     H > 0 with H % 64 == 0, V > 0 */
+                                     H > 0 with H % 64 == 0 and H <= 2^20, V > 0,
+                                     N, V < 2^30 and ceil(V / 256) * ceil(N / 64) < 2^31
+                                     (the LM-head kernel's largest workgroup count) */
   const uint16_t *hidden;         /* [N][H] bf16 final hidden states, 16-byte aligned */
   const uint16_t *w_lm;           /* [V][H] bf16 LM-head weight, or its packed copy (see
                                      w_lm_layout), 16-byte aligned */
@@ -396,8 +398,8 @@ typedef struct asv_k1_launch {
 /* The LM-head launches asv_verify (asv_verify_tuned with tile_rows forced, 0 = the library's
  * choice) enqueues for N tree rows and V vocabulary ids on a GPU with `cus` compute units:
  * fills launches[0 .. *n_launches), at most two, in launch order. Host computation only; no
- * GPU call. ASV_EINVAL for N < 1, V < 1, cus < 1, a tile_rows asv_tuning rejects or null
- * pointers. */
+ * GPU call. ASV_EINVAL for N < 1, V < 1, N and V beyond asv_verify_args' bound, cus < 1, a
+ * tile_rows asv_tuning rejects or null pointers. */
 int asv_k1_plan(int32_t N, int32_t V, int32_t cus, int32_t tile_rows, asv_k1_launch *launches,
                 int32_t *n_launches);
 int asv_draft_step_tuned(const asv_draft_args *args, const asv_tuning *tuning, void *workspace,

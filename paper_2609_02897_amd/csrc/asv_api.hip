@@ -218,11 +218,20 @@ Layout layout(int B, int N, int V) {
   return L;
 }
 
+// Row and vocabulary indices (rounded up to whole tiles) and the LM-head kernel's workgroup
+// count stay ints: N, V < 2^30, and for the 64-row tile, which has the most workgroups,
+// ceil(V / 256) * ceil(N / 64) < 2^31.
+bool grid_ok(int N, int V) {
+  if (N >= (1 << 30) || V >= (1 << 30)) return false;
+  const int64_t S = ((int64_t)V + kSlab - 1) / kSlab, RT = ((int64_t)N + 63) / 64;
+  return S * RT < ((int64_t)1 << 31);
+}
+
 bool sizes_ok(int B, int N, int H, int V) {
   if (B < 0 || N < 0 || H <= 0 || V <= 0) return false;
   if ((B == 0) != (N == 0) || N < B) return false;
   if (H % kKAlign != 0 || H > (1 << 20)) return false;
-  return true;
+  return grid_ok(N, V);
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -554,7 +563,8 @@ extern "C" int asv_verify_tuned(const asv_verify_args* a, const asv_tuning* tuni
 
 extern "C" int asv_k1_plan(int32_t N, int32_t V, int32_t cus, int32_t tile_rows,
                            asv_k1_launch* launches, int32_t* n_launches) {
-  if (N < 1 || V < 1 || cus < 1 || !launches || !n_launches) return ASV_EINVAL;
+  if (N < 1 || V < 1 || cus < 1 || !grid_ok(N, V) || !launches || !n_launches)
+    return ASV_EINVAL;
   Tile forced = Tile::kRows64;
   if (tile_rows != 0 && !forced_tile(tile_rows, &forced)) return ASV_EINVAL;
   const int S = (V + kSlab - 1) / kSlab;

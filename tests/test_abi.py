@@ -81,8 +81,13 @@ def test_workspace_bytes(lib):
     assert out.value % 256 == 0
     assert lib.asv_workspace_bytes(0, 0, 64, 10, ctypes.byref(out)) == 0
     for bad in [(1, 0, 64, 10), (2, 1, 64, 10), (1, 4, 100, 10), (1, 4, 64, 0),
-                (-1, 4, 64, 10)]:
+                (-1, 4, 64, 10), (1, 4, (1 << 20) + 64, 10),
+                (1, 1 << 30, 64, 10), (1, 4, 64, 1 << 30),      # indices past 2^30
+                (1, 1 << 24, 64, 1 << 23)]:                        # 2^33 LM-head workgroups
         assert lib.asv_workspace_bytes(*bad, ctypes.byref(out)) == asv.ASV_EINVAL, bad
+    # the largest accepted workgroup count: ceil(V / 256) * ceil(N / 64) just below 2^31
+    assert lib.asv_workspace_bytes(1, 64 * 1023, 64, 256 * (((1 << 31) - 1) // 1023),
+                                   ctypes.byref(out)) == 0
     assert lib.asv_workspace_bytes(1, 4, 64, 10, None) == asv.ASV_EINVAL
 
 
