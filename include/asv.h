@@ -209,7 +209,9 @@ typedef struct asv_draft_tree {
  * only slot 0, the root, is read by the tree update). Rows of unused slots are computed like any
  * other row and then ignored, so they may hold anything. */
 typedef struct asv_draft_args {
-  int32_t B, H, V;                /* host ints: B >= 0, H > 0 with H % 64 == 0, V >= 4 */
+  int32_t B, H, V;                /* host ints: B >= 0, H > 0 with H % 64 == 0,
+                                     4 <= V < 2^30, 8 B H < 2^31, and the draft LM head's
+                                     workgroup count (slabs x row tiles) below 2^31 */
   int32_t step;                   /* host int: 0 (re)starts every tree from its shape */
   const uint16_t *hidden;         /* [4B][H] bf16 draft hidden states, 16-byte aligned */
   const uint16_t *w_draft;        /* [V][H] bf16 draft LM-head weight, 16-byte aligned */

@@ -370,11 +370,16 @@ DraftLayout draft_layout(int B, int V) {
 }
 
 bool draft_sizes_ok(int B, int H, int V) {
-  if (B < 0 || H <= 0 || V < kTopK) return false;
+  if (B < 0 || H <= 0 || V < kTopK || V >= (1 << 30)) return false;
   if (H % kKAlign != 0 || H > (1 << 20)) return false;
   // 32-bit offsets inside a tile's buffer resource: all 4B rows of X and one slab of W
   if ((int64_t)B * kTopK * H * 2 >= (int64_t)1 << 31) return false;
-  return true;
+  // the draft LM head's workgroup count stays an int
+  const int R = B * kTopK;
+  const DraftTile t = pick_draft_tile(R);
+  const int tr = t == DraftTile::kRows32 ? 32 : t == DraftTile::kRows64 ? 64 : 128;
+  const int64_t S = ((int64_t)V + draft_slab(t) - 1) / draft_slab(t);
+  return S * (((int64_t)R + tr - 1) / tr) < ((int64_t)1 << 31);
 }
 
 template <int TV, int TR, int WV, int WR, int BK, int NST>

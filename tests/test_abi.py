@@ -262,8 +262,10 @@ def test_draft_and_tree_entry_points_reject_on_host(lib):
     assert lib.asv_draft_workspace_bytes(2, 4096, 32000, ctypes.byref(out)) == 0
     S = (32000 + 63) // 64                         # 8 draft rows use 64-wide vocabulary slabs
     assert out.value >= 8 * S * (4 + 4 + 1) * 4 and out.value % 256 == 0
-    for bad in [(-1, 64, 10), (1, 100, 10), (1, 64, 3), (1, 0, 10)]:
+    for bad in [(-1, 64, 10), (1, 100, 10), (1, 64, 3), (1, 0, 10), (1, 64, 1 << 30),
+                (1 << 20, 64, 1 << 29)]:                          # 2^32 draft workgroups
         assert lib.asv_draft_workspace_bytes(*bad, ctypes.byref(out)) == asv.ASV_EINVAL, bad
+    assert lib.asv_draft_workspace_bytes(1, 64, (1 << 30) - 1, ctypes.byref(out)) == 0
     a = _abi.AsvDraftArgs()
     a.B, a.H, a.V, a.step = 0, 64, 10, 0
     assert lib.asv_draft_step(ctypes.byref(a), None, 0, None) == asv.ASV_OK       # empty batch
