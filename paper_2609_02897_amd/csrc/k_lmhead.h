@@ -48,6 +48,9 @@ struct Mfma32 {   // v_mfma_f32_32x32x16_bf16
   static __device__ __forceinline__ Acc mma(bf16x8 a, bf16x8 b, Acc c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
+  static __device__ __forceinline__ Acc mma_chained(bf16x8 a, bf16x8 b, Acc c) {
+    return mma(a, b, c);
+  }
   static __device__ __forceinline__ int row_of(int lane, int e) {
     return 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
   }
@@ -65,6 +68,12 @@ struct Mfma16 {   // v_mfma_f32_16x16x32_bf16
     Acc d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
     asm volatile("" : "+a"(d));
     return d;
+  }
+  // Without the pin, for a result whose only use is a later MFMA of the same loop pass. The
+  // two-slot spread loop pins only each pass's last K step: pinning every step there made the
+  // allocator rotate 12 accumulator registers of the 192-row tile through copies on every pass.
+  static __device__ __forceinline__ Acc mma_chained(bf16x8 a, bf16x8 b, Acc c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
   }
   static __device__ __forceinline__ int row_of(int lane, int e) { return 4 * (lane >> 4) + e; }
   static __device__ __forceinline__ int reg_of(int m) { return m & 3; }
@@ -232,8 +241,14 @@ struct TileIo {
   using C = LmheadCfg<TV, TR, WV, WR, BK, NST, MF>;
   static constexpr int CPR = C::CPR;
   static constexpr bool kStreamW = STREAM_W;
+  static constexpr int NS = C::NS;
   const uint4* lds;
   int lane, wave, wv, wr, lds0, frag_row, frag_grp;
+  // 16-byte units, within a ring slot, of this lane's fragment of W block 0 / X block 0 at
+  // K step s. Block i sits kBlock i rows further on, at the same swizzled chunk (the swizzle
+  // repeats every 16 rows), so a fragment address is one of these plus a constant, which the
+  // LDS read takes as its immediate offset.
+  int w_frag0[NS], x_frag0[NS];
   unsigned w_kstep;             // bytes between the W data of consecutive K stages
   __amdgpu_buffer_rsrc_t w_rsrc, x_rsrc;
   int w_voff[C::DW], x_voff[C::DX];
@@ -247,6 +262,14 @@ struct TileIo {
     wr = wave / WV;
     frag_row = lane % MF::kBlock;
     frag_grp = lane / MF::kBlock;
+    static_assert(MF::kBlock % 16 == 0 && C::kWaveV % 16 == 0 && C::kWaveR % 16 == 0,
+                  "fragment blocks start at whole periods of the swizzle");
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      w_frag0[s] = swz<CPR>(wv * C::kWaveV + frag_row, (MF::kK / 8) * s + frag_grp);
+      x_frag0[s] =
+          C::kStageW / 16 + swz<CPR>(wr * C::kWaveR + frag_row, (MF::kK / 8) * s + frag_grp);
+    }
     lds0 = __builtin_amdgcn_readfirstlane((int)(size_t)smem);
     const int v_end = min(v0 + TV, V);
     const int r_last = min(r0 + TR, N) - 1;
@@ -294,16 +317,12 @@ struct TileIo {
   // the fragment of W block i (of this wave's vocabulary rows), or of X block j (of its tree
   // rows), for MFMA K step s of ring slot `slot`
   __device__ __forceinline__ bf16x8 w_frag(int slot, int s, int i) const {
-    const uint4* w = lds + slot * (C::kStage / 16);
-    return __builtin_bit_cast(
-        bf16x8, w[swz<CPR>(wv * C::kWaveV + MF::kBlock * i + frag_row,
-                           (MF::kK / 8) * s + frag_grp)]);
+    const uint4* w = lds + slot * (C::kStage / 16) + w_frag0[s];
+    return __builtin_bit_cast(bf16x8, w[MF::kBlock * CPR * i]);
   }
   __device__ __forceinline__ bf16x8 x_frag(int slot, int s, int j) const {
-    const uint4* x = lds + slot * (C::kStage / 16) + C::kStageW / 16;
-    return __builtin_bit_cast(
-        bf16x8, x[swz<CPR>(wr * C::kWaveR + MF::kBlock * j + frag_row,
-                           (MF::kK / 8) * s + frag_grp)]);
+    const uint4* x = lds + slot * (C::kStage / 16) + x_frag0[s];
+    return __builtin_bit_cast(bf16x8, x[MF::kBlock * CPR * j]);
   }
 };
 
@@ -524,7 +543,10 @@ __device__ __forceinline__ void lmhead_tile_spread(
     static_for<NM>([&](auto mc) {
       constexpr int m = decltype(mc)::value;
       constexpr int s = m / (MV * MR), q = m % (MV * MR), i = q / MR, j = q % MR;
-      acc[i][j] = MF::mma(fa[s][i], fb[s][j], acc[i][j]);
+      if constexpr (s == NS - 1)
+        acc[i][j] = MF::mma(fa[s][i], fb[s][j], acc[i][j]);
+      else
+        acc[i][j] = MF::mma_chained(fa[s][i], fb[s][j], acc[i][j]);
       if constexpr (m < NR && m % RS == 0) read_frag(slot, HS + m / RS / NF, m / RS % NF);
       if constexpr (m == Q1 - 1) wait_lds_barrier();
       static_for<kCopies>([&](auto cc) {
