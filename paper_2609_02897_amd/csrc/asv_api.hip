@@ -98,13 +98,16 @@ K1Plan plan_k1(int N, int S, int cus) {
     }
   }
   // two families: family a fills k whole rounds on its slabs, family b takes the rest; taken
-  // only when strictly better than every single family
+  // only when strictly better than every single family. The search stops at kMaxSplitRounds
+  // rounds of family a (a launch that long gains nothing from a finer split, and the bound
+  // keeps the host loop short for any size the checks accept).
+  constexpr int64_t kMaxSplitRounds = 4096;
   for (const Family& fa : families) {
     const int64_t ra = (N + fa.rows - 1) / fa.rows;
     for (const Family& fb : families) {
       if (fb.rows == fa.rows) continue;
       const int64_t rb = (N + fb.rows - 1) / fb.rows;
-      for (int64_t k = 1; k * cus < (int64_t)S * ra; ++k) {
+      for (int64_t k = 1; k <= kMaxSplitRounds && k * cus < (int64_t)S * ra; ++k) {
         const int64_t n1 = k * cus / ra;
         if (n1 <= 0 || n1 >= S) continue;
         const int64_t est = rounds(n1 * ra) * fa.cost + rounds((S - n1) * rb) * fb.cost;

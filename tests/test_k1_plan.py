@@ -87,6 +87,15 @@ def test_plan_invariants():
             assert (k["blk_slabs"], k["blk_rows"]) == ((max(1, c // 4), 4) if blocked else (0, 0))
 
 
+def test_plan_of_the_largest_sizes_is_quick():
+    """The two-family search is bounded: one CU and the largest accepted grid plan at once."""
+    import time
+    t0 = time.perf_counter()
+    got = asv.k1_plan((1 << 15) - 64, (1 << 30) - 1, 1)   # 2^22 slabs x 511 64-row tiles
+    assert time.perf_counter() - t0 < 2.0
+    assert sum(k["n_slabs"] for k in got) == ((1 << 30) - 1 + 255) // 256
+
+
 @pytest.mark.parametrize("args", [(0, 1000, 256, 0), (10, 0, 256, 0), (10, 1000, 0, 0),
                                   (10, 1000, 256, 100)])
 def test_plan_rejects(args):
