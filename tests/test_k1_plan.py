@@ -90,9 +90,10 @@ def test_plan_invariants():
 def test_plan_of_the_largest_sizes_is_quick():
     """The two-family search is bounded: one CU and the largest accepted grid plan at once."""
     import time
+    asv.k1_plan(100, 1000, 256)               # loads the library (runtime start-up) untimed
     t0 = time.perf_counter()
     got = asv.k1_plan((1 << 15) - 64, (1 << 30) - 1, 1)   # 2^22 slabs x 511 64-row tiles
-    assert time.perf_counter() - t0 < 2.0
+    assert time.perf_counter() - t0 < 0.5
     assert sum(k["n_slabs"] for k in got) == ((1 << 30) - 1 + 255) // 256
 
 
