@@ -23,7 +23,7 @@ EXPORTS = ("asv_version", "asv_status_string", "asv_last_error", "asv_workspace_
            "asv_draft_step", "asv_draft_prune", "asv_tree_meta", "asv_commit",
            "asv_packed_lm_head_bytes", "asv_pack_lm_head", "asv_packed_draft_head_bytes",
            "asv_pack_draft_head", "asv_verify_tuned", "asv_draft_step_tuned",
-           "asv_verify_noalloc")
+           "asv_verify_noalloc", "asv_k1_plan")
 
 
 class AsvReqState(ctypes.Structure):

@@ -23,7 +23,7 @@ def lib():
 def _declared_functions():
     src = open(os.path.join(ROOT, "include", "asv.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(asv_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(asv_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_header_matches_binding():
@@ -230,7 +230,7 @@ def test_microbench_library_exports_and_checks():
     mb = ctypes.CDLL(_build.MICROBENCH_OUT)
     src = open(os.path.join(ROOT, "include", "asv_microbench.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    names = sorted(set(re.findall(r"\b(asvb_[a-z_]+)\s*\(", src)))
+    names = sorted(set(re.findall(r"\b(asvb_[a-z0-9_]+)\s*\(", src)))
     assert names == ["asvb_lds_read", "asvb_mfma_loop", "asvb_stream_read",
                      "asvb_stream_read_nt"]
     for n in names:
