@@ -16,7 +16,8 @@ def pytest_configure(config):
 
 def pytest_sessionfinish(session, exitstatus):
     """Write every banded decision the parity tests met (rows, nodes, requests, tree shapes,
-    histories that followed the GPU), by test and id, to gpurun_out/parity_bands.json."""
+    histories that followed the GPU), by test and id, to parity_bands.json in the run's output
+    folder at the repository root."""
     harness = sys.modules.get("harness")
     if harness is None or not harness.BAND_LOG:
         return

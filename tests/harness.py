@@ -4,8 +4,8 @@ Bands. The parity bar puts a 1e-3 band around every floating-point decision the 
 argmax (its top-2 gap), a node's margin (|g - M - T ln kappa|) and the walk's choice between
 siblings with distinct tokens. Where the oracle's float64 values put a decision inside a band,
 the GPU's float32 decision may legitimately differ. Every banded row, node and request is
-recorded by id in BAND_LOG (tests/conftest.py writes it to gpurun_out/parity_bands.json at the
-end of the session) together with what the GPU did there, and callers cap how many requests
+recorded by id in BAND_LOG (tests/conftest.py writes it to parity_bands.json at the end of the
+session) together with what the GPU did there, and callers cap how many requests
 of a full-size workload may be banded.
 """
 
