@@ -185,7 +185,7 @@ struct LmheadCfg {
 // Map a launch-order block id to a tile so that each XCD (blocks are dealt to the 8 XCDs
 // round-robin) works through a contiguous range of tiles: the row tiles of one vocabulary
 // slab then run on one XCD and share that slab through its L2.
-__device__ __forceinline__ int xcd_tile(int bid, int G) {
+__host__ __device__ __forceinline__ int xcd_tile(int bid, int G) {
   const int q = G >> 3, rem = G & 7, xcd = bid & 7, loc = bid >> 3;
   return xcd * q + min(xcd, rem) + loc;
 }
@@ -198,7 +198,7 @@ __device__ __forceinline__ int xcd_tile(int bid, int G) {
 // blk_slabs W slabs and blk_rows X row tiles through that XCD's L2 instead of about
 // blk_slabs * blk_rows / RT slabs and all RT row tiles. Every (slab, row tile) pair is taken
 // once; the order changes no result.
-__device__ __forceinline__ void tile_coords(int t, int n_slabs, int RT, int blk_slabs,
+__host__ __device__ __forceinline__ void tile_coords(int t, int n_slabs, int RT, int blk_slabs,
                                             int blk_rows, int& slab, int& rt) {
   if (blk_rows <= 0 || blk_rows >= RT) {
     slab = t / RT;
