@@ -45,16 +45,16 @@ __device__ __forceinline__ void pair_order(float& va, int& ia, float& vb, int& i
 // the logit's bits mapped to an order-preserving unsigned integer, the low word the complement
 // of the id (a lower id gives a larger key). Logits are never a non-number here; -0 is folded
 // into +0 first, so that equal logits compare equal as floats do. Key 0 lies below every pair.
-__device__ __forceinline__ uint64_t pair_key(float v, int id) {
-  const uint32_t u = __float_as_uint(v + 0.f);
+__host__ __device__ __forceinline__ uint64_t pair_key(float v, int id) {
+  const uint32_t u = __builtin_bit_cast(uint32_t, v + 0.f);
   const uint32_t o = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
   return ((uint64_t)o << 32) | (uint32_t)~id;
 }
-__device__ __forceinline__ float key_value(uint64_t k) {
+__host__ __device__ __forceinline__ float key_value(uint64_t k) {
   const uint32_t o = (uint32_t)(k >> 32);
-  return __uint_as_float((o & 0x80000000u) ? (o & 0x7fffffffu) : ~o);
+  return __builtin_bit_cast(float, (o & 0x80000000u) ? (o & 0x7fffffffu) : ~o);
 }
-__device__ __forceinline__ int key_id(uint64_t k) { return (int)~(uint32_t)k; }
+__host__ __device__ __forceinline__ int key_id(uint64_t k) { return (int)~(uint32_t)k; }
 
 // Four pairs as keys in descending order, the best logit m (the value of k[0]) and the sum of
 // exp(z - m) over the set they were taken from (an empty set: keys 0, m = -inf, s = 0).
