@@ -96,12 +96,12 @@ constexpr int kRsrcWord3 = 0x00020000;
 // 2 s + l / 32) and 16x16x32 (row l % 16, chunk 4 s + l / 16). 64-byte rows (32x32x16 only)
 // take f(r) = ((r >> 2) ^ (r >> 1)) & 3.
 template <int CPR>
-__device__ __forceinline__ int swz_phase(int row) {
+__host__ __device__ __forceinline__ int swz_phase(int row) {
   static_assert(CPR == 4 || CPR == 8, "64- or 128-byte staged rows");
   return CPR == 8 ? ((row >> 1) & 7) : (((row >> 2) ^ (row >> 1)) & 3);
 }
 template <int CPR>
-__device__ __forceinline__ int swz(int row, int chunk) {
+__host__ __device__ __forceinline__ int swz(int row, int chunk) {
   return row * CPR + (chunk ^ swz_phase<CPR>(row));
 }
 

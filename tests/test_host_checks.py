@@ -4,7 +4,10 @@ headers (CPU only: each check runs as a host program):
 - K1's tile order: xcd_tile and tile_coords take every tile of a launch exactly once, for every
   grid size up to 4096 blocks and for slab-major and blocked orders with ragged blocks;
 - the draft head's (logit, id) keys: their unsigned order is the pair order over special and
-  random float values and ids, and they decode to the pair."""
+  random float values and ids, and they decode to the pair;
+- the LDS swizzle: under the measured ds_read_b128 pass model every fragment read of every K1
+  and K5 tile family puts the 16 lanes of each pass on 16 distinct bank groups (no conflict
+  cycles)."""
 import os
 import shutil
 import subprocess
@@ -37,3 +40,7 @@ def test_tile_order_is_one_to_one(tmp_path):
 
 def test_draft_keys_order_pairs(tmp_path):
     _run_host_check(tmp_path, "draft_key_check")
+
+
+def test_lds_swizzle_is_conflict_free(tmp_path):
+    _run_host_check(tmp_path, "lds_swizzle_check")
