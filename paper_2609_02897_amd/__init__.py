@@ -163,6 +163,14 @@ def _need(t, name, dtype, shape):
         raise ValueError(f"{name}: must be contiguous")
 
 
+def _same_device(device, **tensors):
+    """Every given tensor (None skipped) on `device`: the kernels run on one GPU and take raw
+    pointers, so an input on another GPU would be read through a foreign address."""
+    for name, t in tensors.items():
+        if t is not None and t.device != device:
+            raise ValueError(f"{name}: on {t.device}, the hidden states are on {device}")
+
+
 class PackedLmHead(NamedTuple):
     """An LM-head weight in a packed tile layout: ``kind`` "target" (``asv_pack_lm_head``,
     [256 rows][64 columns] tiles, for ``verify``) or "draft" (``asv_pack_draft_head``, [64][64]
@@ -254,6 +262,9 @@ def verify(hidden, w_lm, draft_tok, parent, req_offsets, tau, draft_logits=None,
     if state is not None:
         _need(state, "state", torch.uint8, (B, STATE_BYTES))
     dev = hidden.device
+    _same_device(dev, w_lm=w_lm.data if isinstance(w_lm, PackedLmHead) else w_lm,
+                 draft_tok=draft_tok, parent=parent, req_offsets=req_offsets, tau=tau,
+                 draft_logits=draft_logits, state=state)
     if out is None:
         out = alloc_outputs(B, N, dev, draft_logits is not None)
     else:
@@ -365,6 +376,8 @@ def draft_step(hidden, w_draft, trees, step: int, state=None, shape=None, vocab_
     if state is not None:
         _need(state, "state", torch.uint8, (B, STATE_BYTES))
     dev = hidden.device
+    _same_device(dev, w_draft=w_draft.data if isinstance(w_draft, PackedLmHead) else w_draft,
+                 trees=trees, vocab_map=vocab_map, state=state)
     if out is None:
         out = DraftOut(torch.empty((R, TOPK_MAX), dtype=torch.int32, device=dev),
                        torch.empty((R, TOPK_MAX), dtype=torch.float32, device=dev),

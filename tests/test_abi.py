@@ -315,3 +315,15 @@ def test_draft_and_tree_entry_points_reject_on_host(lib):
     assert lib.asv_commit(ctypes.byref(c), None) == asv.ASV_EINVAL
     c.row_dst, c.row_src = fake, fake + 2                                           # misaligned
     assert lib.asv_commit(ctypes.byref(c), None) == asv.ASV_EINVAL
+
+
+def test_inputs_on_another_device_are_rejected():
+    """The binding refuses inputs that sit on another device than the hidden states (the
+    kernels would read them through a foreign address); None entries are skipped."""
+    torch = pytest.importorskip("torch")
+    dev = torch.device("cuda", 0)
+    with pytest.raises(ValueError, match="w_lm"):
+        asv._same_device(dev, w_lm=torch.empty(2, device="meta"))
+    with pytest.raises(ValueError, match="tau"):
+        asv._same_device(dev, parent=None, tau=torch.empty(2, device="meta"))
+    asv._same_device(dev, state=None)
